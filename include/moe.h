@@ -1,0 +1,203 @@
+/*
+ * moe.h - C ABI of libmoe: one GPU's share of an expert-parallel MoE layer on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * ViBE (arXiv 2606.00735) balances per-GPU execution time of expert-parallel
+ * MoE layers. What it balances is the work of this library: each GPU gates its
+ * tokens, builds the per-expert token histogram (one row of the activation
+ * matrix W, Section 4.2.2), runs its local experts on the tokens routed to them
+ * (its token load n_g = sum of w_e over its experts S_g, Section 4.2.3) and
+ * combines the results; the latency of that expert computation as a function
+ * of the token load is the per-GPU performance model f_g(n) (Section 4.2.1,
+ * Algorithm 1 Phase 1).
+ *
+ * Conventions shared by every entry point:
+ *  - Array arguments are caller-owned DEVICE pointers unless marked "host".
+ *    The library allocates no device memory and keeps no device state.
+ *  - Matrices are row-major and dense. Weight matrices are stored
+ *    out-features by in-features (the nn.Linear layout): row n of a matrix
+ *    holds the input weights of output n, so every contraction reads its
+ *    operands along contiguous rows.
+ *  - bf16 data is IEEE bfloat16 (2 bytes); MOE_F32 data is IEEE binary32.
+ *    Gate logits and weights are always fp32.
+ *  - Calls are stream-ordered and asynchronous (except moe_load_sweep) and
+ *    launch only on `stream`. Pointers must be 16-byte aligned.
+ *  - Workspace: call with ws == NULL to receive the byte count in *ws_bytes
+ *    (returns MOE_OK, launches nothing). With ws != NULL, *ws_bytes must be at
+ *    least that count, else MOE_ERR_WORKSPACE.
+ *  - Errors: every call returns a moe_status and never aborts. Arguments are
+ *    validated on the host before anything is launched; launch failures are
+ *    reported as MOE_ERR_HIP (hipGetLastError after each launch). Device
+ *    data the host cannot see (ids, offsets, dest) is clamped inside the
+ *    kernels so that no access leaves its buffer.
+ *  - Thread safety: calls with distinct workspaces and streams are
+ *    independent.
+ */
+#ifndef MOE_SHARD_MOE_H
+#define MOE_SHARD_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+#define MOE_MAX_EXPERTS 256 /* E and E_local limit */
+#define MOE_MAX_TOPK 16
+
+typedef enum moe_status {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, k > E, misaligned */
+  MOE_ERR_UNSUPPORTED = 2, /* valid but outside what the kernels handle */
+  MOE_ERR_WORKSPACE = 3,   /* workspace smaller than the queried size */
+  MOE_ERR_HIP = 4          /* a HIP launch or runtime call failed */
+} moe_status;
+
+typedef enum moe_dtype { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
+
+/* Short text for a status code (static storage, never NULL). */
+const char* moe_status_string(moe_status s);
+
+/* MOE_ABI_VERSION of the built library. */
+int moe_abi_version(void);
+
+/*
+ * moe_gate_topk - router logits, top-k selection and renormalised gate weights.
+ *
+ * Section 2 (Mixture-of-Experts and Expert Parallelism): each token is routed
+ * to a subset of experts. For token t:
+ *   z[t,e]  = fl32( fl32(sum_h x[t,h] * w_router[e,h]) + bias[e] )
+ *   ids[t,:] = the k experts with the largest z, ordered by (z descending,
+ *              expert id ascending): equal logits go to the lower expert id
+ *   w[t,j]  = exp(z_j - z_0) / sum_{j'<k} exp(z_j' - z_0)  (fp32, j ascending)
+ *
+ * x          [T, H]  dt          token activations
+ * w_router   [E, H]  dt          row e = routing vector of expert e
+ * bias       [E]     fp32        per-expert logit bias (may be NULL = 0)
+ * logits_out [T, E]  fp32        optional (NULL to skip): z
+ * topk_ids   [T, k]  int32       selected expert ids
+ * topk_w     [T, k]  fp32        gate weights
+ * Limits: 1 <= E <= 256, 1 <= k <= min(E, 16), H % 8 == 0 (bf16: H % 64 == 0).
+ * T == 0 is a no-op. The kernel accumulates in fp32; inputs whose products
+ * and partial sums are exact in fp32 give order-independent logits.
+ */
+moe_status moe_gate_topk(const void* x, const void* w_router, const float* bias,
+                         int T, int H, int E, int k, moe_dtype dt,
+                         float* logits_out, int32_t* topk_ids, float* topk_w,
+                         hipStream_t stream);
+
+/*
+ * moe_expert_histogram_scan - the activation profile and local offsets.
+ *
+ * counts[e] = #{(t,j) : topk_ids[t,j] == e} for all E experts (one row of the
+ * activation matrix W of Section 4.2.2). expert_map (HOST array [E]) gives
+ * the local slot of each expert on this GPU, or -1 for a remote expert; the
+ * local slots must be exactly 0..E_local-1, each used once (the placement
+ * S_g of Section 4.2.3). offsets[0] = 0 and offsets[l+1] = offsets[l] +
+ * counts[expert in slot l]; offsets[E_local] is the GPU's token load.
+ *
+ * counts  [E]          int32 (device, written)
+ * offsets [E_local+1]  int32 (device, written)
+ * ws      per-block count table and per-block row bases; pass it unchanged
+ *         to moe_permute. Size depends on T, E and E_local only.
+ * Limits: 1 <= E <= 256, 0 <= E_local <= E, 1 <= k <= min(E, 16). Expert ids
+ * outside [0, E) in topk_ids are ignored.
+ */
+moe_status moe_expert_histogram_scan(const int32_t* topk_ids, int T, int k, int E,
+                                     const int32_t* expert_map, int E_local,
+                                     int32_t* counts, int32_t* offsets,
+                                     void* ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
+ * moe_permute - dispatch: a stable counting sort of assignments by local slot.
+ *
+ * For flat assignment i = t*k + j in ascending order, if its expert is local
+ * (slot l), it gets row pos = offsets[l] + (number of earlier assignments to
+ * slot l): perm_src[pos] = i, dest[i] = pos and x_perm[pos,:] = x[t,:].
+ * Remote assignments get dest[i] = -1. Under expert parallelism x_perm is the
+ * send buffer of the dispatch all-to-all (Section 2).
+ *
+ * ws, ws_bytes  the workspace filled by moe_expert_histogram_scan (same T, k,
+ *               E, E_local); expert_map is the same HOST array.
+ * x_perm   [M_cap, H] dt   rows [0, offsets[E_local]) written
+ * perm_src [M_cap]    int32 entries [0, offsets[E_local]) written
+ * dest     [T*k]      int32 all written
+ * Requires M_cap >= T*k (the worst case, so no host sync is needed).
+ */
+moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* expert_map,
+                       const void* ws, size_t ws_bytes, int T, int H, int k, int E,
+                       int E_local, int M_cap, moe_dtype dt, void* x_perm,
+                       int32_t* perm_src, int32_t* dest, hipStream_t stream);
+
+/*
+ * moe_grouped_swiglu_ffn - every local expert on its rows of x_perm.
+ *
+ * For local slot l and rows R = [offsets[l], offsets[l+1]):
+ *   G = x_perm[R] W_gate[l]^T, U = x_perm[R] W_up[l]^T   (fp32 accumulation)
+ *   h = round_dt( silu(G) * U ),  silu(g) = g / (1 + exp(-g))   (fp32)
+ *   y_perm[R] = round_dt( h W_down[l]^T )                  (fp32 accumulation)
+ * This is the expert computation whose latency per token load is f_g(n)
+ * (Section 4.2.1). Experts with no rows cost nothing and are not read.
+ *
+ * w_gate, w_up [E_local, I, H] dt; w_down [E_local, H, I] dt
+ * offsets      [E_local+1] int32 (device, from moe_expert_histogram_scan);
+ *              clamped to [0, M_cap] inside the kernels
+ * y_perm       [M_cap, H] dt, rows [0, offsets[E_local]) written
+ * ws           holds h [M_cap, I] dt
+ * Limits: 0 <= E_local <= 256 (0 is a no-op); bf16: H % 128 == 0 and
+ * I % 128 == 0; fp32: H % 4 == 0 and I % 4 == 0.
+ */
+moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const void* w_up,
+                                  const void* w_down, const int32_t* offsets, int E_local,
+                                  int H, int I, int M_cap, moe_dtype dt, void* y_perm,
+                                  void* ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
+ * moe_unpermute_combine - gather and weighted sum back to token order.
+ *
+ * out[t,:] = round_dt( sum over j ascending with dest[t*k+j] >= 0 of
+ *            topk_w[t,j] * y_perm[dest[t*k+j],:] ), fp32 accumulator.
+ * Tokens with no local assignment get an exactly zero row, so summing the
+ * partial outputs of all GPUs of an expert-parallel group gives the layer
+ * output (the combine all-to-all of Section 2). dest entries outside
+ * [0, M_cap) are treated as -1.
+ *
+ * out [T, H] dt (written completely).
+ */
+moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const int32_t* dest,
+                                 int T, int k, int H, int M_cap, moe_dtype dt, void* out,
+                                 hipStream_t stream);
+
+/*
+ * moe_load_sweep - per-expert latency versus token load.
+ *
+ * Algorithm 1 Phase 1 / Section 4.2.1: profile the expert computation over a
+ * range of token counts to obtain f_g(n). For each M = Ms[i] (HOST array),
+ * runs moe_grouped_swiglu_ffn on one expert with offsets [0, M]: `warmup`
+ * untimed runs, then `iters` runs each bracketed by HIP events on `stream`.
+ * Successive runs rotate through n_rot copies of the expert's weights so
+ * that the 256 MB last-level cache does not hold them between runs.
+ *
+ * x        [maxM, H] dt        input rows (maxM = max of Ms)
+ * w_gate, w_up [n_rot, I, H]; w_down [n_rot, H, I]   dt
+ * y_scratch [maxM, H] dt       output rows (contents unspecified afterwards)
+ * ws       workspace for maxM (query with ws == NULL)
+ * us_out   HOST [nM]: median microseconds per run
+ * us_all   HOST [nM * iters] or NULL: every timed run, in order
+ * Blocks the calling thread until the sweep is done. Limits: 1 <= nM <= 64,
+ * 1 <= Ms[i] <= 1 << 20, 0 <= warmup, 1 <= iters <= 10000, n_rot >= 1.
+ */
+moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up,
+                          const void* w_down, int n_rot, int H, int I, moe_dtype dt,
+                          const int32_t* Ms, int nM, int warmup, int iters,
+                          void* y_scratch, void* ws, size_t* ws_bytes,
+                          float* us_out, float* us_all, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_SHARD_MOE_H */

@@ -1,0 +1,25 @@
+"""One GPU's share of an expert-parallel MoE layer on MI355X (gfx950).
+
+The computation ViBE (arXiv 2606.00735) balances across GPUs: top-k gating,
+the per-expert activation profile, dispatch permutation, grouped SwiGLU
+expert FFN, weighted combine, and the per-expert latency-vs-load sweep from
+which the per-GPU performance model f_g(n) is fitted. Every step runs in the
+HIP kernels of ``libmoe.so`` (C ABI in ``include/moe.h``); this package only
+marshals torch tensors into those calls.
+"""
+from ._lib import (  # noqa: F401
+    EXPORTED,
+    LIB_PATH,
+    MoeError,
+    ffn_hidden,
+    ffn_ws_bytes,
+    hist_ws_bytes,
+    load_library,
+    moe_expert_histogram_scan,
+    moe_gate_topk,
+    moe_grouped_swiglu_ffn,
+    moe_layer,
+    moe_load_sweep,
+    moe_permute,
+    moe_unpermute_combine,
+)

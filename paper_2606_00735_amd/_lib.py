@@ -1,0 +1,295 @@
+"""ctypes binding of libmoe (include/moe.h): argument marshalling only.
+
+Every function takes torch tensors that live on the GPU, checks dtype, shape
+and contiguity, allocates missing outputs with torch (device memory only) and
+calls the C entry point of the same name on torch's current stream. There is
+no CPU path: if libmoe.so is missing or a tensor is not on the GPU, the call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_F32, MOE_BF16 = 0, 1
+MAX_EXPERTS, MAX_TOPK = 256, 16
+
+EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert_histogram_scan",
+            "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep")
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn, status, text):
+        super().__init__(f"{fn} failed: status {status} ({text})")
+        self.status = status
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+_PSZ = ctypes.POINTER(ctypes.c_size_t)
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libmoe.so (built in-tree by ``paper_2606_00735_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run `python -m paper_2606_00735_amd.build`")
+    L = ctypes.CDLL(path)
+    L.moe_status_string.restype = ctypes.c_char_p
+    L.moe_status_string.argtypes = [_I]
+    L.moe_abi_version.restype = _I
+    L.moe_abi_version.argtypes = []
+    L.moe_gate_topk.restype = _I
+    L.moe_gate_topk.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P]
+    L.moe_expert_histogram_scan.restype = _I
+    L.moe_expert_histogram_scan.argtypes = [_P, _I, _I, _I, _P, _I, _P, _P, _P, _PSZ, _P]
+    L.moe_permute.restype = _I
+    L.moe_permute.argtypes = [_P, _P, _P, _P, _SZ, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]
+    L.moe_grouped_swiglu_ffn.restype = _I
+    L.moe_grouped_swiglu_ffn.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _PSZ, _P]
+    L.moe_unpermute_combine.restype = _I
+    L.moe_unpermute_combine.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P]
+    L.moe_load_sweep.restype = _I
+    L.moe_load_sweep.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P, _P]
+    if L.moe_abi_version() != 1:
+        raise RuntimeError("libmoe ABI version mismatch")
+    _lib = L
+    return L
+
+
+def _check(fn, status):
+    if status != MOE_OK:
+        text = load_library().moe_status_string(status).decode()
+        raise MoeError(fn, status, text)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, name, dtype=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU (libmoe has no CPU path)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype == torch.float32:
+        return MOE_F32
+    raise ValueError(f"unsupported dtype {t.dtype}: bf16 or fp32")
+
+
+def _host_map(expert_map):
+    a = np.ascontiguousarray(np.asarray(expert_map, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _ptr_or_null(t, name, dtype=None):
+    return ctypes.c_void_p(None) if t is None else _dev(t, name, dtype)
+
+
+# ---------------------------------------------------------------------------
+# The six entry points
+# ---------------------------------------------------------------------------
+def moe_gate_topk(x, w_router, bias, k, logits=False, ids=None, weights=None):
+    """Top-k gating. Returns (ids [T,k] int32, weights [T,k] fp32, logits [T,E] or None)."""
+    L = load_library()
+    T, H = x.shape
+    E = w_router.shape[0]
+    dt = _dtype_code(x)
+    if w_router.dtype != x.dtype or tuple(w_router.shape) != (E, H):
+        raise ValueError("w_router must be [E, H] with the dtype of x")
+    dev = x.device
+    ids = torch.empty((T, k), dtype=torch.int32, device=dev) if ids is None else ids
+    weights = torch.empty((T, k), dtype=torch.float32, device=dev) if weights is None else weights
+    lg = torch.empty((T, E), dtype=torch.float32, device=dev) if logits is True else (
+        logits if isinstance(logits, torch.Tensor) else None)
+    st = L.moe_gate_topk(_dev(x, "x"), _dev(w_router, "w_router"), _ptr_or_null(bias, "bias", torch.float32),
+                         T, H, E, k, dt, _ptr_or_null(lg, "logits", torch.float32),
+                         _dev(ids, "ids", torch.int32), _dev(weights, "weights", torch.float32), _stream())
+    _check("moe_gate_topk", st)
+    return ids, weights, lg
+
+
+def hist_ws_bytes(T, k, E, expert_map_len_local):
+    L = load_library()
+    n = ctypes.c_size_t(0)
+    st = L.moe_expert_histogram_scan(None, T, k, E, None, expert_map_len_local, None, None, None,
+                                     ctypes.byref(n), None)
+    _check("moe_expert_histogram_scan", st)
+    return n.value
+
+
+def moe_expert_histogram_scan(ids, E, expert_map, ws=None, counts=None, offsets=None):
+    """Activation profile. Returns (counts [E], offsets [E_local+1], ws)."""
+    L = load_library()
+    T, k = ids.shape
+    emap, emap_p = _host_map(expert_map)
+    if emap.shape != (E,):
+        raise ValueError("expert_map must have E entries")
+    E_local = int((emap >= 0).sum())
+    need = hist_ws_bytes(T, k, E, E_local)
+    dev = ids.device
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    counts = torch.empty(E, dtype=torch.int32, device=dev) if counts is None else counts
+    offsets = torch.empty(E_local + 1, dtype=torch.int32, device=dev) if offsets is None else offsets
+    n = ctypes.c_size_t(ws.numel() * ws.element_size())
+    st = L.moe_expert_histogram_scan(_dev(ids, "ids", torch.int32), T, k, E, emap_p, E_local,
+                                     _dev(counts, "counts", torch.int32), _dev(offsets, "offsets", torch.int32),
+                                     _dev(ws, "ws"), ctypes.byref(n), _stream())
+    _check("moe_expert_histogram_scan", st)
+    return counts, offsets, ws
+
+
+def moe_permute(x, ids, expert_map, ws, M_cap=None, x_perm=None, perm_src=None, dest=None):
+    """Dispatch. Returns (x_perm [M_cap,H], perm_src [M_cap], dest [T*k])."""
+    L = load_library()
+    T, H = x.shape
+    k = ids.shape[1]
+    emap, emap_p = _host_map(expert_map)
+    E = emap.shape[0]
+    E_local = int((emap >= 0).sum())
+    M_cap = T * k if M_cap is None else M_cap
+    dev = x.device
+    x_perm = torch.empty((M_cap, H), dtype=x.dtype, device=dev) if x_perm is None else x_perm
+    perm_src = torch.empty(M_cap, dtype=torch.int32, device=dev) if perm_src is None else perm_src
+    dest = torch.empty(T * k, dtype=torch.int32, device=dev) if dest is None else dest
+    st = L.moe_permute(_dev(x, "x"), _dev(ids, "ids", torch.int32), emap_p, _dev(ws, "ws"),
+                       ws.numel() * ws.element_size(), T, H, k, E, E_local, M_cap, _dtype_code(x),
+                       _dev(x_perm, "x_perm", x.dtype), _dev(perm_src, "perm_src", torch.int32),
+                       _dev(dest, "dest", torch.int32), _stream())
+    _check("moe_permute", st)
+    return x_perm, perm_src, dest
+
+
+def ffn_ws_bytes(E_local, H, I, M_cap, dtype):
+    L = load_library()
+    n = ctypes.c_size_t(0)
+    dt = MOE_BF16 if dtype == torch.bfloat16 else MOE_F32
+    st = L.moe_grouped_swiglu_ffn(None, None, None, None, None, E_local, H, I, M_cap, dt, None, None,
+                                  ctypes.byref(n), None)
+    _check("moe_grouped_swiglu_ffn", st)
+    return n.value
+
+
+def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):
+    """Grouped SwiGLU FFN over local experts. Returns (y_perm [M_cap,H], ws)."""
+    L = load_library()
+    M_cap, H = x_perm.shape
+    E_local, I, H2 = w_gate.shape
+    if H2 != H or tuple(w_up.shape) != (E_local, I, H) or tuple(w_down.shape) != (E_local, H, I):
+        raise ValueError("expert weights must be w_gate/w_up [E_local, I, H] and w_down [E_local, H, I]")
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    dt = _dtype_code(x_perm)
+    need = ffn_ws_bytes(E_local, H, I, M_cap, x_perm.dtype)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=x_perm.device)
+    y_perm = torch.empty((M_cap, H), dtype=x_perm.dtype, device=x_perm.device) if y_perm is None else y_perm
+    n = ctypes.c_size_t(ws.numel() * ws.element_size())
+    st = L.moe_grouped_swiglu_ffn(_dev(x_perm, "x_perm"), _dev(w_gate, "w_gate", x_perm.dtype),
+                                  _dev(w_up, "w_up", x_perm.dtype), _dev(w_down, "w_down", x_perm.dtype),
+                                  _dev(offsets, "offsets", torch.int32), E_local, H, I, M_cap, dt,
+                                  _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ctypes.byref(n),
+                                  _stream())
+    _check("moe_grouped_swiglu_ffn", st)
+    return y_perm, ws
+
+
+def moe_unpermute_combine(y_perm, weights, dest, T, out=None):
+    """Weighted combine back to token order. Returns out [T,H]."""
+    L = load_library()
+    M_cap, H = y_perm.shape
+    k = weights.shape[1]
+    out = torch.empty((T, H), dtype=y_perm.dtype, device=y_perm.device) if out is None else out
+    st = L.moe_unpermute_combine(_dev(y_perm, "y_perm"), _dev(weights, "weights", torch.float32),
+                                 _dev(dest, "dest", torch.int32), T, k, H, M_cap, _dtype_code(y_perm),
+                                 _dev(out, "out", y_perm.dtype), _stream())
+    _check("moe_unpermute_combine", st)
+    return out
+
+
+def moe_load_sweep(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=None, ws=None,
+                   keep_all=False):
+    """Per-expert latency vs token load. Returns (median_us [nM], all_us [nM,iters] or None)."""
+    L = load_library()
+    n_rot, I, H = w_gate.shape
+    Ms = np.ascontiguousarray(np.asarray(Ms, dtype=np.int32))
+    nM = len(Ms)
+    max_m = int(Ms.max())
+    if x.shape[0] < max_m or x.shape[1] != H:
+        raise ValueError("x must be [max(Ms), H]")
+    dt = _dtype_code(x)
+    n = ctypes.c_size_t(0)
+    st = L.moe_load_sweep(None, None, None, None, n_rot, H, I, dt, Ms.ctypes.data_as(ctypes.c_void_p), nM,
+                          warmup, iters, None, None, ctypes.byref(n), None, None, None)
+    _check("moe_load_sweep", st)
+    if ws is None:
+        ws = torch.empty(n.value, dtype=torch.uint8, device=x.device)
+    if y_scratch is None:
+        y_scratch = torch.empty((max_m, H), dtype=x.dtype, device=x.device)
+    us = np.zeros(nM, np.float32)
+    us_all = np.zeros((nM, iters), np.float32) if keep_all else None
+    n = ctypes.c_size_t(ws.numel())
+    st = L.moe_load_sweep(_dev(x, "x"), _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
+                          _dev(w_down, "w_down", x.dtype), n_rot, H, I, dt, Ms.ctypes.data_as(ctypes.c_void_p),
+                          nM, warmup, iters, _dev(y_scratch, "y_scratch", x.dtype), _dev(ws, "ws"),
+                          ctypes.byref(n), us.ctypes.data_as(ctypes.c_void_p),
+                          us_all.ctypes.data_as(ctypes.c_void_p) if keep_all else None, _stream())
+    _check("moe_load_sweep", st)
+    return us, us_all
+
+
+# ---------------------------------------------------------------------------
+# Whole layer: the five stream-ordered calls, no host synchronisation.
+# ---------------------------------------------------------------------------
+def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=False, bufs=None):
+    """One GPU's share of the MoE layer; returns a dict of every output.
+
+    ``bufs`` (optional dict) supplies preallocated outputs and workspaces so
+    that repeated calls allocate nothing.
+    """
+    b = {} if bufs is None else bufs
+    T = x.shape[0]
+    E = w_router.shape[0]
+    ids, wts, lg = moe_gate_topk(x, w_router, bias, k, logits=logits, ids=b.get("ids"),
+                                 weights=b.get("weights"))
+    counts, offsets, hws = moe_expert_histogram_scan(ids, E, expert_map, ws=b.get("hist_ws"),
+                                                     counts=b.get("counts"), offsets=b.get("offsets"))
+    x_perm, perm_src, dest = moe_permute(x, ids, expert_map, hws, x_perm=b.get("x_perm"),
+                                         perm_src=b.get("perm_src"), dest=b.get("dest"))
+    y_perm, fws = moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=b.get("ffn_ws"),
+                                         y_perm=b.get("y_perm"))
+    out = moe_unpermute_combine(y_perm, wts, dest, T, out=b.get("out"))
+    if bufs is not None:
+        bufs.update(ids=ids, weights=wts, hist_ws=hws, counts=counts, offsets=offsets, x_perm=x_perm,
+                    perm_src=perm_src, dest=dest, ffn_ws=fws, y_perm=y_perm, out=out)
+    return dict(ids=ids, weights=wts, logits=lg, counts=counts, offsets=offsets, x_perm=x_perm,
+                perm_src=perm_src, dest=dest, y_perm=y_perm, h=fws, out=out)
+
+
+def ffn_hidden(ws, M_cap, I, dtype):
+    """View of the expert hidden activations h [M_cap, I] held in an FFN workspace."""
+    es = 2 if dtype == torch.bfloat16 else 4
+    return ws[: M_cap * I * es].view(dtype).view(M_cap, I)

@@ -1,0 +1,96 @@
+// Device-side types and helpers shared by the libmoe kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef uint16_t bf16_t;  // raw IEEE bfloat16 bits
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+constexpr int kMaxExperts = 256;
+constexpr int kMaxTopk = 16;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// ---------------------------------------------------------------------------
+// Swizzled LDS tiles filled by direct global->LDS loads.
+//
+// A tile row holds 64 bf16 (128 B = 8 chunks of 16 B). Chunk c of row r is
+// stored at chunk position c ^ (r & 7), so the 32 rows read by one MFMA
+// operand load hit 8 different chunk positions (all 32 banks) per group of
+// 8 lanes, while each wave's load instruction still fills 1 KB (8 rows) of
+// LDS contiguously, as global_load_lds_dwordx4 requires (lane i writes bytes
+// [16 i, 16 i + 16) past the wave-uniform LDS address).
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ (row & 7); }
+
+// Loads rows [0, R) (64 bf16 each, starting at column `col0`) of a row-major
+// matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
+// `row_limit` re-read row `row_limit - 1` (their results are never stored),
+// so no load leaves the matrix. R must be a multiple of 32 (4 waves x 8 rows).
+template <int R>
+__device__ __forceinline__ void dma_rows(const bf16_t* __restrict__ src, size_t ld, int col0, int row_limit,
+                                         bf16_t* lds, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < R / 32; ++i) {
+    const int r0 = (i * 4 + wave) * 8;
+    const int r = r0 + (lane >> 3);
+    const int c = swz_chunk(r, lane & 7);
+    const int rr = r < row_limit ? r : row_limit - 1;
+    __builtin_amdgcn_global_load_lds(src + (size_t)rr * ld + col0 + c * 8, (lds_void_t*)(lds + r0 * 64), 16, 0,
+                                     0);
+  }
+}
+
+// 16-byte operand fragment: elements [8 * chunk, 8 * chunk + 8) of tile row `row`.
+__device__ __forceinline__ bf16x8_t lds_frag(const bf16_t* lds, int row, int chunk) {
+  return as_bf16x8(*reinterpret_cast<const uint4*>(lds + row * 64 + swz_chunk(row, chunk) * 8));
+}
+
+// s_waitcnt vmcnt(N) (gfx9 encoding; expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// (value, index) ordering of the router: larger value first, then lower index.
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+// Slot map of a shard, passed to kernels by value (kernel argument segment).
+struct SlotMap {
+  int32_t n_experts;                 // E
+  int32_t n_local;                   // E_local
+  int16_t slot_of[kMaxExperts];      // expert -> local slot or -1
+  int16_t expert_of[kMaxExperts];    // local slot -> expert
+};
+
+}  // namespace moe

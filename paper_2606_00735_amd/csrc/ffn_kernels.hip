@@ -1,0 +1,315 @@
+// Grouped SwiGLU expert FFN (gfx950): the expert computation whose latency
+// per token load is ViBE's per-GPU performance model f_g(n) (Section 4.2.1).
+//
+// Two persistent launches per call:
+//   gate/up:  h[R] = bf16( silu(X_R W_gate^T) * (X_R W_up^T) )   (dual GEMM)
+//   down:     y[R] = bf16( h[R] W_down^T )
+// for each local expert's row range R = [offsets[e], offsets[e+1]).
+//
+// Per-expert row counts live only on the device, so each block rebuilds the
+// tile list from `offsets` (a scan over at most 256 experts) and walks it
+// with a grid stride. An expert with M_e <= 32 rows gets 32-row tiles (its
+// cost is streaming its weights once); larger experts get 128-row tiles.
+// Within an expert, consecutive tile indices share a weight column block, so
+// blocks running at the same time read the same weights.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+
+constexpr int kBK = 64;            // K chunk per pipeline stage
+constexpr int kBN = 128;           // output columns per tile
+constexpr int kSmallM = 32;        // experts with at most this many rows use 32-row tiles
+
+struct GemmArgs {
+  const bf16_t* A;        // [M_cap, K]
+  const bf16_t* B0;       // [E_local, N, K]
+  const bf16_t* B1;       // [E_local, N, K] (dual only)
+  bf16_t* C;              // [M_cap, N]
+  const int32_t* offsets; // [E_local + 1]
+  int E_local, M_cap, N, K;
+};
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  const float sig = 1.0f / (1.0f + expf(-g));
+  return (g * sig) * u;
+}
+
+// One BM x 128 output tile (two of them, gate and up, when DUAL) over the
+// whole K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from
+// global memory into two swizzled LDS stages (loads of chunk k+1 overlap the
+// MFMAs on chunk k).
+constexpr int kARows = 128;  // A rows reserved per stage
+
+template <int BM, bool DUAL>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t* st1, int e, int m0, int m_end,
+                                          int n0) {
+  constexpr int NB = DUAL ? 2 : 1;
+  constexpr int WAVES_M = (BM == 128) ? 2 : 1;
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = kBN / WAVES_N;
+  constexpr int MI = WM / 32, NI = WN / 32;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int K = a.K, N = a.N;
+  const bf16_t* A = a.A + (size_t)m0 * K;
+  const int a_rows = m_end - m0;
+  const bf16_t* B0 = a.B0 + ((size_t)e * N + n0) * K;
+  const bf16_t* B1 = DUAL ? a.B1 + ((size_t)e * N + n0) * K : nullptr;
+
+  f32x16_t acc[NB][MI][NI];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
+
+  auto issue = [&](int kc, bf16_t* st) {
+    dma_rows<BM>(A, K, kc * kBK, a_rows, st, wave, lane);
+    dma_rows<kBN>(B0, K, kc * kBK, kBN, st + kARows * 64, wave, lane);
+    if (DUAL) dma_rows<kBN>(B1, K, kc * kBK, kBN, st + (kARows + kBN) * 64, wave, lane);
+  };
+  auto compute = [&](const bf16_t* st) {
+#pragma unroll
+    for (int s = 0; s < kBK / 16; ++s) {
+      const int chunk = 2 * s + (lane >> 5);
+      bf16x8_t af[MI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) af[i] = lds_frag(st, wm * WM + i * 32 + (lane & 31), chunk);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          const bf16x8_t bf = lds_frag(st + (kARows + b * kBN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf, acc[b][i][j], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  const int nK = K / kBK;
+  issue(0, st0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int kc = 0; kc < nK; ++kc) {
+    bf16_t* cur = (kc & 1) ? st1 : st0;
+    bf16_t* nxt = (kc & 1) ? st0 : st1;
+    if (kc + 1 < nK) issue(kc + 1, nxt);
+    compute(cur);
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  // Epilogue. 32x32 accumulator layout: register v of lane l is row
+  // 8 * (v / 4) + 4 * (l / 32) + (v % 4), column l % 32 of the MFMA block.
+#pragma unroll
+  for (int i = 0; i < MI; ++i)
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int col = n0 + wn * WN + j * 32 + (lane & 31);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        if (row < m_end) {
+          float r;
+          if (DUAL)
+            r = silu_mul(acc[0][i][j][v], acc[NB - 1][i][j][v]);
+          else
+            r = acc[0][i][j][v];
+          a.C[(size_t)row * N + col] = f32_to_bf16(r);
+        }
+      }
+    }
+}
+
+template <bool DUAL>
+__global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  constexpr int NB = DUAL ? 2 : 1;
+  constexpr int STAGE = (kARows + NB * kBN) * 64;
+  __shared__ __align__(16) bf16_t st0[STAGE];
+  __shared__ __align__(16) bf16_t st1[STAGE];
+  __shared__ int s_start[kMaxExperts + 1];
+  __shared__ int s_row0[kMaxExperts];
+  __shared__ int s_rows[kMaxExperts];
+  __shared__ int s_tot[4];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = a.E_local;
+  const int n_nt = a.N / kBN;
+
+  // Tile list: rows of each expert, clamped so no access leaves [0, M_cap).
+  int tiles = 0;
+  if (tid < E) {
+    int o0 = a.offsets[tid], o1 = a.offsets[tid + 1];
+    o0 = min(max(o0, 0), a.M_cap);
+    o1 = min(max(o1, o0), a.M_cap);
+    const int rows = o1 - o0;
+    s_row0[tid] = o0;
+    s_rows[tid] = rows;
+    const int bm = rows <= kSmallM ? kSmallM : 128;
+    tiles = ((rows + bm - 1) / bm) * n_nt;
+  }
+  // exclusive scan of tile counts over experts
+  int inc = tiles;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int n = __shfl_up(inc, off, kWave);
+    if (lane >= off) inc += n;
+  }
+  if (lane == 63) s_tot[wave] = inc;
+  __syncthreads();
+  int base = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) base += s_tot[w];
+    total += s_tot[w];
+  }
+  if (tid < E) s_start[tid] = base + inc - tiles;
+  __syncthreads();
+
+  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+    // last expert whose first tile is <= tile (experts with no tiles share
+    // their start with the next one, so the last match is the owner)
+    int lo = 0, hi = E - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_start[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    const int e = lo;
+    const int local = tile - s_start[e];
+    const int rows = s_rows[e];
+    const bool small = rows <= kSmallM;
+    const int bm = small ? kSmallM : 128;
+    const int n_mt = (rows + bm - 1) / bm;
+    const int nt = local / n_mt, mt = local % n_mt;
+    const int m0 = s_row0[e] + mt * bm;
+    const int m_end = min(m0 + bm, s_row0[e] + rows);
+    if (small)
+      gemm_tile<kSmallM, DUAL>(a, st0, st1, e, m0, m_end, nt * kBN);
+    else
+      gemm_tile<128, DUAL>(a, st0, st1, e, m0, m_end, nt * kBN);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 expert FFN: plain VALU dot products, one thread per output element.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int find_slot(const int32_t* offsets, int E, int M_cap, int row) {
+  for (int e = 0; e < E; ++e) {
+    const int o0 = min(max(offsets[e], 0), M_cap);
+    const int o1 = min(max(offsets[e + 1], o0), M_cap);
+    if (row >= o0 && row < o1) return e;
+  }
+  return -1;
+}
+
+__global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ X, const float* __restrict__ Wg,
+                                                         const float* __restrict__ Wu,
+                                                         const int32_t* __restrict__ offsets, int E, int M_cap,
+                                                         int H, int I, float* __restrict__ h) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (size_t)M_cap * I) return;
+  const int row = (int)(idx / I), i = (int)(idx % I);
+  const int e = find_slot(offsets, E, M_cap, row);
+  if (e < 0) return;
+  const float* x = X + (size_t)row * H;
+  const float* wg = Wg + ((size_t)e * I + i) * H;
+  const float* wu = Wu + ((size_t)e * I + i) * H;
+  float g = 0.0f, u = 0.0f;
+  for (int c = 0; c < H; ++c) {
+    g = __builtin_fmaf(x[c], wg[c], g);
+    u = __builtin_fmaf(x[c], wu[c], u);
+  }
+  h[(size_t)row * I + i] = silu_mul(g, u);
+}
+
+__global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ h, const float* __restrict__ Wd,
+                                                       const int32_t* __restrict__ offsets, int E, int M_cap, int H,
+                                                       int I, float* __restrict__ y) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (size_t)M_cap * H) return;
+  const int row = (int)(idx / H), c = (int)(idx % H);
+  const int e = find_slot(offsets, E, M_cap, row);
+  if (e < 0) return;
+  const float* hr = h + (size_t)row * I;
+  const float* wd = Wd + ((size_t)e * H + c) * I;
+  float s = 0.0f;
+  for (int i = 0; i < I; ++i) s = __builtin_fmaf(hr[i], wd[i], s);
+  y[(size_t)row * H + c] = s;
+}
+
+__global__ void set_offsets_kernel(int32_t* offsets, int m) {
+  if (threadIdx.x == 0) {
+    offsets[0] = 0;
+    offsets[1] = m;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+size_t ffn_ws_bytes(int M_cap, int I, bool bf16) {
+  const size_t h = (size_t)M_cap * I * (bf16 ? 2 : 4);
+  return ((h + 255) / 256) * 256 + 256;
+}
+
+static int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
+                      const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
+                      void* ws, hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  void* h = ws;
+  if (!bf16) {
+    const size_t n1 = (size_t)M_cap * I, n2 = (size_t)M_cap * H;
+    gateup_f32_kernel<<<(unsigned)((n1 + 255) / 256), 256, 0, s>>>(
+        static_cast<const float*>(x_perm), static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
+        offsets, E_local, M_cap, H, I, static_cast<float*>(h));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    down_f32_kernel<<<(unsigned)((n2 + 255) / 256), 256, 0, s>>>(static_cast<const float*>(h),
+                                                                  static_cast<const float*>(w_down), offsets,
+                                                                  E_local, M_cap, H, I,
+                                                                  static_cast<float*>(y_perm));
+    return hipGetLastError();
+  }
+  const int cus = device_cu_count();
+  // Upper bound on tiles: every expert could need one partial tile plus
+  // ceil(rows / 32) full ones.
+  auto grid_for = [&](int N, int per_cu) {
+    const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / kBN);
+    long long g = (long long)cus * per_cu;
+    if (ub < g) g = ub;
+    return (unsigned)(g < 1 ? 1 : g);
+  };
+  GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
+              static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H};
+  grouped_gemm_bf16_kernel<true><<<grid_for(I, 1), 256, 0, s>>>(g1);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
+              static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I};
+  grouped_gemm_bf16_kernel<false><<<grid_for(H, 2), 256, 0, s>>>(g2);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {
+  set_offsets_kernel<<<1, 64, 0, s>>>(offsets, m);
+  return hipGetLastError();
+}
+
+}  // namespace moe

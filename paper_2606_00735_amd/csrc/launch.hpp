@@ -1,0 +1,31 @@
+// Host-side launchers of the libmoe kernels. Arguments are validated by the
+// C ABI (moe_abi.cpp) before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace moe {
+
+hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, int T, int H, int E, int k,
+                            bool bf16, float* logits, int32_t* ids, float* wts, hipStream_t s);
+
+size_t hist_ws_bytes(int T, int E, int E_local);
+hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map, int32_t* counts,
+                            int32_t* offsets, void* ws, hipStream_t s);
+hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map, const void* ws, int T, int H,
+                          int k, int M_cap, bool bf16, void* x_perm, int32_t* perm_src, int32_t* dest,
+                          hipStream_t s);
+hipError_t launch_combine(const void* y, const float* w, const int32_t* dest, int T, int k, int H, int M_cap,
+                          bool bf16, void* out, hipStream_t s);
+
+size_t ffn_ws_bytes(int M_cap, int I, bool bf16);
+hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
+                      const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
+                      void* ws, hipStream_t s);
+hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,263 @@
+// C ABI of libmoe (declared in include/moe.h): argument validation on the
+// host, then stream-ordered kernel launches. Nothing here allocates device
+// memory; the load sweep creates HIP events only.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/moe.h"
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace {
+
+using moe::SlotMap;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool valid_dtype(moe_dtype dt) { return dt == MOE_F32 || dt == MOE_BF16; }
+
+moe_status hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_HIP; }
+
+// Validates a host expert map: entries in [-1, E_local), slots 0..E_local-1
+// each used exactly once.
+moe_status build_slot_map(const int32_t* expert_map, int E, int E_local, SlotMap* m) {
+  if (expert_map == nullptr) return MOE_ERR_INVALID_ARG;
+  if (E < 1 || E > MOE_MAX_EXPERTS || E_local < 0 || E_local > E) return MOE_ERR_INVALID_ARG;
+  m->n_experts = E;
+  m->n_local = E_local;
+  for (int i = 0; i < moe::kMaxExperts; ++i) {
+    m->slot_of[i] = -1;
+    m->expert_of[i] = -1;
+  }
+  for (int e = 0; e < E; ++e) {
+    const int s = expert_map[e];
+    if (s < -1 || s >= E_local) return MOE_ERR_INVALID_ARG;
+    if (s >= 0) {
+      if (m->expert_of[s] != -1) return MOE_ERR_INVALID_ARG;  // slot used twice
+      m->expert_of[s] = static_cast<int16_t>(e);
+      m->slot_of[e] = static_cast<int16_t>(s);
+    }
+  }
+  for (int s = 0; s < E_local; ++s)
+    if (m->expert_of[s] == -1) return MOE_ERR_INVALID_ARG;  // slot unused
+  return MOE_OK;
+}
+
+moe_status check_tk(int T, int k, int E) {
+  if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS) return MOE_ERR_INVALID_ARG;
+  if (k < 1 || k > E || k > MOE_MAX_TOPK) return MOE_ERR_INVALID_ARG;
+  if ((long long)T * k > INT_MAX) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+moe_status ffn_shape_ok(int E_local, int H, int I, int M_cap, moe_dtype dt) {
+  if (!valid_dtype(dt) || E_local < 0 || H < 1 || I < 1 || M_cap < 0) return MOE_ERR_INVALID_ARG;
+  if (E_local > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
+  if (dt == MOE_BF16 && (H % 128 != 0 || I % 128 != 0)) return MOE_ERR_UNSUPPORTED;
+  if (dt == MOE_F32 && (H % 4 != 0 || I % 4 != 0)) return MOE_ERR_UNSUPPORTED;
+  // the fp32 kernels use one thread per output element
+  if (dt == MOE_F32 && (long long)M_cap * std::max(H, I) > (long long)INT_MAX) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_status_string(moe_status s) {
+  switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported shape or option";
+    case MOE_ERR_WORKSPACE: return "workspace too small";
+    case MOE_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+moe_status moe_gate_topk(const void* x, const void* w_router, const float* bias, int T, int H, int E, int k,
+                         moe_dtype dt, float* logits_out, int32_t* topk_ids, float* topk_w,
+                         hipStream_t stream) {
+  moe_status st = check_tk(T, k, E);
+  if (st != MOE_OK) return st;
+  if (!valid_dtype(dt) || H < 1 || H % 8 != 0) return MOE_ERR_INVALID_ARG;
+  if (dt == MOE_BF16 && H % 64 != 0) return MOE_ERR_UNSUPPORTED;
+  if (T == 0) return MOE_OK;
+  if (!x || !w_router || !topk_ids || !topk_w) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(w_router) || !aligned4(topk_ids) || !aligned4(topk_w) ||
+      (bias && !aligned4(bias)) || (logits_out && !aligned4(logits_out)))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_gate_topk(x, w_router, bias, T, H, E, k, dt == MOE_BF16, logits_out, topk_ids,
+                                          topk_w, stream));
+}
+
+moe_status moe_expert_histogram_scan(const int32_t* topk_ids, int T, int k, int E, const int32_t* expert_map,
+                                     int E_local, int32_t* counts, int32_t* offsets, void* ws,
+                                     size_t* ws_bytes, hipStream_t stream) {
+  moe_status st = check_tk(T, k, E);
+  if (st != MOE_OK) return st;
+  if (E_local < 0 || E_local > E || ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
+  const size_t need = moe::hist_ws_bytes(T, E, E_local);
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  SlotMap map;
+  st = build_slot_map(expert_map, E, E_local, &map);
+  if (st != MOE_OK) return st;
+  if (!counts || !offsets || (T > 0 && !topk_ids)) return MOE_ERR_INVALID_ARG;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned16(ws) || (topk_ids && !aligned4(topk_ids)))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_hist_scan(topk_ids, T, k, map, counts, offsets, ws, stream));
+}
+
+moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* expert_map, const void* ws,
+                       size_t ws_bytes, int T, int H, int k, int E, int E_local, int M_cap, moe_dtype dt,
+                       void* x_perm, int32_t* perm_src, int32_t* dest, hipStream_t stream) {
+  moe_status st = check_tk(T, k, E);
+  if (st != MOE_OK) return st;
+  if (!valid_dtype(dt) || H < 1 || H % 8 != 0 || E_local < 0 || E_local > E) return MOE_ERR_INVALID_ARG;
+  if (M_cap < 0 || (long long)M_cap < (long long)T * k) return MOE_ERR_INVALID_ARG;
+  SlotMap map;
+  st = build_slot_map(expert_map, E, E_local, &map);
+  if (st != MOE_OK) return st;
+  if (ws == nullptr) return MOE_ERR_INVALID_ARG;
+  if (ws_bytes < moe::hist_ws_bytes(T, E, E_local)) return MOE_ERR_WORKSPACE;
+  if (T == 0) return MOE_OK;
+  if (!x || !topk_ids || !dest || (M_cap > 0 && (!x_perm || !perm_src))) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(ws) || (x_perm && !aligned16(x_perm)) || !aligned4(topk_ids) ||
+      !aligned4(dest) || (perm_src && !aligned4(perm_src)))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_permute(x, topk_ids, map, ws, T, H, k, M_cap, dt == MOE_BF16, x_perm, perm_src,
+                                        dest, stream));
+}
+
+moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
+                                  const int32_t* offsets, int E_local, int H, int I, int M_cap, moe_dtype dt,
+                                  void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream) {
+  moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
+  if (st != MOE_OK) return st;
+  if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
+  const size_t need = moe::ffn_ws_bytes(M_cap, I, dt == MOE_BF16);
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!x_perm || !w_gate || !w_up || !w_down || !offsets || !y_perm) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x_perm) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_perm) ||
+      !aligned16(ws) || !aligned4(offsets))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_ffn(x_perm, w_gate, w_up, w_down, offsets, E_local, H, I, M_cap,
+                                    dt == MOE_BF16, y_perm, ws, stream));
+}
+
+moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const int32_t* dest, int T, int k,
+                                 int H, int M_cap, moe_dtype dt, void* out, hipStream_t stream) {
+  if (T < 0 || k < 1 || k > MOE_MAX_TOPK || H < 1 || M_cap < 0 || !valid_dtype(dt)) return MOE_ERR_INVALID_ARG;
+  if ((long long)T * k > INT_MAX) return MOE_ERR_UNSUPPORTED;
+  if (H % (dt == MOE_BF16 ? 8 : 4) != 0) return MOE_ERR_INVALID_ARG;
+  if (T == 0) return MOE_OK;
+  if (!topk_w || !dest || !out || (M_cap > 0 && !y_perm)) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(out) || (y_perm && !aligned16(y_perm)) || !aligned4(topk_w) || !aligned4(dest))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_combine(y_perm, topk_w, dest, T, k, H, M_cap, dt == MOE_BF16, out, stream));
+}
+
+moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, const void* w_down, int n_rot,
+                          int H, int I, moe_dtype dt, const int32_t* Ms, int nM, int warmup, int iters,
+                          void* y_scratch, void* ws, size_t* ws_bytes, float* us_out, float* us_all,
+                          hipStream_t stream) {
+  if (Ms == nullptr || nM < 1 || nM > 64 || warmup < 0 || iters < 1 || iters > 10000 || n_rot < 1 ||
+      ws_bytes == nullptr)
+    return MOE_ERR_INVALID_ARG;
+  int max_m = 0;
+  for (int i = 0; i < nM; ++i) {
+    if (Ms[i] < 1 || Ms[i] > (1 << 20)) return MOE_ERR_INVALID_ARG;
+    max_m = std::max(max_m, Ms[i]);
+  }
+  moe_status st = ffn_shape_ok(1, H, I, max_m, dt);
+  if (st != MOE_OK) return st;
+  const bool bf16 = dt == MOE_BF16;
+  const size_t ffn_ws = moe::ffn_ws_bytes(max_m, I, bf16);
+  const size_t need = ffn_ws + 256;
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (!x || !w_gate || !w_up || !w_down || !y_scratch || !us_out) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_scratch) ||
+      !aligned16(ws))
+    return MOE_ERR_INVALID_ARG;
+
+  const size_t es = bf16 ? 2 : 4;
+  const size_t wmat = (size_t)H * I * es;  // bytes of one expert matrix
+  int32_t* offsets = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + ffn_ws);
+  std::vector<hipEvent_t> ev(2 * (size_t)iters, nullptr);
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto& d : ev)
+        if (d) (void)hipEventDestroy(d);
+      return MOE_ERR_HIP;
+    }
+  std::vector<float> t(iters);
+  moe_status result = MOE_OK;
+  int rot = 0;
+  for (int mi = 0; mi < nM && result == MOE_OK; ++mi) {
+    const int m = Ms[mi];
+    if (moe::launch_set_offsets(offsets, m, stream) != hipSuccess) {
+      result = MOE_ERR_HIP;
+      break;
+    }
+    for (int it = 0; it < warmup + iters; ++it) {
+      const char* g = static_cast<const char*>(w_gate) + (size_t)rot * wmat;
+      const char* u = static_cast<const char*>(w_up) + (size_t)rot * wmat;
+      const char* d = static_cast<const char*>(w_down) + (size_t)rot * wmat;
+      rot = (rot + 1) % n_rot;
+      const int ti = it - warmup;
+      if (ti >= 0 && hipEventRecord(ev[2 * ti], stream) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      if (moe::launch_ffn(x, g, u, d, offsets, 1, H, I, m, bf16, y_scratch, ws, stream) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      if (ti >= 0 && hipEventRecord(ev[2 * ti + 1], stream) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+    }
+    if (result != MOE_OK) break;
+    if (hipEventSynchronize(ev[2 * iters - 1]) != hipSuccess) {
+      result = MOE_ERR_HIP;
+      break;
+    }
+    for (int i = 0; i < iters; ++i) {
+      float ms = 0.0f;
+      if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      t[i] = ms * 1000.0f;
+      if (us_all) us_all[(size_t)mi * iters + i] = t[i];
+    }
+    std::vector<float> sorted(t);
+    std::sort(sorted.begin(), sorted.end());
+    us_out[mi] = (iters % 2) ? sorted[iters / 2] : 0.5f * (sorted[iters / 2 - 1] + sorted[iters / 2]);
+  }
+  if (result != MOE_OK) (void)hipStreamSynchronize(stream);
+  for (auto& e : ev) (void)hipEventDestroy(e);
+  return result;
+}
+
+}  // extern "C"

@@ -1,0 +1,540 @@
+// Gating, activation profile, dispatch permutation and combine kernels (gfx950).
+//
+// The routed MoE layer of ViBE's Section 2: tokens pick k experts each; this
+// GPU counts the picks per expert (the activation profile, Section 4.2.2),
+// gathers the rows routed to its local experts (its token load, Section 4.2.3)
+// and, after the expert FFN, scatters the weighted results back.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+
+// ---------------------------------------------------------------------------
+// Block-wide helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    int n = __shfl_up(v, off, kWave);
+    if (lane >= off) v += n;
+  }
+  return v;
+}
+
+// Exclusive scan of one int per thread over a 256-thread block.
+__device__ __forceinline__ int block_exclusive_scan_256(int v, int* s_wave_tot, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int inc = wave_inclusive_scan(v, lane);
+  if (lane == 63) s_wave_tot[wave] = inc;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    int t = s_wave_tot[w];
+    if (w < wave) base += t;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+// ---------------------------------------------------------------------------
+// Top-k over one row held by a group of GROUP lanes, NV values per lane; the
+// value in slot q of lane g is column q * GROUP + g. Selection order is
+// (value descending, column ascending). Every lane of the group ends with the
+// same selection.
+// ---------------------------------------------------------------------------
+template <int GROUP, int NV>
+__device__ __forceinline__ void topk_group(const float (&val)[NV], int g, int E, int k,
+                                           float (&sel_v)[kMaxTopk], int (&sel_i)[kMaxTopk]) {
+  uint32_t taken = 0;
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    if (j < k) {
+      float lv = -__builtin_huge_valf();
+      int li = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < NV; ++q) {
+        const int col = q * GROUP + g;
+        if (!((taken >> q) & 1u) && col < E && better(val[q], col, lv, li)) {
+          lv = val[q];
+          li = col;
+        }
+      }
+#pragma unroll
+      for (int off = GROUP / 2; off >= 1; off >>= 1) {
+        float ov = __shfl_xor(lv, off, GROUP);
+        int oi = __shfl_xor(li, off, GROUP);
+        if (better(ov, oi, lv, li)) {
+          lv = ov;
+          li = oi;
+        }
+      }
+      sel_v[j] = lv;
+      sel_i[j] = li;
+      if ((li % GROUP) == g) taken |= 1u << (li / GROUP);
+    }
+  }
+}
+
+// Renormalised softmax over the k selected logits; lane g < k of the group
+// writes slot g of the row.
+__device__ __forceinline__ void write_topk(const float (&sel_v)[kMaxTopk], const int (&sel_i)[kMaxTopk],
+                                           int g, int k, int row, int32_t* __restrict__ ids,
+                                           float* __restrict__ wts) {
+  float p[kMaxTopk];
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    if (j < k) {
+      p[j] = expf(sel_v[j] - sel_v[0]);
+      s = s + p[j];
+    }
+  }
+  if (g < k) {
+    float pj = 0.0f;
+    int ij = 0;
+#pragma unroll
+    for (int j = 0; j < kMaxTopk; ++j) {
+      if (j == g) {
+        pj = p[j];
+        ij = sel_i[j];
+      }
+    }
+    ids[(size_t)row * k + g] = ij;
+    wts[(size_t)row * k + g] = pj / s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Router, bf16: logits on MFMA (v_mfma_f32_32x32x16_bf16), top-k in registers.
+//
+// A block of 4 waves takes 128 tokens; each wave owns 32 tokens and all
+// E_pad = 32 * NCB expert columns. Token rows and router weights are loaded
+// straight into two swizzled LDS stages, one 64-wide K chunk at a time (the
+// loads of chunk k+1 overlap the MFMAs on chunk k).
+// ---------------------------------------------------------------------------
+constexpr int kGateBK = 64;
+
+template <int NCB>
+__global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
+    int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
+    float* __restrict__ wts) {
+  constexpr int BROWS = NCB * 32;
+  constexpr int STAGE = (128 + BROWS) * 64;
+  __shared__ __align__(16) bf16_t st0[STAGE];
+  __shared__ __align__(16) bf16_t st1[STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 31, half = lane >> 5;
+  const int row0 = blockIdx.x * 128 + wave * 32;
+  const bf16_t* xa = x + (size_t)blockIdx.x * 128 * H;
+  const int a_rows = T - blockIdx.x * 128;
+  const int nK = H / kGateBK;
+
+  f32x16_t acc[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
+
+  auto issue = [&](int kc, bf16_t* st) {
+    dma_rows<128>(xa, H, kc * kGateBK, a_rows, st, wave, lane);
+    dma_rows<BROWS>(wr, H, kc * kGateBK, E, st + 128 * 64, wave, lane);
+  };
+  auto compute = [&](const bf16_t* st) {
+#pragma unroll
+    for (int i = 0; i < kGateBK / 16; ++i) {
+      const int chunk = 2 * i + half;
+      const bf16x8_t a = lds_frag(st, wave * 32 + r, chunk);
+#pragma unroll
+      for (int c = 0; c < NCB; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, lds_frag(st + 128 * 64, c * 32 + r, chunk), acc[c], 0,
+                                                         0, 0);
+    }
+  };
+
+  issue(0, st0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int kc = 0; kc < nK; ++kc) {
+    bf16_t* cur = (kc & 1) ? st1 : st0;
+    bf16_t* nxt = (kc & 1) ? st0 : st1;
+    if (kc + 1 < nK) issue(kc + 1, nxt);
+    compute(cur);
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  float bias_r[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    const int col = c * 32 + r;
+    bias_r[c] = (bias != nullptr && col < E) ? bias[col] : 0.0f;
+  }
+
+  // 32x32 accumulator layout: register v of lane (r, half) is row
+  // 8 * (v / 4) + 4 * half + (v % 4), column r of the block.
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int row = row0 + 8 * (v >> 2) + 4 * half + (v & 3);
+    float val[NCB];
+#pragma unroll
+    for (int c = 0; c < NCB; ++c) {
+      const int col = c * 32 + r;
+      val[c] = (col < E) ? acc[c][v] + bias_r[c] : -__builtin_huge_valf();
+    }
+    if (logits != nullptr && row < T) {
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) {
+        const int col = c * 32 + r;
+        if (col < E) logits[(size_t)row * E + col] = val[c];
+      }
+    }
+    float sel_v[kMaxTopk];
+    int sel_i[kMaxTopk];
+    topk_group<32, NCB>(val, r, E, k, sel_v, sel_i);
+    if (row < T) write_topk(sel_v, sel_i, r, k, row, ids, wts);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Router, fp32: one wave per token, lanes over experts, VALU dot products in
+// ascending h.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gate_topk_f32_kernel(
+    const float* __restrict__ x, const float* __restrict__ wr, const float* __restrict__ bias,
+    int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
+    float* __restrict__ wts) {
+  constexpr int NV = kMaxExperts / kWave;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= T) return;
+  const float* xr = x + (size_t)row * H;
+  float val[NV];
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    const int e = q * kWave + lane;
+    float z = -__builtin_huge_valf();
+    if (e < E) {
+      const float* w = wr + (size_t)e * H;
+      float s = 0.0f;
+      for (int h = 0; h < H; ++h) s = __builtin_fmaf(xr[h], w[h], s);
+      z = s + (bias != nullptr ? bias[e] : 0.0f);
+      if (logits != nullptr) logits[(size_t)row * E + e] = z;
+    }
+    val[q] = z;
+  }
+  float sel_v[kMaxTopk];
+  int sel_i[kMaxTopk];
+  topk_group<kWave, NV>(val, lane, E, k, sel_v, sel_i);
+  write_topk(sel_v, sel_i, lane, k, row, ids, wts);
+}
+
+// ---------------------------------------------------------------------------
+// Activation profile: per-block expert counts (LDS atomics on integers, so
+// the result does not depend on their order).
+// ---------------------------------------------------------------------------
+constexpr int kTokPerBlk = 256;
+
+__global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
+                                                   int32_t* __restrict__ table) {
+  __shared__ int cnt[kMaxExperts];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += 256) cnt[e] = 0;
+  __syncthreads();
+  const size_t first = (size_t)blockIdx.x * kTokPerBlk * k;
+  const size_t last = min((size_t)T * k, first + (size_t)kTokPerBlk * k);
+  for (size_t p = first + tid; p < last; p += 256) {
+    const int e = ids[p];
+    if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += 256) table[(size_t)blockIdx.x * E + e] = cnt[e];
+}
+
+// Totals, local offsets (exclusive scan over slots) and per-block row bases.
+__global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ table, int n_blk,
+                                                   SlotMap map, int32_t* __restrict__ counts,
+                                                   int32_t* __restrict__ offsets,
+                                                   int32_t* __restrict__ bases) {
+  __shared__ int s_cnt[kMaxExperts];
+  __shared__ int s_tot[4];
+  const int tid = threadIdx.x;
+  const int E = map.n_experts, L = map.n_local;
+  for (int e = tid; e < E; e += 256) {
+    int c = 0;
+    for (int b = 0; b < n_blk; ++b) c += table[(size_t)b * E + e];
+    counts[e] = c;
+    s_cnt[e] = c;
+  }
+  __syncthreads();
+  const int my_e = tid < L ? map.expert_of[tid] : 0;
+  const int v = tid < L ? s_cnt[my_e] : 0;
+  int total;
+  const int excl = block_exclusive_scan_256(v, s_tot, &total);
+  if (tid < L) {
+    offsets[tid + 1] = excl + v;
+    int run = excl;
+    for (int b = 0; b < n_blk; ++b) {
+      bases[(size_t)b * L + tid] = run;
+      run += table[(size_t)b * E + my_e];
+    }
+  }
+  if (tid == 0) offsets[0] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Dispatch permutation. Block b re-reads the ids of its 256 tokens; the rank
+// of an assignment within its slot comes from per-wave 64-bit lane masks
+// (order of lanes = order of tokens), never from atomic return order, so
+// the permutation is the stable counting sort and is identical run to run.
+// Each wave then copies its tokens' rows once per local assignment.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void permute_kernel(
+    const uint4* __restrict__ x, int row_vecs, const int32_t* __restrict__ ids, int T, int k,
+    SlotMap map, const int32_t* __restrict__ bases, int M_cap, uint4* __restrict__ x_perm,
+    int32_t* __restrict__ perm_src, int32_t* __restrict__ dest) {
+  __shared__ unsigned long long s_mask[4][kMaxExperts];
+  __shared__ int s_pre[4][kMaxExperts];
+  __shared__ int s_pos[kTokPerBlk][kMaxTopk];
+  __shared__ int16_t s_slot_of[kMaxExperts];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int E = map.n_experts, L = map.n_local;
+  for (int i = tid; i < 4 * kMaxExperts; i += 256) (&s_mask[0][0])[i] = 0ull;
+  for (int e = tid; e < E; e += 256) s_slot_of[e] = map.slot_of[e];
+  __syncthreads();
+
+  const int t = blockIdx.x * kTokPerBlk + tid;
+  int my_slot[kMaxTopk];
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    my_slot[j] = -1;
+    if (j < k && t < T) {
+      const int e = ids[(size_t)t * k + j];
+      const int s = ((unsigned)e < (unsigned)E) ? s_slot_of[e] : -1;
+      my_slot[j] = s;
+      if (s >= 0) atomicOr(&s_mask[wave][s], 1ull << lane);
+    }
+  }
+  __syncthreads();
+  if (tid < L) {
+    int run = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      s_pre[w][tid] = run;
+      run += __popcll(s_mask[w][tid]);
+    }
+  }
+  __syncthreads();
+  const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    if (j < k) {
+      const int s = my_slot[j];
+      int pos = -1;
+      if (s >= 0) {
+        pos = bases[(size_t)blockIdx.x * L + s] + s_pre[wave][s] + __popcll(s_mask[wave][s] & below);
+        if (pos < 0 || pos >= M_cap) pos = -1;
+      }
+      if (t < T) {
+        dest[(size_t)t * k + j] = pos;
+        if (pos >= 0) perm_src[pos] = t * k + j;
+      }
+      s_pos[tid][j] = pos;
+    }
+  }
+  __syncthreads();
+
+  for (int tt = 0; tt < kWave; ++tt) {
+    const int slot_t = wave * kWave + tt;
+    const int tok = blockIdx.x * kTokPerBlk + slot_t;
+    if (tok >= T) break;
+    int pj[kMaxTopk];
+    bool any = false;
+#pragma unroll
+    for (int j = 0; j < kMaxTopk; ++j) {
+      pj[j] = (j < k) ? s_pos[slot_t][j] : -1;
+      any |= pj[j] >= 0;
+    }
+    if (!any) continue;
+    const uint4* src = x + (size_t)tok * row_vecs;
+    for (int v = lane; v < row_vecs; v += kWave) {
+      const uint4 val = src[v];
+#pragma unroll
+      for (int j = 0; j < kMaxTopk; ++j)
+        if (pj[j] >= 0) x_perm[(size_t)pj[j] * row_vecs + v] = val;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Combine: one wave per token, 16-byte vectors along H, fp32 accumulation in
+// ascending slot order (no contraction, so each step rounds like the
+// definition: a product, then a sum).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void combine_bf16_kernel(const uint4* __restrict__ y, const float* __restrict__ w,
+                                                           const int32_t* __restrict__ dest, int T, int k,
+                                                           int row_vecs, int M_cap, uint4* __restrict__ out) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  int d[kMaxTopk];
+  float wt[kMaxTopk];
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    d[j] = -1;
+    wt[j] = 0.0f;
+    if (j < k) {
+      const int dj = dest[(size_t)t * k + j];
+      d[j] = (dj >= 0 && dj < M_cap) ? dj : -1;
+      wt[j] = w[(size_t)t * k + j];
+    }
+  }
+  for (int v = lane; v < row_vecs; v += kWave) {
+    float acc[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxTopk; ++j) {
+      if (j < k && d[j] >= 0) {
+        const uint4 yv = y[(size_t)d[j] * row_vecs + v];
+        const uint32_t u[4] = {yv.x, yv.y, yv.z, yv.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float lo = __uint_as_float(u[q] << 16);
+          const float hi = __uint_as_float(u[q] & 0xffff0000u);
+          const float plo = wt[j] * lo;
+          const float phi = wt[j] * hi;
+          acc[2 * q] = acc[2 * q] + plo;
+          acc[2 * q + 1] = acc[2 * q + 1] + phi;
+        }
+      }
+    }
+    uint4 o;
+    o.x = pack_bf16x2(acc[0], acc[1]);
+    o.y = pack_bf16x2(acc[2], acc[3]);
+    o.z = pack_bf16x2(acc[4], acc[5]);
+    o.w = pack_bf16x2(acc[6], acc[7]);
+    out[(size_t)t * row_vecs + v] = o;
+  }
+}
+
+__global__ __launch_bounds__(256) void combine_f32_kernel(const float4* __restrict__ y, const float* __restrict__ w,
+                                                          const int32_t* __restrict__ dest, int T, int k,
+                                                          int row_vecs, int M_cap, float4* __restrict__ out) {
+#pragma clang fp contract(off)
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  for (int v = lane; v < row_vecs; v += kWave) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < k; ++j) {
+      const int dj = dest[(size_t)t * k + j];
+      if (dj < 0 || dj >= M_cap) continue;
+      const float wj = w[(size_t)t * k + j];
+      const float4 yv = y[(size_t)dj * row_vecs + v];
+      const float px = wj * yv.x, py = wj * yv.y, pz = wj * yv.z, pw = wj * yv.w;
+      acc.x = acc.x + px;
+      acc.y = acc.y + py;
+      acc.z = acc.z + pz;
+      acc.w = acc.w + pw;
+    }
+    out[(size_t)t * row_vecs + v] = acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers (called from the C ABI after validation).
+// ---------------------------------------------------------------------------
+hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, int T, int H, int E, int k,
+                            bool bf16, float* logits, int32_t* ids, float* wts, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (!bf16) {
+    gate_topk_f32_kernel<<<(T + 3) / 4, 256, 0, s>>>(static_cast<const float*>(x),
+                                                     static_cast<const float*>(wr), bias, T, H, E, k,
+                                                     logits, ids, wts);
+    return hipGetLastError();
+  }
+  const int ncb = (E + 31) / 32;
+  const dim3 grid((T + 127) / 128);
+  const bf16_t* xb = static_cast<const bf16_t*>(x);
+  const bf16_t* wb = static_cast<const bf16_t*>(wr);
+#define MOE_GATE_CASE(N)                                                                        \
+  case N:                                                                                       \
+    gate_topk_bf16_kernel<N><<<grid, 256, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts); \
+    break;
+  switch (ncb) {
+    MOE_GATE_CASE(1)
+    MOE_GATE_CASE(2)
+    MOE_GATE_CASE(3)
+    MOE_GATE_CASE(4)
+    MOE_GATE_CASE(5)
+    MOE_GATE_CASE(6)
+    MOE_GATE_CASE(7)
+    MOE_GATE_CASE(8)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef MOE_GATE_CASE
+  return hipGetLastError();
+}
+
+size_t hist_ws_bytes(int T, int E, int E_local) {
+  const size_t n_blk = (size_t)(T + kTokPerBlk - 1) / kTokPerBlk;
+  const size_t table = n_blk * E * sizeof(int32_t);
+  const size_t bases = n_blk * E_local * sizeof(int32_t);
+  return ((table + 255) / 256) * 256 + ((bases + 255) / 256) * 256 + 256;
+}
+
+static void hist_ws_split(void* ws, int T, int E, int32_t** table, int32_t** bases) {
+  const size_t n_blk = (size_t)(T + kTokPerBlk - 1) / kTokPerBlk;
+  const size_t tb = ((n_blk * E * sizeof(int32_t) + 255) / 256) * 256;
+  *table = static_cast<int32_t*>(ws);
+  *bases = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + tb);
+}
+
+hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map, int32_t* counts,
+                            int32_t* offsets, void* ws, hipStream_t s) {
+  const int n_blk = (T + kTokPerBlk - 1) / kTokPerBlk;
+  int32_t *table, *bases;
+  hist_ws_split(ws, T, map.n_experts, &table, &bases);
+  if (n_blk > 0) {
+    hist_kernel<<<n_blk, 256, 0, s>>>(ids, T, k, map.n_experts, table);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  scan_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map, const void* ws, int T, int H,
+                          int k, int M_cap, bool bf16, void* x_perm, int32_t* perm_src, int32_t* dest,
+                          hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int n_blk = (T + kTokPerBlk - 1) / kTokPerBlk;
+  int32_t *table, *bases;
+  hist_ws_split(const_cast<void*>(ws), T, map.n_experts, &table, &bases);
+  const int row_vecs = (H * (bf16 ? 2 : 4)) / 16;
+  permute_kernel<<<n_blk, 256, 0, s>>>(static_cast<const uint4*>(x), row_vecs, ids, T, k, map, bases, M_cap,
+                                       static_cast<uint4*>(x_perm), perm_src, dest);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const void* y, const float* w, const int32_t* dest, int T, int k, int H, int M_cap,
+                          bool bf16, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const dim3 grid((T + 3) / 4);
+  if (bf16) {
+    combine_bf16_kernel<<<grid, 256, 0, s>>>(static_cast<const uint4*>(y), w, dest, T, k, H / 8, M_cap,
+                                             static_cast<uint4*>(out));
+  } else {
+    combine_f32_kernel<<<grid, 256, 0, s>>>(static_cast<const float4*>(y), w, dest, T, k, H / 4, M_cap,
+                                            static_cast<float4*>(out));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace moe

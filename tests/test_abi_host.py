@@ -1,0 +1,168 @@
+"""CPU tests of the C ABI: the library loads, exports what include/moe.h
+declares, and rejects bad arguments on the host before launching anything.
+
+None of these calls reaches a kernel launch (every one fails validation or is
+a workspace-size query), so they run without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_00735_amd as moe
+from paper_2606_00735_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+INVALID, UNSUPPORTED, WORKSPACE = 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def L():
+    return moe.load_library()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "moe.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:moe_status|const char\*|int)\s+(moe_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_six_entry_points():
+    names = declared_functions()
+    for n in ("moe_gate_topk", "moe_expert_histogram_scan", "moe_permute", "moe_grouped_swiglu_ffn",
+              "moe_unpermute_combine", "moe_load_sweep"):
+        assert n in names
+    assert set(names) == set(_lib.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(L):
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", moe.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (moe_\w+)$", out, re.M))
+    for n in declared_functions():
+        assert n in exported, n
+        assert hasattr(L, n)
+
+
+def test_version_and_status_strings(L):
+    assert L.moe_abi_version() == 1
+    assert L.moe_status_string(0) == b"ok"
+    assert L.moe_status_string(3) == b"workspace too small"
+    assert L.moe_status_string(99) == b"unknown status"
+
+
+FAKE = ctypes.c_void_p(0x10000)      # aligned, never dereferenced: validation fails first
+MISALIGNED = ctypes.c_void_p(0x10004)
+
+
+@pytest.mark.parametrize("T,H,E,k,dt,expect", [
+    (4, 128, 8, 9, 1, INVALID),     # k > E
+    (4, 128, 8, 0, 1, INVALID),     # k = 0
+    (4, 128, 300, 2, 1, INVALID),   # E > 256
+    (4, 128, 32, 17, 1, INVALID),   # k > 16
+    (-1, 128, 8, 2, 1, INVALID),    # T < 0
+    (4, 100, 8, 2, 0, INVALID),     # H % 8
+    (4, 72, 8, 2, 1, UNSUPPORTED),  # bf16 needs H % 64
+    (4, 128, 8, 2, 7, INVALID),     # bad dtype
+])
+def test_gate_topk_validation(L, T, H, E, k, dt, expect):
+    st = L.moe_gate_topk(FAKE, FAKE, None, T, H, E, k, dt, None, FAKE, FAKE, None)
+    assert st == expect
+
+
+def test_gate_topk_null_and_alignment(L):
+    assert L.moe_gate_topk(None, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_gate_topk(MISALIGNED, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_gate_topk(None, None, None, 0, 128, 8, 2, 1, None, None, None, None) == 0  # T=0 no-op
+
+
+def _hist(L, emap, T=64, k=2, E=8, E_local=None, ws=FAKE, nbytes=10 ** 9):
+    emap = np.asarray(emap, np.int32)
+    E_local = int((emap >= 0).sum()) if E_local is None else E_local
+    n = ctypes.c_size_t(nbytes)
+    return L.moe_expert_histogram_scan(FAKE, T, k, E, emap.ctypes.data_as(ctypes.c_void_p), E_local,
+                                       ctypes.c_void_p(None), FAKE, ws, ctypes.byref(n), None), n.value
+
+
+def test_histogram_workspace_query(L):
+    st, n = _hist(L, np.arange(8), ws=ctypes.c_void_p(None), nbytes=0)
+    assert st == 0 and n >= 1 * 8 * 4
+    st, n2 = _hist(L, np.arange(8), T=16384, k=8, E=256, ws=ctypes.c_void_p(None), nbytes=0)
+    assert st == 0 and n2 >= 64 * 256 * 4
+    st, _ = _hist(L, np.arange(8), nbytes=n - 1)
+    assert st == WORKSPACE
+
+
+@pytest.mark.parametrize("emap", [
+    [0, 1, 2, 3, 4, 5, 6, 6],          # slot used twice
+    [0, 1, 2, 3, 4, 5, 6, 8],          # slot out of range
+    [0, 1, 2, 3, 4, 5, -2, 7],         # below -1
+    [-1, 1, 2, 3, 4, 5, 6, 7],         # slot 0 unused
+])
+def test_histogram_rejects_bad_expert_map(L, emap):
+    emap = np.asarray(emap, np.int32)
+    st, _ = _hist(L, emap, E_local=7 if (emap == -1).any() else 8)
+    assert st == INVALID
+
+
+def test_histogram_counts_pointer_required(L):
+    st, _ = _hist(L, np.arange(8))   # counts = NULL
+    assert st == INVALID
+
+
+def test_permute_validation(L):
+    emap = np.arange(8, dtype=np.int32)
+    p = emap.ctypes.data_as(ctypes.c_void_p)
+    # M_cap < T*k
+    assert L.moe_permute(FAKE, FAKE, p, FAKE, 10 ** 9, 64, 128, 2, 8, 8, 100, 1, FAKE, FAKE, FAKE,
+                         None) == INVALID
+    # workspace too small
+    assert L.moe_permute(FAKE, FAKE, p, FAKE, 8, 64, 128, 2, 8, 8, 128, 1, FAKE, FAKE, FAKE, None) == WORKSPACE
+    # E_local does not match the map
+    assert L.moe_permute(FAKE, FAKE, p, FAKE, 10 ** 9, 64, 128, 2, 8, 7, 128, 1, FAKE, FAKE, FAKE,
+                         None) == INVALID
+
+
+def test_ffn_validation_and_query(L):
+    n = ctypes.c_size_t(0)
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 4096, 14336, 8192, 1, None, None,
+                                    ctypes.byref(n), None) == 0
+    assert n.value >= 8192 * 14336 * 2
+    for H, I in ((4096, 14300), (4000, 14336)):
+        assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, H, I, 64, 1, None, None,
+                                        ctypes.byref(n), None) == UNSUPPORTED
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 300, 128, 128, 64, 1, None, None,
+                                    ctypes.byref(n), None) == UNSUPPORTED
+    n = ctypes.c_size_t(10)
+    assert L.moe_grouped_swiglu_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 64, 1, FAKE, FAKE,
+                                    ctypes.byref(n), None) == WORKSPACE
+
+
+def test_combine_validation(L):
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, 4, 0, 128, 8, 1, FAKE, None) == INVALID
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, 4, 2, 100, 8, 1, FAKE, None) == INVALID
+    assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, 4, 2, 128, 8, 1, MISALIGNED, None) == INVALID
+    assert L.moe_unpermute_combine(None, None, None, 0, 2, 128, 8, 1, None, None) == 0
+
+
+def test_sweep_validation(L):
+    Ms = np.array([1, 2, 4], np.int32)
+    p = Ms.ctypes.data_as(ctypes.c_void_p)
+    n = ctypes.c_size_t(0)
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 1, p, 3, 1, 5, None, None,
+                            ctypes.byref(n), None, None, None) == 0
+    assert n.value >= 4 * 768 * 2
+    bad = np.array([1, 0], np.int32)
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 1, bad.ctypes.data_as(ctypes.c_void_p), 2,
+                            1, 5, None, None, ctypes.byref(n), None, None, None) == INVALID
+    assert L.moe_load_sweep(None, None, None, None, 0, 2048, 768, 1, p, 3, 1, 5, None, None,
+                            ctypes.byref(n), None, None, None) == INVALID
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(4, 128, dtype=torch.bfloat16)
+    w = torch.zeros(8, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        moe.moe_gate_topk(x, w, None, 2)

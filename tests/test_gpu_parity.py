@@ -1,0 +1,215 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Every case prints its name, shape and seed before touching the GPU. Sizes
+are chosen so the oracle finishes in seconds while still spanning several
+tiles and ragged per-expert tails; full-size cases (the bench's launch
+configuration) are in test_gpu_fullsize.py.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_00735_amd as moe
+from oracle import moe_oracle as O
+from synth import CONFIGS, make_layer
+from synth.moe_inputs import LayerInputs, expert_map_for, make_experts, make_router
+import gpu_helpers as G
+
+pytestmark = pytest.mark.gpu
+
+
+def banner(*a):
+    print("CASE", *a, flush=True)
+
+
+def run_gpu(li, logits=True):
+    d = G.upload_layer(li)
+    bufs = G.poison_bufs(li.T, li.shape.k, li.shape.H, li.shape.E, len(li.local), d["dtype"])
+    g = moe.moe_layer(d["x"], d["w_router"], d["bias"], li.shape.k, li.expert_map, d["w_gate"], d["w_up"],
+                      d["w_down"], logits=logits, bufs=bufs)
+    torch.cuda.synchronize()
+    return g
+
+
+REDUCED = [
+    ("tiny", 64, 1.0),
+    ("tiny", 37, 0.0),
+    ("mixtral", 64, 0.0),
+    ("mixtral", 96, 1.0),
+    ("qwen3", 256, 0.0),
+    ("qwen3", 200, 1.0),
+    ("qwen3", 256, 1.5),
+    ("dsv3_shard", 512, 0.0),
+    ("dsv3_shard", 384, 1.5),
+    ("maverick_shard", 1024, 1.0),
+]
+
+
+@pytest.mark.parametrize("name,T,alpha", REDUCED, ids=[f"{n}-T{t}-a{a}" for n, t, a in REDUCED])
+def test_layer_parity(name, T, alpha):
+    banner("layer", name, T, alpha, "seed 0")
+    li = make_layer(name, T, alpha, seed=0)
+    r = G.oracle_layer(li)
+    g = run_gpu(li)
+    stats = G.compare_layer(li, g, r, f"{name} T={T} a={alpha}")
+    print("  stats", stats, "M_loc", int(r["offsets"][-1]), flush=True)
+
+
+def test_layer_parity_seed1():
+    banner("layer qwen3 T=128 a=1.0 seed 1")
+    li = make_layer("qwen3", 128, 1.0, seed=1)
+    G.compare_layer(li, run_gpu(li), G.oracle_layer(li), "qwen3 seed1")
+
+
+def test_deterministic_bitwise():
+    banner("determinism qwen3 T=512 a=1.0")
+    li = make_layer("qwen3", 512, 1.0, seed=0)
+    a = run_gpu(li)
+    b = run_gpu(li)
+    for key in ("logits", "ids", "weights", "counts", "offsets", "dest", "out"):
+        assert torch.equal(a[key], b[key]), key
+    m = int(a["offsets"][-1])
+    for key in ("perm_src", "x_perm", "y_perm"):
+        assert torch.equal(a[key][:m], b[key][:m]), key
+
+
+def _custom(shape, T, alpha, seed=0, local=None, tie=False):
+    x, w, b, rank = make_router(shape, T, alpha, seed)
+    if tie:
+        w = np.zeros_like(w)
+        b = np.zeros_like(b)
+    local = np.arange(shape.E) if local is None else np.sort(np.asarray(local))
+    emap = expert_map_for(shape, local)
+    wg, wu, wd = make_experts(shape, local, seed)
+    return LayerInputs(shape, T, alpha, seed, x, w, b, rank, local, emap, wg, wu, wd)
+
+
+def test_single_token():
+    banner("edge T=1 qwen3")
+    li = make_layer("qwen3", 1, 1.0, seed=2)
+    G.compare_layer(li, run_gpu(li), G.oracle_layer(li), "T=1")
+
+
+def test_top1_gather_exact():
+    """k = 1: the weight is exactly 1, so out is y_perm gathered bit for bit."""
+    banner("edge k=1 maverick-like small")
+    shape = dataclasses.replace(CONFIGS["maverick_shard"], H=256, I=384, E=16, E_local=16)
+    li = _custom(shape, 300, 1.0)
+    r = G.oracle_layer(li)
+    g = run_gpu(li)
+    G.compare_layer(li, g, r, "k=1")
+    assert torch.all(g["weights"] == 1.0)
+    dest = g["dest"].long()
+    assert torch.equal(g["out"], g["y_perm"][dest])
+
+
+def test_k_equals_e():
+    banner("edge k=E=8")
+    shape = dataclasses.replace(CONFIGS["mixtral"], H=128, I=256, E=8, k=8, E_local=8)
+    li = _custom(shape, 70, 0.5)
+    G.compare_layer(li, run_gpu(li), G.oracle_layer(li), "k=E")
+
+
+def test_all_tokens_on_one_expert():
+    """A huge bias sends every token to the rank-1 expert: one expert with
+    M = T rows (two full 128-row tiles and a ragged one), the rest idle."""
+    banner("edge all tokens one expert")
+    shape = dataclasses.replace(CONFIGS["qwen3"], H=256, I=384, E=16, k=1, E_local=16)
+    li = _custom(shape, 300, 50.0)
+    r = G.oracle_layer(li)
+    assert r["counts"].max() == 300
+    G.compare_layer(li, run_gpu(li), r, "one expert")
+
+
+def test_ties_go_to_lower_ids():
+    banner("edge all logits tie")
+    shape = dataclasses.replace(CONFIGS["qwen3"], H=128, I=128, E=16, k=4, E_local=16)
+    li = _custom(shape, 50, 0.0, tie=True)
+    r = G.oracle_layer(li)
+    assert np.all(r["ids"] == np.arange(4))
+    G.compare_layer(li, run_gpu(li), r, "ties")
+
+
+def test_shard_without_local_experts():
+    banner("edge E_local=0")
+    shape = dataclasses.replace(CONFIGS["dsv3_shard"], H=128, I=128, E=16, k=2, E_local=0)
+    li = _custom(shape, 40, 1.0, local=[])
+    r = G.oracle_layer(li)
+    g = run_gpu(li)
+    assert np.array_equal(G.down(g["counts"]), r["counts"])
+    assert torch.all(g["dest"] == -1)
+    assert torch.all(g["out"] == 0)
+    assert G.down(g["offsets"]).tolist() == [0]
+
+
+def test_mixed_small_and_large_experts():
+    """Skewed loads: some experts take more than 128 rows, some fewer than 32,
+    some none, with ragged tails everywhere, in one launch."""
+    banner("edge mixed tiles")
+    shape = dataclasses.replace(CONFIGS["qwen3"], H=384, I=256, E=24, k=3, E_local=24)
+    li = _custom(shape, 400, 1.2, seed=5)
+    r = G.oracle_layer(li)
+    c = r["counts"]
+    assert c.max() > 128 and ((c > 0) & (c <= 32)).any()
+    G.compare_layer(li, run_gpu(li), r, "mixed")
+
+
+def test_empty_batch():
+    banner("edge T=0")
+    d = G.upload_layer(make_layer("tiny", 1, 1.0))
+    x = d["x"][:0]
+    ids, w, _ = moe.moe_gate_topk(x, d["w_router"], d["bias"], 2)
+    counts, offsets, ws = moe.moe_expert_histogram_scan(ids, 8, np.arange(8))
+    torch.cuda.synchronize()
+    assert torch.all(counts == 0) and torch.all(offsets == 0)
+
+
+def test_ffn_stage_on_oracle_inputs():
+    """The FFN alone, fed the oracle's x_perm and offsets."""
+    banner("stage ffn dsv3-like")
+    li = make_layer("dsv3_shard", 256, 0.0, seed=3)
+    r = G.oracle_layer(li)
+    m = int(r["offsets"][-1])
+    M_cap = m + 5
+    xp = np.zeros((M_cap, li.shape.H), np.float32)
+    xp[:m] = r["x_perm"]
+    d = G.upload_layer(li)
+    y, ws = moe.moe_grouped_swiglu_ffn(G.up(xp, torch.bfloat16), d["w_gate"], d["w_up"], d["w_down"],
+                                       G.up_i32(r["offsets"]))
+    torch.cuda.synchronize()
+    h = G.down(moe.ffn_hidden(ws, M_cap, li.shape.I, torch.bfloat16))[:m]
+    G.check_bf16(h, r["h"], "stage h")
+    G.check_bf16(G.down(y)[:m], r["y_perm"], "stage y")
+
+
+def test_combine_stage_on_oracle_inputs():
+    banner("stage combine qwen3")
+    li = make_layer("qwen3", 64, 1.0, seed=4)
+    r = G.oracle_layer(li)
+    yp = G.up(r["y_perm"], torch.bfloat16)
+    out = moe.moe_unpermute_combine(yp, G.up(r["weights"], torch.float32), G.up_i32(r["dest"]), li.T)
+    torch.cuda.synchronize()
+    G.check_bf16(G.down(out), r["out"], "stage out")
+
+
+def test_load_sweep_output_and_timing():
+    """The sweep's last run leaves y for the largest M; it must match the
+    oracle's single-expert FFN, and every median must be positive."""
+    banner("sweep qwen3 expert")
+    shape = CONFIGS["qwen3"]
+    wg, wu, wd = make_experts(shape, [5], seed=0)
+    x, *_ = make_router(shape, 300, 0.0, seed=0)
+    Ms = [1, 7, 33, 128, 300]
+    rot = 3
+    dg = G.up(np.repeat(wg, rot, 0), torch.bfloat16)
+    du = G.up(np.repeat(wu, rot, 0), torch.bfloat16)
+    dd = G.up(np.repeat(wd, rot, 0), torch.bfloat16)
+    y = torch.full((300, shape.H), float("nan"), dtype=torch.bfloat16, device="cuda")
+    us, allus = moe.moe_load_sweep(G.up(x, torch.bfloat16), dg, du, dd, Ms, warmup=2, iters=5, y_scratch=y,
+                                   keep_all=True)
+    print("  sweep us", us.tolist(), flush=True)
+    assert np.all(us > 0) and allus.shape == (5, 5)
+    _, yref = O.swiglu_rows(x, wg[0], wu[0], wd[0], bf16=True)
+    G.check_bf16(G.down(y), yref, "sweep y")
