@@ -261,9 +261,12 @@ def moe_layer_rows(x, w_router, bias, k, expert_map, w_gate, w_up, w_down,
         y[sel[:, 0], sel[:, 1]] = ys
         local[sel[:, 0], sel[:, 1]] = True
     out = np.zeros((n, H), F32)
+    abs_terms = np.zeros((n, H))
     for j in range(k):
         m = local[:, j]
         out[m] = (out[m] + (w[m, j][:, None] * y[m, j]).astype(F32)).astype(F32)
+        abs_terms[m] += np.abs(w[m, j].astype(np.float64))[:, None] * np.abs(y[m, j].astype(np.float64))
     if bf16:
         out = bf16_rne(out)
-    return dict(logits=z, ids=ids, weights=w, out=out)
+    # abs_terms = sum_j |w_j y_j|: the magnitude of what was summed into out
+    return dict(logits=z, ids=ids, weights=w, out=out, abs_terms=abs_terms)

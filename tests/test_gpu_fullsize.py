@@ -65,8 +65,10 @@ def test_fullsize(name, T, alpha):
     ref = O.moe_layer_rows(li.x, li.w_router, li.bias, k, li.expert_map, li.w_gate, li.w_up, li.w_down,
                            bf16=bf16, rows=rows)
     got = G.down(g["out"])[rows]
+    no_loc = np.all(dest.reshape(T, k)[rows] < 0, axis=1)
+    assert np.all(got[no_loc] == 0.0), "rows without local experts must be zero"
     if bf16:
-        G.check_bf16(got, ref["out"], f"{name} out rows")
+        G.check_bf16(got, ref["out"], f"{name} out rows", scale=ref["abs_terms"])
     else:
         G.check_f32(got, ref["out"], f"{name} out rows")
     assert np.all(np.isfinite(G.down(g["out"]))), "unwritten out rows"

@@ -245,3 +245,19 @@ def _count_failures(ns):
         except (AssertionError, ValueError, IndexError):
             failed.append(name)
     return failed
+
+
+@pytest.mark.parametrize("name,T,alpha", [("dsv3_shard", 512, 0.0), ("maverick_shard", 1024, 1.0),
+                                          ("qwen3", 256, 1.0)])
+def test_tolerance_rule_accepts_two_correct_oracles(name, T, alpha):
+    """The bf16 comparison rule used on the GPU must accept the fp32-accumulate
+    oracle against the fp64-accumulate oracle (same rounding points): both are
+    correct, so any rule that rejects one of them is too tight."""
+    import gpu_helpers as G
+    from synth import make_layer
+    li = make_layer(name, T, alpha, seed=0)
+    a = G.oracle_layer(li, "f32")
+    b = G.oracle_layer(li, "f64")
+    G.check_bf16(a["y_perm"], b["y_perm"], "y", scale=G.down_scale(b["h"], li.w_down, b["offsets"]))
+    G.check_bf16(a["out"], b["out"], "out",
+                 scale=G.combine_scale(b["weights"], b["y_perm"], b["dest"], T, li.shape.k))
