@@ -235,6 +235,7 @@ def main():
         rep = lambda a: up(a).repeat(n_rot, 1, 1).contiguous()
         xs = up(make_router(shape, max(SWEEP_MS), 0.0, seed=args.seed)[0])
         med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), SWEEP_MS, warmup=3, iters=args.sweep_iters)
+        med = [float(v) for v in med]
         result["load_sweep"] = {"M": SWEEP_MS, "us": [round(float(v), 2) for v in med], "n_rot": n_rot,
                                 "tflops": [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, u in
                                            zip(SWEEP_MS, med)],

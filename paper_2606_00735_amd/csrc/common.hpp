@@ -53,18 +53,38 @@ __device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ (r
 // Loads rows [0, R) (64 bf16 each, starting at column `col0`) of a row-major
 // matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
 // `row_limit` re-read row `row_limit - 1` (their results are never stored),
-// so no load leaves the matrix. R must be a multiple of 32 (4 waves x 8 rows).
+// so no load leaves the matrix. With live == false every lane reads the
+// first 16 bytes of the matrix instead (one cache line per instruction): the
+// pipelines below issue such a load where no chunk is left, so the number of
+// loads in flight never depends on a branch. R must be a multiple of 32
+// (4 waves x 8 rows).
+//
+// The load is issued through inline assembly, so the compiler does not track
+// it: every consumer waits for it explicitly (wait_vmcnt + lds_barrier).
+// Tracked, the compiler would add a vmcnt(0) before LDS reads it cannot prove
+// disjoint from a load still in flight, which serialises the pipeline. Its
+// own vmcnt waits stay correct: loads complete in issue order, so untracked
+// younger loads only make those waits more conservative. Nothing else in
+// these kernels uses M0.
+__device__ __forceinline__ void dma16(const void* gaddr, const bf16_t* lds) {
+  const uint32_t m0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gaddr), "s"(m0)
+               : "memory");
+}
+
 template <int R>
 __device__ __forceinline__ void dma_rows(const bf16_t* __restrict__ src, size_t ld, int col0, int row_limit,
-                                         bf16_t* lds, int wave, int lane) {
+                                         bool live, bf16_t* lds, int wave, int lane) {
 #pragma unroll
   for (int i = 0; i < R / 32; ++i) {
     const int r0 = (i * 4 + wave) * 8;
     const int r = r0 + (lane >> 3);
     const int c = swz_chunk(r, lane & 7);
     const int rr = r < row_limit ? r : row_limit - 1;
-    __builtin_amdgcn_global_load_lds(src + (size_t)rr * ld + col0 + c * 8, (lds_void_t*)(lds + r0 * 64), 16, 0,
-                                     0);
+    const size_t off = live ? (size_t)rr * ld + col0 + c * 8 : 0;
+    dma16(src + off, lds + r0 * 64);
   }
 }
 
@@ -78,6 +98,50 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier for the LDS pipelines. __syncthreads() adds a release
+// fence, which makes the compiler drain every outstanding global load
+// (vmcnt(0)) before the barrier, prefetches included. The pipelines instead
+// wait explicitly (wait_vmcnt) for the stage they are about to read, so the
+// barrier itself only needs to keep the compiler from moving memory
+// operations across it (signal fences emit no instructions).
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Three-stage K pipeline over 64-wide chunks. issue(kc, live, stage) loads
+// chunk kc into a stage with exactly LOADS load instructions per wave
+// (live == false: a placeholder load, see dma_rows); compute(stage) consumes
+// one stage. Chunk c+2 is requested while the MFMAs work on chunk c, so two
+// chunks are always in flight. The stages are three distinct arrays chosen
+// statically (the loop is unrolled three ways), so the compiler can see that
+// a pending load into one stage does not touch the stage being read and adds
+// no wait of its own. Every wave writes only its own 1 KB slices of a stage.
+template <int LOADS, class Issue, class Compute>
+__device__ __forceinline__ void pipeline3(int nK, bf16_t* st0, bf16_t* st1, bf16_t* st2, Issue&& issue,
+                                          Compute&& compute) {
+  auto step = [&](int c, bf16_t* cur, bf16_t* pf) {
+    wait_vmcnt<LOADS>();  // chunk c landed; chunk c+1 may still be in flight
+    lds_barrier();        // every wave's chunk c landed; every wave is done with chunk c-1
+    issue(c + 2, c + 2 < nK, pf);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(cur);
+  };
+  wait_vmcnt<0>();  // nothing older (e.g. a previous tile's stores) is left in the count
+  issue(0, true, st0);
+  issue(1, 1 < nK, st1);
+  for (int kc = 0;; kc += 3) {
+    step(kc, st0, st2);
+    if (kc + 1 >= nK) break;
+    step(kc + 1, st1, st0);
+    if (kc + 2 >= nK) break;
+    step(kc + 2, st2, st1);
+    if (kc + 3 >= nK) break;
+  }
+  lds_barrier();  // all waves are done reading before the stages are refilled
 }
 
 // (value, index) ordering of the router: larger value first, then lower index.

@@ -37,20 +37,24 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
 
 // One BM x 128 output tile (two of them, gate and up, when DUAL) over the
 // whole K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from
-// global memory into two swizzled LDS stages (loads of chunk k+1 overlap the
-// MFMAs on chunk k).
+// global memory into three swizzled LDS stages. Chunk c+2 is requested while
+// the MFMAs work on chunk c, so two chunks of loads are always in flight.
+// The stages are distinct arrays selected statically (the loop is unrolled
+// three ways), which lets the compiler see that a pending load into one stage
+// does not touch the stage being read.
 constexpr int kARows = 128;  // A rows reserved per stage
 
 template <int BM, bool DUAL>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t* st1, int e, int m0, int m_end,
-                                          int n0) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t* st1, bf16_t* st2, int e,
+                                          int m0, int m_end, int n0) {
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_M = (BM == 128) ? 2 : 1;
   constexpr int WAVES_N = 4 / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = kBN / WAVES_N;
   constexpr int MI = WM / 32, NI = WN / 32;
+  constexpr int LOADS = BM / 32 + NB * (kBN / 32);  // DMA instructions per wave per chunk
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int K = a.K, N = a.N;
   const bf16_t* A = a.A + (size_t)m0 * K;
@@ -66,10 +70,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
 
-  auto issue = [&](int kc, bf16_t* st) {
-    dma_rows<BM>(A, K, kc * kBK, a_rows, st, wave, lane);
-    dma_rows<kBN>(B0, K, kc * kBK, kBN, st + kARows * 64, wave, lane);
-    if (DUAL) dma_rows<kBN>(B1, K, kc * kBK, kBN, st + (kARows + kBN) * 64, wave, lane);
+  auto issue = [&](int kc, bool live, bf16_t* st) {
+    dma_rows<BM>(A, K, kc * kBK, a_rows, live, st, wave, lane);
+    dma_rows<kBN>(B0, K, kc * kBK, kBN, live, st + kARows * 64, wave, lane);
+    if (DUAL) dma_rows<kBN>(B1, K, kc * kBK, kBN, live, st + (kARows + kBN) * 64, wave, lane);
   };
   auto compute = [&](const bf16_t* st) {
 #pragma unroll
@@ -90,19 +94,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
       }
     }
   };
-
-  const int nK = K / kBK;
-  issue(0, st0);
-  wait_vmcnt<0>();
-  __syncthreads();
-  for (int kc = 0; kc < nK; ++kc) {
-    bf16_t* cur = (kc & 1) ? st1 : st0;
-    bf16_t* nxt = (kc & 1) ? st0 : st1;
-    if (kc + 1 < nK) issue(kc + 1, nxt);
-    compute(cur);
-    wait_vmcnt<0>();
-    __syncthreads();
-  }
+  pipeline3<LOADS>(K / kBK, st0, st1, st2, issue, compute);
 
   // Epilogue. 32x32 accumulator layout: register v of lane l is row
   // 8 * (v / 4) + 4 * (l / 32) + (v % 4), column l % 32 of the MFMA block.
@@ -132,6 +124,7 @@ __global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
   constexpr int STAGE = (kARows + NB * kBN) * 64;
   __shared__ __align__(16) bf16_t st0[STAGE];
   __shared__ __align__(16) bf16_t st1[STAGE];
+  __shared__ __align__(16) bf16_t st2[STAGE];
   __shared__ int s_start[kMaxExperts + 1];
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
@@ -189,9 +182,9 @@ __global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
     const int m0 = s_row0[e] + mt * bm;
     const int m_end = min(m0 + bm, s_row0[e] + rows);
     if (small)
-      gemm_tile<kSmallM, DUAL>(a, st0, st1, e, m0, m_end, nt * kBN);
+      gemm_tile<kSmallM, DUAL>(a, st0, st1, st2, e, m0, m_end, nt * kBN);
     else
-      gemm_tile<128, DUAL>(a, st0, st1, e, m0, m_end, nt * kBN);
+      gemm_tile<128, DUAL>(a, st0, st1, st2, e, m0, m_end, nt * kBN);
   }
 }
 
@@ -303,7 +296,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   if (e != hipSuccess) return e;
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I};
-  grouped_gemm_bf16_kernel<false><<<grid_for(H, 2), 256, 0, s>>>(g2);
+  grouped_gemm_bf16_kernel<false><<<grid_for(H, 1), 256, 0, s>>>(g2);
   return hipGetLastError();
 }
 

@@ -4,6 +4,8 @@
 // GPU counts the picks per expert (the activation profile, Section 4.2.2),
 // gathers the rows routed to its local experts (its token load, Section 4.2.3)
 // and, after the expert FFN, scatters the weighted results back.
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -112,8 +114,8 @@ __device__ __forceinline__ void write_topk(const float (&sel_v)[kMaxTopk], const
 //
 // A block of 4 waves takes 128 tokens; each wave owns 32 tokens and all
 // E_pad = 32 * NCB expert columns. Token rows and router weights are loaded
-// straight into two swizzled LDS stages, one 64-wide K chunk at a time (the
-// loads of chunk k+1 overlap the MFMAs on chunk k).
+// straight into three swizzled LDS stages, one 64-wide K chunk at a time
+// (see pipeline3).
 // ---------------------------------------------------------------------------
 constexpr int kGateBK = 64;
 
@@ -126,8 +128,9 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
   constexpr int STAGE = (128 + BROWS) * 64;
   __shared__ __align__(16) bf16_t st0[STAGE];
   __shared__ __align__(16) bf16_t st1[STAGE];
+  __shared__ __align__(16) bf16_t st2[STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, half = lane >> 5;
   const int row0 = blockIdx.x * 128 + wave * 32;
   const bf16_t* xa = x + (size_t)blockIdx.x * 128 * H;
@@ -138,9 +141,9 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
 #pragma unroll
   for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
 
-  auto issue = [&](int kc, bf16_t* st) {
-    dma_rows<128>(xa, H, kc * kGateBK, a_rows, st, wave, lane);
-    dma_rows<BROWS>(wr, H, kc * kGateBK, E, st + 128 * 64, wave, lane);
+  auto issue = [&](int kc, bool live, bf16_t* st) {
+    dma_rows<128>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
+    dma_rows<BROWS>(wr, H, kc * kGateBK, E, live, st + 128 * 64, wave, lane);
   };
   auto compute = [&](const bf16_t* st) {
 #pragma unroll
@@ -153,18 +156,7 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
                                                          0, 0);
     }
   };
-
-  issue(0, st0);
-  wait_vmcnt<0>();
-  __syncthreads();
-  for (int kc = 0; kc < nK; ++kc) {
-    bf16_t* cur = (kc & 1) ? st1 : st0;
-    bf16_t* nxt = (kc & 1) ? st0 : st1;
-    if (kc + 1 < nK) issue(kc + 1, nxt);
-    compute(cur);
-    wait_vmcnt<0>();
-    __syncthreads();
-  }
+  pipeline3<4 + NCB>(nK, st0, st1, st2, issue, compute);
 
   float bias_r[NCB];
 #pragma unroll
@@ -235,7 +227,7 @@ __global__ __launch_bounds__(256) void gate_topk_f32_kernel(
 // Activation profile: per-block expert counts (LDS atomics on integers, so
 // the result does not depend on their order).
 // ---------------------------------------------------------------------------
-constexpr int kTokPerBlk = 256;
+constexpr int kTokPerBlk = 1024;  // tokens per block of the count table
 
 __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
                                                    int32_t* __restrict__ table) {
@@ -257,7 +249,7 @@ __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ i
 __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ table, int n_blk,
                                                    SlotMap map, int32_t* __restrict__ counts,
                                                    int32_t* __restrict__ offsets,
-                                                   int32_t* __restrict__ bases) {
+                                                   int32_t* __restrict__ bases, int32_t* __restrict__ m_loc) {
   __shared__ int s_cnt[kMaxExperts];
   __shared__ int s_tot[4];
   const int tid = threadIdx.x;
@@ -281,91 +273,99 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
       run += table[(size_t)b * E + my_e];
     }
   }
-  if (tid == 0) offsets[0] = 0;
+  if (tid == 0) {
+    offsets[0] = 0;
+    *m_loc = total;
+  }
 }
 
 // ---------------------------------------------------------------------------
-// Dispatch permutation. Block b re-reads the ids of its 256 tokens; the rank
-// of an assignment within its slot comes from per-wave 64-bit lane masks
-// (order of lanes = order of tokens), never from atomic return order, so
-// the permutation is the stable counting sort and is identical run to run.
-// Each wave then copies its tokens' rows once per local assignment.
+// Dispatch permutation, step 1: positions. Block b re-reads the ids of its
+// 1024 tokens in four rounds of 256 (one token per thread). The rank of an
+// assignment within its slot comes from 64-bit lane masks per (round, wave)
+// -- lane order is token order -- never from atomic return order, so the
+// permutation is the stable counting sort and is identical run to run.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void permute_kernel(
-    const uint4* __restrict__ x, int row_vecs, const int32_t* __restrict__ ids, int T, int k,
-    SlotMap map, const int32_t* __restrict__ bases, int M_cap, uint4* __restrict__ x_perm,
-    int32_t* __restrict__ perm_src, int32_t* __restrict__ dest) {
-  __shared__ unsigned long long s_mask[4][kMaxExperts];
-  __shared__ int s_pre[4][kMaxExperts];
-  __shared__ int s_pos[kTokPerBlk][kMaxTopk];
+constexpr int kRounds = kTokPerBlk / 256;
+
+__global__ __launch_bounds__(256) void permute_index_kernel(const int32_t* __restrict__ ids, int T, int k,
+                                                            SlotMap map, const int32_t* __restrict__ bases,
+                                                            int M_cap, int32_t* __restrict__ perm_src,
+                                                            int32_t* __restrict__ dest) {
+  __shared__ unsigned long long s_mask[kRounds * 4][kMaxExperts];
+  __shared__ int s_pre[kRounds * 4][kMaxExperts];
   __shared__ int16_t s_slot_of[kMaxExperts];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = map.n_experts, L = map.n_local;
-  for (int i = tid; i < 4 * kMaxExperts; i += 256) (&s_mask[0][0])[i] = 0ull;
+  for (int i = tid; i < kRounds * 4 * kMaxExperts; i += 256) (&s_mask[0][0])[i] = 0ull;
   for (int e = tid; e < E; e += 256) s_slot_of[e] = map.slot_of[e];
   __syncthreads();
 
-  const int t = blockIdx.x * kTokPerBlk + tid;
-  int my_slot[kMaxTopk];
-#pragma unroll
-  for (int j = 0; j < kMaxTopk; ++j) {
-    my_slot[j] = -1;
-    if (j < k && t < T) {
-      const int e = ids[(size_t)t * k + j];
-      const int s = ((unsigned)e < (unsigned)E) ? s_slot_of[e] : -1;
-      my_slot[j] = s;
-      if (s >= 0) atomicOr(&s_mask[wave][s], 1ull << lane);
-    }
+  auto slot_of = [&](int t, int j) {
+    const int e = ids[(size_t)t * k + j];
+    return ((unsigned)e < (unsigned)E) ? (int)s_slot_of[e] : -1;
+  };
+  for (int rd = 0; rd < kRounds; ++rd) {
+    const int t = blockIdx.x * kTokPerBlk + rd * 256 + tid;
+    if (t < T)
+      for (int j = 0; j < k; ++j) {
+        const int s = slot_of(t, j);
+        if (s >= 0) atomicOr(&s_mask[rd * 4 + wave][s], 1ull << lane);
+      }
   }
   __syncthreads();
   if (tid < L) {
     int run = 0;
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      s_pre[w][tid] = run;
-      run += __popcll(s_mask[w][tid]);
+    for (int q = 0; q < kRounds * 4; ++q) {
+      s_pre[q][tid] = run;
+      run += __popcll(s_mask[q][tid]);
     }
   }
   __syncthreads();
   const unsigned long long below = (1ull << lane) - 1ull;
-#pragma unroll
-  for (int j = 0; j < kMaxTopk; ++j) {
-    if (j < k) {
-      const int s = my_slot[j];
+  for (int rd = 0; rd < kRounds; ++rd) {
+    const int t = blockIdx.x * kTokPerBlk + rd * 256 + tid;
+    if (t >= T) break;
+    const int q = rd * 4 + wave;
+    for (int j = 0; j < k; ++j) {
+      const int s = slot_of(t, j);
       int pos = -1;
       if (s >= 0) {
-        pos = bases[(size_t)blockIdx.x * L + s] + s_pre[wave][s] + __popcll(s_mask[wave][s] & below);
+        pos = bases[(size_t)blockIdx.x * L + s] + s_pre[q][s] + __popcll(s_mask[q][s] & below);
         if (pos < 0 || pos >= M_cap) pos = -1;
       }
-      if (t < T) {
-        dest[(size_t)t * k + j] = pos;
-        if (pos >= 0) perm_src[pos] = t * k + j;
-      }
-      s_pos[tid][j] = pos;
+      dest[(size_t)t * k + j] = pos;
+      if (pos >= 0) perm_src[pos] = t * k + j;
     }
   }
-  __syncthreads();
+}
 
-  for (int tt = 0; tt < kWave; ++tt) {
-    const int slot_t = wave * kWave + tt;
-    const int tok = blockIdx.x * kTokPerBlk + slot_t;
-    if (tok >= T) break;
-    int pj[kMaxTopk];
-    bool any = false;
-#pragma unroll
-    for (int j = 0; j < kMaxTopk; ++j) {
-      pj[j] = (j < k) ? s_pos[slot_t][j] : -1;
-      any |= pj[j] >= 0;
-    }
-    if (!any) continue;
+// Dispatch permutation, step 2: x_perm[pos] = x[perm_src[pos] / k] for
+// pos < offsets[E_local]. One wave per row, 16-byte vectors, up to eight
+// loads in flight per lane before the stores.
+__global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x, int row_vecs, int T, int k,
+                                                          const int32_t* __restrict__ perm_src,
+                                                          const int32_t* __restrict__ m_loc, int M_cap,
+                                                          uint4* __restrict__ x_perm) {
+  constexpr int U = 8;
+  const int lane = threadIdx.x & 63;
+  const int m = min(max(*m_loc, 0), M_cap);
+  const int waves = gridDim.x * 4;
+  for (int pos = blockIdx.x * 4 + (threadIdx.x >> 6); pos < m; pos += waves) {
+    const int tok = perm_src[pos] / k;
+    if ((unsigned)tok >= (unsigned)T) continue;
     const uint4* src = x + (size_t)tok * row_vecs;
-    for (int v = lane; v < row_vecs; v += kWave) {
-      const uint4 val = src[v];
+    uint4* dst = x_perm + (size_t)pos * row_vecs;
+    int v0 = 0;
+    for (; v0 + U * kWave <= row_vecs; v0 += U * kWave) {
+      uint4 buf[U];
 #pragma unroll
-      for (int j = 0; j < kMaxTopk; ++j)
-        if (pj[j] >= 0) x_perm[(size_t)pj[j] * row_vecs + v] = val;
+      for (int u = 0; u < U; ++u) buf[u] = src[v0 + u * kWave + lane];
+#pragma unroll
+      for (int u = 0; u < U; ++u) dst[v0 + u * kWave + lane] = buf[u];
     }
+    for (int v = v0 + lane; v < row_vecs; v += kWave) dst[v] = src[v];
   }
 }
 
@@ -489,24 +489,28 @@ size_t hist_ws_bytes(int T, int E, int E_local) {
   return ((table + 255) / 256) * 256 + ((bases + 255) / 256) * 256 + 256;
 }
 
-static void hist_ws_split(void* ws, int T, int E, int32_t** table, int32_t** bases) {
+// Workspace: count table [n_blk][E] | row bases [n_blk][E_local] | local total.
+static void hist_ws_split(void* ws, int T, int E, int E_local, int32_t** table, int32_t** bases,
+                          int32_t** m_loc) {
   const size_t n_blk = (size_t)(T + kTokPerBlk - 1) / kTokPerBlk;
   const size_t tb = ((n_blk * E * sizeof(int32_t) + 255) / 256) * 256;
+  const size_t bb = ((n_blk * E_local * sizeof(int32_t) + 255) / 256) * 256;
   *table = static_cast<int32_t*>(ws);
   *bases = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + tb);
+  *m_loc = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + tb + bb);
 }
 
 hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map, int32_t* counts,
                             int32_t* offsets, void* ws, hipStream_t s) {
   const int n_blk = (T + kTokPerBlk - 1) / kTokPerBlk;
-  int32_t *table, *bases;
-  hist_ws_split(ws, T, map.n_experts, &table, &bases);
+  int32_t *table, *bases, *m_loc;
+  hist_ws_split(ws, T, map.n_experts, map.n_local, &table, &bases, &m_loc);
   if (n_blk > 0) {
     hist_kernel<<<n_blk, 256, 0, s>>>(ids, T, k, map.n_experts, table);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  scan_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases);
+  scan_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases, m_loc);
   return hipGetLastError();
 }
 
@@ -515,11 +519,20 @@ hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map,
                           hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int n_blk = (T + kTokPerBlk - 1) / kTokPerBlk;
-  int32_t *table, *bases;
-  hist_ws_split(const_cast<void*>(ws), T, map.n_experts, &table, &bases);
+  int32_t *table, *bases, *m_loc;
+  hist_ws_split(const_cast<void*>(ws), T, map.n_experts, map.n_local, &table, &bases, &m_loc);
+  permute_index_kernel<<<n_blk, 256, 0, s>>>(ids, T, k, map, bases, M_cap, perm_src, dest);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || map.n_local == 0 || M_cap == 0) return e;
   const int row_vecs = (H * (bf16 ? 2 : 4)) / 16;
-  permute_kernel<<<n_blk, 256, 0, s>>>(static_cast<const uint4*>(x), row_vecs, ids, T, k, map, bases, M_cap,
-                                       static_cast<uint4*>(x_perm), perm_src, dest);
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  const long long want = ((long long)M_cap + 3) / 4;
+  const unsigned grid = (unsigned)std::min<long long>(want, (long long)cus * 8);
+  gather_rows_kernel<<<grid, 256, 0, s>>>(static_cast<const uint4*>(x), row_vecs, T, k, perm_src, m_loc, M_cap,
+                                          static_cast<uint4*>(x_perm));
   return hipGetLastError();
 }
 

@@ -89,7 +89,7 @@ def test_histogram_workspace_query(L):
     st, n = _hist(L, np.arange(8), ws=ctypes.c_void_p(None), nbytes=0)
     assert st == 0 and n >= 1 * 8 * 4
     st, n2 = _hist(L, np.arange(8), T=16384, k=8, E=256, ws=ctypes.c_void_p(None), nbytes=0)
-    assert st == 0 and n2 >= 64 * 256 * 4
+    assert st == 0 and n2 >= 256 * 4 and n2 > n
     st, _ = _hist(L, np.arange(8), nbytes=n - 1)
     assert st == WORKSPACE
 
