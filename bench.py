@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--no-extras", action="store_true", help="skip the skew table and load sweep")
     p.add_argument("--sweep-iters", type=int, default=10)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="first run three device-to-device copies of this many MiB (a plain copy kernel of "
+                        "known size, to calibrate HBM byte counters)")
     return p.parse_args()
 
 
@@ -158,6 +161,15 @@ def main():
         stage = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)])) * 1e3
                  for i, n in enumerate(names)}
         return (t1 - t0) * 1e3 / steps, stage
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     bufs = make_bufs(T, x)
     bufs["bias"] = bias

@@ -36,6 +36,30 @@ def command(out: str = LIB, extra=()) -> list:
             "-x", "hip", *srcs, *extra, "-o", out]
 
 
+STAMP = LIB + ".srchash"
+
+
+def source_hash() -> str:
+    """sha256 over every source and header that goes into libmoe.so."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in SOURCES + HEADERS:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    with open(os.path.join(ROOT, "include", "moe.h"), "rb") as fh:
+        h.update(fh.read())
+    return h.hexdigest()
+
+
+def is_fresh() -> bool:
+    """True when libmoe.so was built from the sources as they are now."""
+    try:
+        with open(STAMP) as fh:
+            return os.path.exists(LIB) and fh.read().strip() == source_hash()
+    except OSError:
+        return False
+
+
 def build(verbose: bool = False) -> str:
     """Compile libmoe.so next to this file; returns its path."""
     tmp = LIB + ".tmp"
@@ -50,8 +74,12 @@ def build(verbose: bool = False) -> str:
     if verbose and err.strip():
         print(err, file=sys.stderr)
     os.replace(tmp, LIB)
+    with open(STAMP, "w") as fh:
+        fh.write(source_hash())
     return LIB
 
 
 if __name__ == "__main__":
+    if len(sys.argv) > 1 and sys.argv[1] == "--check":
+        sys.exit(0 if is_fresh() else 1)
     print(build(verbose=True))

@@ -39,16 +39,20 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
 // ---------------------------------------------------------------------------
 // Swizzled LDS tiles filled by direct global->LDS loads.
 //
-// A tile row holds 64 bf16 (128 B = 8 chunks of 16 B). Chunk c of row r is
-// stored at chunk position c ^ (r & 7), so the 32 rows read by one MFMA
-// operand load hit 8 different chunk positions (all 32 banks) per group of
-// 8 lanes, while each wave's load instruction still fills 1 KB (8 rows) of
+// A tile row holds 64 bf16 (128 B = 8 chunks of 16 B). The LDS serves a
+// 128-bit read 16 lanes at a time across 64 banks (256 B), so with 128-byte
+// rows the even rows of an MFMA operand load land in banks 0-31 and the odd
+// rows in banks 32-63. Chunk c of row r is stored at chunk position
+// c ^ ((r >> 1) & 7): the 8 even (and the 8 odd) rows of any 16 consecutive
+// rows then use 8 different chunk positions, so those 16 lanes touch 64
+// different banks. Each wave's load instruction still fills 1 KB (8 rows) of
 // LDS contiguously, as global_load_lds_dwordx4 requires (lane i writes bytes
-// [16 i, 16 i + 16) past the wave-uniform LDS address).
+// [16 i, 16 i + 16) past the wave-uniform LDS address); the swizzle is its own
+// inverse, so the loading lane of position p fetches chunk swz_chunk(r, p).
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-__device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ (row & 7); }
+__device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
 // Loads rows [0, R) (64 bf16 each, starting at column `col0`) of a row-major
 // matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
@@ -56,8 +60,8 @@ __device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ (r
 // so no load leaves the matrix. With live == false every lane reads the
 // first 16 bytes of the matrix instead (one cache line per instruction): the
 // pipelines below issue such a load where no chunk is left, so the number of
-// loads in flight never depends on a branch. R must be a multiple of 32
-// (4 waves x 8 rows).
+// loads in flight never depends on a branch. NW waves share the rows; R must
+// be a multiple of 8 * NW.
 //
 // The load is issued through inline assembly, so the compiler does not track
 // it: every consumer waits for it explicitly (wait_vmcnt + lds_barrier).
@@ -74,12 +78,13 @@ __device__ __forceinline__ void dma16(const void* gaddr, const bf16_t* lds) {
                : "memory");
 }
 
-template <int R>
+template <int R, int NW>
 __device__ __forceinline__ void dma_rows(const bf16_t* __restrict__ src, size_t ld, int col0, int row_limit,
                                          bool live, bf16_t* lds, int wave, int lane) {
+  static_assert(R % (8 * NW) == 0, "rows per wave");
 #pragma unroll
-  for (int i = 0; i < R / 32; ++i) {
-    const int r0 = (i * 4 + wave) * 8;
+  for (int i = 0; i < R / (8 * NW); ++i) {
+    const int r0 = (i * NW + wave) * 8;
     const int r = r0 + (lane >> 3);
     const int c = swz_chunk(r, lane & 7);
     const int rr = r < row_limit ? r : row_limit - 1;
@@ -112,34 +117,29 @@ __device__ __forceinline__ void lds_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// Three-stage K pipeline over 64-wide chunks. issue(kc, live, stage) loads
-// chunk kc into a stage with exactly LOADS load instructions per wave
-// (live == false: a placeholder load, see dma_rows); compute(stage) consumes
-// one stage. Chunk c+2 is requested while the MFMAs work on chunk c, so two
-// chunks are always in flight. The stages are three distinct arrays chosen
-// statically (the loop is unrolled three ways), so the compiler can see that
-// a pending load into one stage does not touch the stage being read and adds
-// no wait of its own. Every wave writes only its own 1 KB slices of a stage.
-template <int LOADS, class Issue, class Compute>
-__device__ __forceinline__ void pipeline3(int nK, bf16_t* st0, bf16_t* st1, bf16_t* st2, Issue&& issue,
-                                          Compute&& compute) {
-  auto step = [&](int c, bf16_t* cur, bf16_t* pf) {
-    wait_vmcnt<LOADS>();  // chunk c landed; chunk c+1 may still be in flight
-    lds_barrier();        // every wave's chunk c landed; every wave is done with chunk c-1
-    issue(c + 2, c + 2 < nK, pf);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(cur);
-  };
+// NS-stage K pipeline over 64-wide chunks held in one LDS array (stage i at
+// smem + i * stage_elems). issue(kc, live, stage) loads chunk kc into a stage
+// with exactly LOADS load instructions per wave (live == false: a placeholder
+// load, see dma_rows); compute(stage) consumes one stage. Chunk c+NS-1 is
+// requested while the MFMAs work on chunk c, so NS-1 chunks are in flight.
+// The loads are invisible to the compiler (dma16), so it adds no waits of its
+// own; each wave writes only its own 1 KB slices of a stage.
+template <int NS, int LOADS, class Issue, class Compute>
+__device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, Issue&& issue,
+                                         Compute&& compute) {
+  static_assert(NS >= 2 && NS <= 4, "stages");
   wait_vmcnt<0>();  // nothing older (e.g. a previous tile's stores) is left in the count
-  issue(0, true, st0);
-  issue(1, 1 < nK, st1);
-  for (int kc = 0;; kc += 3) {
-    step(kc, st0, st2);
-    if (kc + 1 >= nK) break;
-    step(kc + 1, st1, st0);
-    if (kc + 2 >= nK) break;
-    step(kc + 2, st2, st1);
-    if (kc + 3 >= nK) break;
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) issue(i, i < nK, smem + i * stage_elems);
+  int cur = 0;
+  for (int c = 0; c < nK; ++c) {
+    wait_vmcnt<LOADS * (NS - 2)>();  // chunk c landed; the NS-2 newer ones may still be in flight
+    lds_barrier();                   // every wave's chunk c landed; every wave is done with chunk c-1
+    const int pf = (cur == 0 ? NS : cur) - 1;  // stage of chunk c-1 == stage of chunk c+NS-1
+    issue(c + NS - 1, c + NS - 1 < nK, smem + pf * stage_elems);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(smem + cur * stage_elems);
+    cur = (cur + 1 == NS) ? 0 : cur + 1;
   }
   lds_barrier();  // all waves are done reading before the stages are refilled
 }

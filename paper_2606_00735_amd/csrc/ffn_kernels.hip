@@ -17,9 +17,18 @@
 
 namespace moe {
 
-constexpr int kBK = 64;            // K chunk per pipeline stage
-constexpr int kBN = 128;           // output columns per tile
-constexpr int kSmallM = 32;        // experts with at most this many rows use 32-row tiles
+constexpr int kBK = 64;  // K chunk per pipeline stage
+
+// Blocks of 8 waves (two per SIMD, so one wave's LDS waits are covered by
+// the other's MFMAs). Tile classes, chosen per expert from its row count M_e:
+//   small  M_e <= 64    64 x 128 tiles, waves 2x4, 3 stages  (weight streaming)
+//   mid    M_e <= 192  128 x 128 tiles, waves 2x4, 3 stages
+//   large  otherwise   256 x 128 tiles, waves 4x2, 2 stages  (MFMA bound)
+// with 128 output columns per matrix (gate and up both, in the dual GEMM).
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kSmallM = 64;
+constexpr int kMidM = 192;
 
 struct GemmArgs {
   const bf16_t* A;        // [M_cap, K]
@@ -35,24 +44,18 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
   return (g * sig) * u;
 }
 
-// One BM x 128 output tile (two of them, gate and up, when DUAL) over the
-// whole K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from
-// global memory into three swizzled LDS stages. Chunk c+2 is requested while
-// the MFMAs work on chunk c, so two chunks of loads are always in flight.
-// The stages are distinct arrays selected statically (the loop is unrolled
-// three ways), which lets the compiler see that a pending load into one stage
-// does not touch the stage being read.
-constexpr int kARows = 128;  // A rows reserved per stage
-
-template <int BM, bool DUAL>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t* st1, bf16_t* st2, int e,
-                                          int m0, int m_end, int n0) {
+// One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
+// K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
+// memory into NS swizzled LDS stages (see pipeline).
+template <int BM, int BN, int WAVES_M, int NS, bool DUAL>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0) {
   constexpr int NB = DUAL ? 2 : 1;
-  constexpr int WAVES_M = (BM == 128) ? 2 : 1;
-  constexpr int WAVES_N = 4 / WAVES_M;
-  constexpr int WM = BM / WAVES_M, WN = kBN / WAVES_N;
+  constexpr int WAVES_N = kWaves / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int MI = WM / 32, NI = WN / 32;
-  constexpr int LOADS = BM / 32 + NB * (kBN / 32);  // DMA instructions per wave per chunk
+  constexpr int LOADS = (BM + NB * BN) / (8 * kWaves);  // DMA instructions per wave per chunk
+  constexpr int STAGE = (BM + NB * BN) * 64;        // elements per stage
+  static_assert(MI >= 1 && NI >= 1, "wave tile");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -71,9 +74,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
       for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
 
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    dma_rows<BM>(A, K, kc * kBK, a_rows, live, st, wave, lane);
-    dma_rows<kBN>(B0, K, kc * kBK, kBN, live, st + kARows * 64, wave, lane);
-    if (DUAL) dma_rows<kBN>(B1, K, kc * kBK, kBN, live, st + (kARows + kBN) * 64, wave, lane);
+    dma_rows<BM, kWaves>(A, K, kc * kBK, a_rows, live, st, wave, lane);
+    dma_rows<BN, kWaves>(B0, K, kc * kBK, BN, live, st + BM * 64, wave, lane);
+    if (DUAL) dma_rows<BN, kWaves>(B1, K, kc * kBK, BN, live, st + (BM + BN) * 64, wave, lane);
   };
   auto compute = [&](const bf16_t* st) {
 #pragma unroll
@@ -86,7 +89,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
       for (int b = 0; b < NB; ++b) {
 #pragma unroll
         for (int j = 0; j < NI; ++j) {
-          const bf16x8_t bf = lds_frag(st + (kARows + b * kBN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
+          const bf16x8_t bf = lds_frag(st + (BM + b * BN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
 #pragma unroll
           for (int i = 0; i < MI; ++i)
             acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf, acc[b][i][j], 0, 0, 0);
@@ -94,7 +97,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
       }
     }
   };
-  pipeline3<LOADS>(K / kBK, st0, st1, st2, issue, compute);
+  pipeline<NS, LOADS>(K / kBK, smem, STAGE, issue, compute);
 
   // Epilogue. 32x32 accumulator layout: register v of lane l is row
   // 8 * (v / 4) + 4 * (l / 32) + (v % 4), column l % 32 of the MFMA block.
@@ -119,20 +122,36 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* st0, bf16_t
 }
 
 template <bool DUAL>
-__global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
-  constexpr int NB = DUAL ? 2 : 1;
-  constexpr int STAGE = (kARows + NB * kBN) * 64;
-  __shared__ __align__(16) bf16_t st0[STAGE];
-  __shared__ __align__(16) bf16_t st1[STAGE];
-  __shared__ __align__(16) bf16_t st2[STAGE];
+struct GemmShapes {
+  static constexpr int NB = DUAL ? 2 : 1;
+  static constexpr int kSmallStage = (64 + NB * 128) * 64 * 3;
+  static constexpr int kMidStage = (128 + NB * 128) * 64 * 3;
+  static constexpr int kLargeStage = (256 + NB * 128) * 64 * 2;
+  static constexpr int kSmem = kSmallStage > kMidStage ? (kSmallStage > kLargeStage ? kSmallStage : kLargeStage)
+                                                       : (kMidStage > kLargeStage ? kMidStage : kLargeStage);
+};
+
+__device__ __forceinline__ int tile_class(int rows) { return rows <= kSmallM ? 0 : (rows <= kMidM ? 1 : 2); }
+__device__ __forceinline__ int class_rows(int cls) { return cls == 0 ? kSmallM : (cls == 1 ? 128 : 256); }
+
+// Persistent grouped GEMM over every local expert. The grid is a multiple of
+// 8 and block b runs on XCD b % 8; in each round of gridDim.x tiles, the
+// blocks of one XCD take consecutive logical tiles. The logical order walks
+// each expert's row tiles fastest, so the row tiles that share a weight
+// column block run at the same time on one XCD: every weight byte comes from
+// HBM about once, and the rows (a few hundred MB at most) come from the
+// last-level cache.
+template <bool DUAL>
+__global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  using S = GemmShapes<DUAL>;
+  __shared__ __align__(16) bf16_t smem[S::kSmem];
   __shared__ int s_start[kMaxExperts + 1];
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
-  __shared__ int s_tot[4];
+  __shared__ int s_tot[kWaves];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = a.E_local;
-  const int n_nt = a.N / kBN;
 
   // Tile list: rows of each expert, clamped so no access leaves [0, M_cap).
   int tiles = 0;
@@ -143,8 +162,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
     const int rows = o1 - o0;
     s_row0[tid] = o0;
     s_rows[tid] = rows;
-    const int bm = rows <= kSmallM ? kSmallM : 128;
-    tiles = ((rows + bm - 1) / bm) * n_nt;
+    const int bm = class_rows(tile_class(rows));
+    tiles = ((rows + bm - 1) / bm) * (a.N / 128);
   }
   // exclusive scan of tile counts over experts
   int inc = tiles;
@@ -157,14 +176,17 @@ __global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
   __syncthreads();
   int base = 0, total = 0;
 #pragma unroll
-  for (int w = 0; w < 4; ++w) {
+  for (int w = 0; w < kWaves; ++w) {
     if (w < wave) base += s_tot[w];
     total += s_tot[w];
   }
   if (tid < E) s_start[tid] = base + inc - tiles;
   __syncthreads();
 
-  for (int tile = blockIdx.x; tile < total; tile += gridDim.x) {
+  const int G = gridDim.x;
+  const int per_xcd = G >> 3;
+  const int slot = (G & 7) ? (int)blockIdx.x : ((int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3));
+  for (int tile = slot; tile < total; tile += G) {
     // last expert whose first tile is <= tile (experts with no tiles share
     // their start with the next one, so the last match is the owner)
     int lo = 0, hi = E - 1;
@@ -175,16 +197,19 @@ __global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
     const int e = lo;
     const int local = tile - s_start[e];
     const int rows = s_rows[e];
-    const bool small = rows <= kSmallM;
-    const int bm = small ? kSmallM : 128;
+    const int cls = tile_class(rows);
+    const int bm = class_rows(cls);
     const int n_mt = (rows + bm - 1) / bm;
-    const int nt = local / n_mt, mt = local % n_mt;
+    // row tile fastest: all row tiles of a weight column block run together
+    const int nt = local / n_mt, mt = local - nt * n_mt;
     const int m0 = s_row0[e] + mt * bm;
     const int m_end = min(m0 + bm, s_row0[e] + rows);
-    if (small)
-      gemm_tile<kSmallM, DUAL>(a, st0, st1, st2, e, m0, m_end, nt * kBN);
+    if (cls == 0)
+      gemm_tile<64, 128, 2, 3, DUAL>(a, smem, e, m0, m_end, nt * 128);
+    else if (cls == 1)
+      gemm_tile<128, 128, 2, 3, DUAL>(a, smem, e, m0, m_end, nt * 128);
     else
-      gemm_tile<128, DUAL>(a, st0, st1, st2, e, m0, m_end, nt * kBN);
+      gemm_tile<256, 128, 4, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
   }
 }
 
@@ -282,21 +307,22 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   }
   const int cus = device_cu_count();
   // Upper bound on tiles: every expert could need one partial tile plus
-  // ceil(rows / 32) full ones.
-  auto grid_for = [&](int N, int per_cu) {
-    const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / kBN);
-    long long g = (long long)cus * per_cu;
+  // ceil(rows / 32) full ones. The grid is a multiple of 8 (one share per XCD).
+  auto grid_for = [&](int N) {
+    const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128);
+    long long g = cus;  // one 8-wave block per CU
     if (ub < g) g = ub;
+    if (g >= 8) g &= ~7LL;
     return (unsigned)(g < 1 ? 1 : g);
   };
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H};
-  grouped_gemm_bf16_kernel<true><<<grid_for(I, 1), 256, 0, s>>>(g1);
+  grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I};
-  grouped_gemm_bf16_kernel<false><<<grid_for(H, 1), 256, 0, s>>>(g2);
+  grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   return hipGetLastError();
 }
 

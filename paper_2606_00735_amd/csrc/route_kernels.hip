@@ -115,7 +115,7 @@ __device__ __forceinline__ void write_topk(const float (&sel_v)[kMaxTopk], const
 // A block of 4 waves takes 128 tokens; each wave owns 32 tokens and all
 // E_pad = 32 * NCB expert columns. Token rows and router weights are loaded
 // straight into three swizzled LDS stages, one 64-wide K chunk at a time
-// (see pipeline3).
+// (see pipeline).
 // ---------------------------------------------------------------------------
 constexpr int kGateBK = 64;
 
@@ -126,9 +126,7 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
     float* __restrict__ wts) {
   constexpr int BROWS = NCB * 32;
   constexpr int STAGE = (128 + BROWS) * 64;
-  __shared__ __align__(16) bf16_t st0[STAGE];
-  __shared__ __align__(16) bf16_t st1[STAGE];
-  __shared__ __align__(16) bf16_t st2[STAGE];
+  __shared__ __align__(16) bf16_t smem[3 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, half = lane >> 5;
@@ -142,8 +140,8 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
   for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
 
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    dma_rows<128>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
-    dma_rows<BROWS>(wr, H, kc * kGateBK, E, live, st + 128 * 64, wave, lane);
+    dma_rows<128, 4>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
+    dma_rows<BROWS, 4>(wr, H, kc * kGateBK, E, live, st + 128 * 64, wave, lane);
   };
   auto compute = [&](const bf16_t* st) {
 #pragma unroll
@@ -156,7 +154,7 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
                                                          0, 0);
     }
   };
-  pipeline3<4 + NCB>(nK, st0, st1, st2, issue, compute);
+  pipeline<3, 4 + NCB>(nK, smem, STAGE, issue, compute);
 
   float bias_r[NCB];
 #pragma unroll
