@@ -78,23 +78,46 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
     dma_rows<BN, kWaves>(B0, K, kc * kBK, BN, live, st + BM * 64, wave, lane);
     if (DUAL) dma_rows<BN, kWaves>(B1, K, kc * kBK, BN, live, st + (BM + BN) * 64, wave, lane);
   };
+  // Fragments of k-step s+1 are read from LDS before the MFMAs of k-step s
+  // are issued, so the MFMAs never wait on the read that feeds them.
   auto compute = [&](const bf16_t* st) {
+    bf16x8_t af[2][MI], bfr[2][NB][NI];
+    auto read = [&](int s, int buf) {
+      const int chunk = 2 * s + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < MI; ++i) af[buf][i] = lds_frag(st, wm * WM + i * 32 + (lane & 31), chunk);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          bfr[buf][b][j] = lds_frag(st + (BM + b * BN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
+    };
+    constexpr int NREAD = MI + NB * NI, NMFMA = NB * MI * NI;
+    constexpr int PAIRS = NREAD < NMFMA ? NREAD : NMFMA;
+    read(0, 0);
 #pragma unroll
     for (int s = 0; s < kBK / 16; ++s) {
-      const int chunk = 2 * s + (lane >> 5);
-      bf16x8_t af[MI];
+      const bool next = s + 1 < kBK / 16;
+      if (next) read(s + 1, (s + 1) & 1);
 #pragma unroll
-      for (int i = 0; i < MI; ++i) af[i] = lds_frag(st, wm * WM + i * 32 + (lane & 31), chunk);
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-          const bf16x8_t bf = lds_frag(st + (BM + b * BN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
+        for (int j = 0; j < NI; ++j)
 #pragma unroll
           for (int i = 0; i < MI; ++i)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf, acc[b][i][j], 0, 0, 0);
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bfr[s & 1][b][j], acc[b][i][j], 0,
+                                                                   0, 0);
+      // issue order: one MFMA of this step, one LDS read of the next, ...
+      if (next) {
+#pragma unroll
+        for (int q = 0; q < PAIRS; ++q) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         }
+        if (NMFMA > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - PAIRS, 0);
+        if (NREAD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - PAIRS, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);  // each k-step is its own scheduling region
     }
   };
   pipeline<NS, LOADS>(K / kBK, smem, STAGE, issue, compute);
