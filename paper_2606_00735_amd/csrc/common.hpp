@@ -28,8 +28,13 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return static_cast<bf16_t>(u >> 16);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values rounded to bf16 (nearest, ties to even) in one
+// v_cvt_pk_bf16_f32; `lo` lands in the low half.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+  const bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
@@ -39,30 +44,26 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) {
 // ---------------------------------------------------------------------------
 // Swizzled LDS tiles filled by direct global->LDS loads.
 //
-// A tile row holds 64 bf16 (128 B = 8 chunks of 16 B). The LDS serves a
-// 128-bit read 16 lanes at a time across 64 banks (256 B), so with 128-byte
-// rows the even rows of an MFMA operand load land in banks 0-31 and the odd
-// rows in banks 32-63. Chunk c of row r is stored at chunk position
-// c ^ ((r >> 1) & 7): the 8 even (and the 8 odd) rows of any 16 consecutive
-// rows then use 8 different chunk positions, so those 16 lanes touch 64
-// different banks. Each wave's load instruction still fills 1 KB (8 rows) of
-// LDS contiguously, as global_load_lds_dwordx4 requires (lane i writes bytes
-// [16 i, 16 i + 16) past the wave-uniform LDS address); the swizzle is its own
-// inverse, so the loading lane of position p fetches chunk swz_chunk(r, p).
+// A tile row holds BK bf16 (BK = 64: 128 B = 8 chunks of 16 B; BK = 32: 64 B
+// = 4 chunks). The LDS serves a 128-bit read 16 lanes at a time across 64
+// banks (256 B), and an MFMA operand load has 16 lanes read 16 consecutive
+// rows at the same logical chunk. Chunk c of row r is stored at position
+//   BK = 64: c ^ ((r >> 1) & 7)   (even rows in banks 0-31, odd in 32-63)
+//   BK = 32: c ^ ((r >> 2) & 3)   (row r in bank quarter r % 4)
+// so those 16 lanes always touch 16 different 16-byte bank slots. Each
+// wave's load instruction fills 1 KB of LDS contiguously, as
+// global_load_lds_dwordx4 requires (lane i writes bytes [16 i, 16 i + 16)
+// past the wave-uniform LDS address); the swizzle is its own inverse, so the
+// lane that fills position p of row r fetches chunk swz_chunk<BK>(r, p).
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-__device__ __forceinline__ int swz_chunk(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+template <int BK>
+__device__ __forceinline__ int swz_chunk(int row, int chunk) {
+  static_assert(BK == 64 || BK == 32, "chunk width");
+  return BK == 64 ? (chunk ^ ((row >> 1) & 7)) : (chunk ^ ((row >> 2) & 3));
+}
 
-// Loads rows [0, R) (64 bf16 each, starting at column `col0`) of a row-major
-// matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
-// `row_limit` re-read row `row_limit - 1` (their results are never stored),
-// so no load leaves the matrix. With live == false every lane reads the
-// first 16 bytes of the matrix instead (one cache line per instruction): the
-// pipelines below issue such a load where no chunk is left, so the number of
-// loads in flight never depends on a branch. NW waves share the rows; R must
-// be a multiple of 8 * NW.
-//
 // The load is issued through inline assembly, so the compiler does not track
 // it: every consumer waits for it explicitly (wait_vmcnt + lds_barrier).
 // Tracked, the compiler would add a vmcnt(0) before LDS reads it cannot prove
@@ -78,24 +79,36 @@ __device__ __forceinline__ void dma16(const void* gaddr, const bf16_t* lds) {
                : "memory");
 }
 
-template <int R, int NW>
+// Loads rows [0, R) (BK bf16 each, starting at column `col0`) of a row-major
+// matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
+// `row_limit` re-read row `row_limit - 1` (their results are never stored),
+// so no load leaves the matrix. With live == false every lane reads the
+// first 16 bytes of the matrix instead (one cache line per instruction): the
+// pipelines below issue such a load where no chunk is left, so the number of
+// loads in flight never depends on a branch. NW waves share the rows; one
+// instruction covers 1 KB = 1024 / (2 BK) rows; R must be a multiple of
+// NW times that.
+template <int R, int NW, int BK>
 __device__ __forceinline__ void dma_rows(const bf16_t* __restrict__ src, size_t ld, int col0, int row_limit,
                                          bool live, bf16_t* lds, int wave, int lane) {
-  static_assert(R % (8 * NW) == 0, "rows per wave");
+  constexpr int CPR = BK / 8;           // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;         // rows per instruction
+  static_assert(R % (RPI * NW) == 0, "rows per wave");
 #pragma unroll
-  for (int i = 0; i < R / (8 * NW); ++i) {
-    const int r0 = (i * NW + wave) * 8;
-    const int r = r0 + (lane >> 3);
-    const int c = swz_chunk(r, lane & 7);
+  for (int i = 0; i < R / (RPI * NW); ++i) {
+    const int r0 = (i * NW + wave) * RPI;
+    const int r = r0 + lane / CPR;
+    const int c = swz_chunk<BK>(r, lane % CPR);
     const int rr = r < row_limit ? r : row_limit - 1;
     const size_t off = live ? (size_t)rr * ld + col0 + c * 8 : 0;
-    dma16(src + off, lds + r0 * 64);
+    dma16(src + off, lds + r0 * BK);
   }
 }
 
 // 16-byte operand fragment: elements [8 * chunk, 8 * chunk + 8) of tile row `row`.
+template <int BK>
 __device__ __forceinline__ bf16x8_t lds_frag(const bf16_t* lds, int row, int chunk) {
-  return as_bf16x8(*reinterpret_cast<const uint4*>(lds + row * 64 + swz_chunk(row, chunk) * 8));
+  return as_bf16x8(*reinterpret_cast<const uint4*>(lds + row * BK + swz_chunk<BK>(row, chunk) * 8));
 }
 
 // s_waitcnt vmcnt(N) (gfx9 encoding; expcnt and lgkmcnt left unconstrained).
@@ -117,7 +130,7 @@ __device__ __forceinline__ void lds_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// NS-stage K pipeline over 64-wide chunks held in one LDS array (stage i at
+// NS-stage K pipeline over K chunks held in one LDS array (stage i at
 // smem + i * stage_elems). issue(kc, live, stage) loads chunk kc into a stage
 // with exactly LOADS load instructions per wave (live == false: a placeholder
 // load, see dma_rows); compute(stage) consumes one stage. Chunk c+NS-1 is
@@ -127,7 +140,7 @@ __device__ __forceinline__ void lds_barrier() {
 template <int NS, int LOADS, class Issue, class Compute>
 __device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, Issue&& issue,
                                          Compute&& compute) {
-  static_assert(NS >= 2 && NS <= 4, "stages");
+  static_assert(NS >= 2 && NS <= 8, "stages");
   wait_vmcnt<0>();  // nothing older (e.g. a previous tile's stores) is left in the count
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i) issue(i, i < nK, smem + i * stage_elems);

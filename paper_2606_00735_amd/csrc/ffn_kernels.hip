@@ -17,18 +17,33 @@
 
 namespace moe {
 
-constexpr int kBK = 64;  // K chunk per pipeline stage
+constexpr int kBK = 64;  // K chunk per pipeline stage (128-byte tile rows)
 
 // Blocks of 8 waves (two per SIMD, so one wave's LDS waits are covered by
-// the other's MFMAs). Tile classes, chosen per expert from its row count M_e:
-//   small  M_e <= 64    64 x 128 tiles, waves 2x4, 3 stages  (weight streaming)
-//   mid    M_e <= 192  128 x 128 tiles, waves 2x4, 3 stages
-//   large  otherwise   256 x 128 tiles, waves 4x2, 2 stages  (MFMA bound)
+// the other's MFMAs). Tile classes (see row_tiles):
+//   small   64 x 128 tiles, waves 2x4   (weight streaming at small M_e)
+//   mid    128 x 128 tiles, waves 2x4
+//   large  256 x 128 tiles, waves 4x2   (MFMA bound)
 // with 128 output columns per matrix (gate and up both, in the dual GEMM).
+// K advances in 64-wide chunks (whole 128-byte cache lines per tile row);
+// each class keeps as many chunks in flight as 144 KB of LDS allows
+// (Stages below).
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kSmallM = 64;
-constexpr int kMidM = 192;
+constexpr int kDmaRows = kWaves * 1024 / (2 * kBK);  // rows one DMA round of all waves covers
+
+template <int BM, int BN, bool DUAL>
+struct Stages {
+  static constexpr int NB = DUAL ? 2 : 1;
+  static constexpr int AROWS = BM > kDmaRows ? BM : kDmaRows;  // A rows loaded per stage
+  static constexpr int ROWS = AROWS + NB * BN;
+  static constexpr int ELEMS = ROWS * kBK;
+  static constexpr int FIT = (144 * 1024) / (ELEMS * 2);  // stages that fit in 144 KB of LDS
+  static constexpr int NS = FIT < 2 ? 2 : (FIT > 8 ? 8 : FIT);
+  static constexpr int BYTES = ELEMS * 2 * NS;
+  static constexpr int LOADS = ROWS / kDmaRows;  // DMA instructions per wave per chunk
+};
 
 struct GemmArgs {
   const bf16_t* A;        // [M_cap, K]
@@ -44,17 +59,26 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
   return (g * sig) * u;
 }
 
+// SiLU(g) * u for the bf16 path: exp2 and reciprocal on the hardware
+// transcendental unit (v_exp_f32, v_rcp_f32; about 1 ulp of fp32 each), far
+// below the bf16 rounding of h that follows. exp(-g) = exp2(-g * log2 e).
+__device__ __forceinline__ float silu_mul_fast(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(-g * 1.4426950408889634f);
+  const float sig = __builtin_amdgcn_rcpf(1.0f + e);
+  return (g * sig) * u;
+}
+
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
 // K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
 // memory into NS swizzled LDS stages (see pipeline).
-template <int BM, int BN, int WAVES_M, int NS, bool DUAL>
+template <int BM, int BN, int WAVES_M, bool DUAL>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0) {
+  using St = Stages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int MI = WM / 32, NI = WN / 32;
-  constexpr int LOADS = (BM + NB * BN) / (8 * kWaves);  // DMA instructions per wave per chunk
-  constexpr int STAGE = (BM + NB * BN) * 64;        // elements per stage
+  constexpr int AR = St::AROWS;
   static_assert(MI >= 1 && NI >= 1, "wave tile");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -74,9 +98,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
       for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
 
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    dma_rows<BM, kWaves>(A, K, kc * kBK, a_rows, live, st, wave, lane);
-    dma_rows<BN, kWaves>(B0, K, kc * kBK, BN, live, st + BM * 64, wave, lane);
-    if (DUAL) dma_rows<BN, kWaves>(B1, K, kc * kBK, BN, live, st + (BM + BN) * 64, wave, lane);
+    dma_rows<AR, kWaves, kBK>(A, K, kc * kBK, a_rows, live, st, wave, lane);
+    dma_rows<BN, kWaves, kBK>(B0, K, kc * kBK, BN, live, st + AR * kBK, wave, lane);
+    if (DUAL) dma_rows<BN, kWaves, kBK>(B1, K, kc * kBK, BN, live, st + (AR + BN) * kBK, wave, lane);
   };
   // Fragments of k-step s+1 are read from LDS before the MFMAs of k-step s
   // are issued, so the MFMAs never wait on the read that feeds them.
@@ -85,12 +109,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
     auto read = [&](int s, int buf) {
       const int chunk = 2 * s + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < MI; ++i) af[buf][i] = lds_frag(st, wm * WM + i * 32 + (lane & 31), chunk);
+      for (int i = 0; i < MI; ++i) af[buf][i] = lds_frag<kBK>(st, wm * WM + i * 32 + (lane & 31), chunk);
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
-          bfr[buf][b][j] = lds_frag(st + (BM + b * BN) * 64, wn * WN + j * 32 + (lane & 31), chunk);
+          bfr[buf][b][j] = lds_frag<kBK>(st + (AR + b * BN) * kBK, wn * WN + j * 32 + (lane & 31), chunk);
     };
     constexpr int NREAD = MI + NB * NI, NMFMA = NB * MI * NI;
     constexpr int PAIRS = NREAD < NMFMA ? NREAD : NMFMA;
@@ -105,7 +129,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
         for (int j = 0; j < NI; ++j)
 #pragma unroll
           for (int i = 0; i < MI; ++i)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bfr[s & 1][b][j], acc[b][i][j], 0,
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s & 1][b][j], af[s & 1][i], acc[b][i][j], 0,
                                                                    0, 0);
       // issue order: one MFMA of this step, one LDS read of the next, ...
       if (next) {
@@ -120,42 +144,53 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
       __builtin_amdgcn_sched_barrier(0);  // each k-step is its own scheduling region
     }
   };
-  pipeline<NS, LOADS>(K / kBK, smem, STAGE, issue, compute);
+  pipeline<St::NS, St::LOADS>(K / kBK, smem, St::ELEMS, issue, compute);
 
-  // Epilogue. 32x32 accumulator layout: register v of lane l is row
-  // 8 * (v / 4) + 4 * (l / 32) + (v % 4), column l % 32 of the MFMA block.
+  // Epilogue. The MFMAs computed transposed 32x32 blocks (weights as the A
+  // operand): register v of lane l holds output column 8 * (v / 4) +
+  // 4 * (l / 32) + (v % 4) of the block for row (token) l % 32, so each lane
+  // owns 4 consecutive columns per group g = v / 4 and stores them as one
+  // 8-byte write.
 #pragma unroll
-  for (int i = 0; i < MI; ++i)
+  for (int i = 0; i < MI; ++i) {
+    const int row = m0 + wm * WM + i * 32 + (lane & 31);
+    if (row < m_end) {
+      bf16_t* crow = a.C + (size_t)row * N + n0 + wn * WN + 4 * (lane >> 5);
 #pragma unroll
-    for (int j = 0; j < NI; ++j) {
-      const int col = n0 + wn * WN + j * 32 + (lane & 31);
+      for (int j = 0; j < NI; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * WM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (row < m_end) {
-          float r;
-          if (DUAL)
-            r = silu_mul(acc[0][i][j][v], acc[NB - 1][i][j][v]);
-          else
-            r = acc[0][i][j][v];
-          a.C[(size_t)row * N + col] = f32_to_bf16(r);
+        for (int g = 0; g < 4; ++g) {
+          float r[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int v = 4 * g + q;
+            r[q] = DUAL ? silu_mul_fast(acc[0][i][j][v], acc[NB - 1][i][j][v]) : acc[0][i][j][v];
+          }
+          uint2 packed;
+          packed.x = pack_bf16x2(r[0], r[1]);
+          packed.y = pack_bf16x2(r[2], r[3]);
+          *reinterpret_cast<uint2*>(crow + j * 32 + 8 * g) = packed;
         }
-      }
     }
+  }
 }
 
 template <bool DUAL>
 struct GemmShapes {
-  static constexpr int NB = DUAL ? 2 : 1;
-  static constexpr int kSmallStage = (64 + NB * 128) * 64 * 3;
-  static constexpr int kMidStage = (128 + NB * 128) * 64 * 3;
-  static constexpr int kLargeStage = (256 + NB * 128) * 64 * 2;
-  static constexpr int kSmem = kSmallStage > kMidStage ? (kSmallStage > kLargeStage ? kSmallStage : kLargeStage)
-                                                       : (kMidStage > kLargeStage ? kMidStage : kLargeStage);
+  // dual: 128 columns per matrix; single: 128 or 256 columns (see the kernel)
+  static constexpr int BNW = DUAL ? 128 : 256;
+  static constexpr int b0 = Stages<64, BNW, DUAL>::BYTES, b1 = Stages<128, BNW, DUAL>::BYTES;
+  static constexpr int b2 = Stages<256, BNW, DUAL>::BYTES, b3 = Stages<256, 128, DUAL>::BYTES;
+  static constexpr int m01 = b0 > b1 ? b0 : b1, m23 = b2 > b3 ? b2 : b3;
+  static constexpr int kSmem = (m01 > m23 ? m01 : m23) / 2;  // bf16 elements
 };
 
-__device__ __forceinline__ int tile_class(int rows) { return rows <= kSmallM ? 0 : (rows <= kMidM ? 1 : 2); }
-__device__ __forceinline__ int class_rows(int cls) { return cls == 0 ? kSmallM : (cls == 1 ? 128 : 256); }
+// An expert's rows are cut into 256-row tiles; the last one is a 64-, 128- or
+// 256-row tile, whichever is the smallest that holds the remainder (a
+// 300-row expert: one 256-row tile and one 64-row tile). A ragged tail then
+// wastes at most part of its own class's tile.
+__device__ __forceinline__ int row_tiles(int rows) { return (rows + 255) / 256; }
+__device__ __forceinline__ int tile_class(int left) { return left > 128 ? 2 : (left > kSmallM ? 1 : 0); }
 
 // Persistent grouped GEMM over every local expert. The grid is a multiple of
 // 8 and block b runs on XCD b % 8; in each round of gridDim.x tiles, the
@@ -185,8 +220,7 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     const int rows = o1 - o0;
     s_row0[tid] = o0;
     s_rows[tid] = rows;
-    const int bm = class_rows(tile_class(rows));
-    tiles = ((rows + bm - 1) / bm) * (a.N / 128);
+    tiles = row_tiles(rows) * (a.N / 128);  // counted at 128 columns; halved below for 256
   }
   // exclusive scan of tile counts over experts
   int inc = tiles;
@@ -202,6 +236,17 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
   for (int w = 0; w < kWaves; ++w) {
     if (w < wave) base += s_tot[w];
     total += s_tot[w];
+  }
+  // Single-output GEMM: 256-column tiles halve the bytes moved per MFMA but
+  // halve the tile count; use them only when every CU still gets about four
+  // tiles, so the last partial round costs little. Every block sees the same
+  // offsets, so every block makes the same choice.
+  const bool wide = !DUAL && (a.N % 256 == 0) && (total / 2 >= 4 * (int)gridDim.x);
+  if (wide) {
+    total /= 2;
+    base /= 2;
+    inc /= 2;
+    tiles /= 2;
   }
   if (tid < E) s_start[tid] = base + inc - tiles;
   __syncthreads();
@@ -220,19 +265,28 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     const int e = lo;
     const int local = tile - s_start[e];
     const int rows = s_rows[e];
-    const int cls = tile_class(rows);
-    const int bm = class_rows(cls);
-    const int n_mt = (rows + bm - 1) / bm;
+    const int n_mt = row_tiles(rows);
     // row tile fastest: all row tiles of a weight column block run together
     const int nt = local / n_mt, mt = local - nt * n_mt;
-    const int m0 = s_row0[e] + mt * bm;
-    const int m_end = min(m0 + bm, s_row0[e] + rows);
-    if (cls == 0)
-      gemm_tile<64, 128, 2, 3, DUAL>(a, smem, e, m0, m_end, nt * 128);
-    else if (cls == 1)
-      gemm_tile<128, 128, 2, 3, DUAL>(a, smem, e, m0, m_end, nt * 128);
-    else
-      gemm_tile<256, 128, 4, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
+    const int m0 = s_row0[e] + mt * 256;
+    const int left = rows - mt * 256;  // rows from m0 to the expert's end, >= 1
+    const int cls = tile_class(left);
+    const int m_end = m0 + (left < 256 ? left : 256);
+    if (!DUAL && wide) {
+      if (cls == 0)
+        gemm_tile<64, 256, 2, DUAL>(a, smem, e, m0, m_end, nt * 256);
+      else if (cls == 1)
+        gemm_tile<128, 256, 2, DUAL>(a, smem, e, m0, m_end, nt * 256);
+      else
+        gemm_tile<256, 256, 4, DUAL>(a, smem, e, m0, m_end, nt * 256);
+    } else {
+      if (cls == 0)
+        gemm_tile<64, 128, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
+      else if (cls == 1)
+        gemm_tile<128, 128, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
+      else
+        gemm_tile<256, 128, 4, DUAL>(a, smem, e, m0, m_end, nt * 128);
+    }
   }
 }
 

@@ -140,17 +140,17 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
   for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
 
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    dma_rows<128, 4>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
-    dma_rows<BROWS, 4>(wr, H, kc * kGateBK, E, live, st + 128 * 64, wave, lane);
+    dma_rows<128, 4, kGateBK>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
+    dma_rows<BROWS, 4, kGateBK>(wr, H, kc * kGateBK, E, live, st + 128 * 64, wave, lane);
   };
   auto compute = [&](const bf16_t* st) {
 #pragma unroll
     for (int i = 0; i < kGateBK / 16; ++i) {
       const int chunk = 2 * i + half;
-      const bf16x8_t a = lds_frag(st, wave * 32 + r, chunk);
+      const bf16x8_t a = lds_frag<kGateBK>(st, wave * 32 + r, chunk);
 #pragma unroll
       for (int c = 0; c < NCB; ++c)
-        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, lds_frag(st + 128 * 64, c * 32 + r, chunk), acc[c], 0,
+        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, lds_frag<kGateBK>(st + 128 * 64, c * 32 + r, chunk), acc[c], 0,
                                                          0, 0);
     }
   };
