@@ -136,7 +136,9 @@ __device__ __forceinline__ void lds_barrier() {
 // load, see dma_rows); compute(stage) consumes one stage. Chunk c+NS-1 is
 // requested while the MFMAs work on chunk c, so NS-1 chunks are in flight.
 // The loads are invisible to the compiler (dma16), so it adds no waits of its
-// own; each wave writes only its own 1 KB slices of a stage.
+// own; each wave writes only its own 1 KB slices of a stage. On return no
+// load is in flight and every wave is done with the stages, so the caller
+// may reuse the LDS for anything.
 template <int NS, int LOADS, class Issue, class Compute>
 __device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, Issue&& issue,
                                          Compute&& compute) {
@@ -154,7 +156,10 @@ __device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, 
     compute(smem + cur * stage_elems);
     cur = (cur + 1 == NS) ? 0 : cur + 1;
   }
-  lds_barrier();  // all waves are done reading before the stages are refilled
+  // The last steps issued placeholder loads into stages nobody reads; they
+  // must land before the caller reuses the LDS (or refills the stages).
+  wait_vmcnt<0>();
+  lds_barrier();  // all waves are done reading and no load is in flight
 }
 
 // (value, index) ordering of the router: larger value first, then lower index.

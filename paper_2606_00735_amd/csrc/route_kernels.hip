@@ -189,6 +189,95 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Router, bf16, for small batches of few experts (E <= 128): 32 tokens per
+// block, so that a batch of a few thousand tokens still spreads over the
+// CUs. The 4 waves split every 64-wide K chunk (wave w takes k-step w), then
+// sum their partial logits in wave order through LDS. On inputs whose
+// partial sums are exact in fp32 the split gives the same logits as any
+// other order.
+// ---------------------------------------------------------------------------
+template <int NCB>
+__global__ __launch_bounds__(256) void gate_topk_bf16_ksplit_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
+    int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
+    float* __restrict__ wts) {
+  constexpr int BROWS = NCB * 32;
+  constexpr int STAGE = (32 + BROWS) * 64;
+  constexpr int FIT = (96 * 1024) / (STAGE * 2);  // stages in 96 KB: small blocks need depth
+  constexpr int NS = FIT > 8 ? 8 : FIT;
+  constexpr int RED = 4 * NCB * 16 * kWave;  // fp32 partials of all waves
+  constexpr int SMEM_BYTES = (NS * STAGE * 2 > RED * 4) ? NS * STAGE * 2 : RED * 4;
+  __shared__ __align__(16) unsigned char smem_raw[SMEM_BYTES];
+  bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
+  float* red = reinterpret_cast<float*>(smem_raw);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 31, half = lane >> 5;
+  const int row0 = blockIdx.x * 32;
+  const bf16_t* xa = x + (size_t)row0 * H;
+  const int a_rows = T - row0;
+  const int nK = H / kGateBK;
+
+  f32x16_t acc[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
+
+  auto issue = [&](int kc, bool live, bf16_t* st) {
+    dma_rows<32, 4, kGateBK>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
+    dma_rows<BROWS, 4, kGateBK>(wr, H, kc * kGateBK, E, live, st + 32 * 64, wave, lane);
+  };
+  auto compute = [&](const bf16_t* st) {
+    const int chunk = 2 * wave + half;
+    const bf16x8_t a = lds_frag<kGateBK>(st, r, chunk);
+#pragma unroll
+    for (int c = 0; c < NCB; ++c)
+      acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, lds_frag<kGateBK>(st + 32 * 64, c * 32 + r, chunk),
+                                                       acc[c], 0, 0, 0);
+  };
+  pipeline<NS, 1 + NCB>(nK, smem, STAGE, issue, compute);
+
+  // partial logits of wave w -> red[w][c][v][lane]
+#pragma unroll
+  for (int c = 0; c < NCB; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[((wave * NCB + c) * 16 + v) * kWave + lane] = acc[c][v];
+  __syncthreads();
+
+  float bias_r[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    const int col = c * 32 + r;
+    bias_r[c] = (bias != nullptr && col < E) ? bias[col] : 0.0f;
+  }
+  // wave w finishes accumulator registers v = 4w .. 4w+3 (8 of the 32 rows)
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int v = 4 * wave + q;
+    const int row = row0 + 8 * (v >> 2) + 4 * half + (v & 3);
+    float val[NCB];
+#pragma unroll
+    for (int c = 0; c < NCB; ++c) {
+      float z = 0.0f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) z += red[((w * NCB + c) * 16 + v) * kWave + lane];
+      const int col = c * 32 + r;
+      val[c] = (col < E) ? z + bias_r[c] : -__builtin_huge_valf();
+    }
+    if (logits != nullptr && row < T) {
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) {
+        const int col = c * 32 + r;
+        if (col < E) logits[(size_t)row * E + col] = val[c];
+      }
+    }
+    float sel_v[kMaxTopk];
+    int sel_i[kMaxTopk];
+    topk_group<32, NCB>(val, r, E, k, sel_v, sel_i);
+    if (row < T) write_topk(sel_v, sel_i, r, k, row, ids, wts);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Router, fp32: one wave per token, lanes over experts, VALU dot products in
 // ascending h.
 // ---------------------------------------------------------------------------
@@ -457,9 +546,28 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
     return hipGetLastError();
   }
   const int ncb = (E + 31) / 32;
-  const dim3 grid((T + 127) / 128);
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   const bf16_t* wb = static_cast<const bf16_t*>(wr);
+  // Few experts and fewer than 256 blocks of 128 tokens: 32-token blocks with
+  // the K range split over the waves, so more CUs stream x.
+  if (ncb <= 4 && (T + 127) / 128 < 256) {
+    const dim3 g32((T + 31) / 32);
+#define MOE_GATE_KSPLIT(N)                                                                            \
+  case N:                                                                                             \
+    gate_topk_bf16_ksplit_kernel<N><<<g32, 256, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts); \
+    break;
+    switch (ncb) {
+      MOE_GATE_KSPLIT(1)
+      MOE_GATE_KSPLIT(2)
+      MOE_GATE_KSPLIT(3)
+      MOE_GATE_KSPLIT(4)
+      default:
+        return hipErrorInvalidValue;
+    }
+#undef MOE_GATE_KSPLIT
+    return hipGetLastError();
+  }
+  const dim3 grid((T + 127) / 128);
 #define MOE_GATE_CASE(N)                                                                        \
   case N:                                                                                       \
     gate_topk_bf16_kernel<N><<<grid, 256, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts); \
