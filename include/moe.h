@@ -146,7 +146,9 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  * offsets      [E_local+1] int32 (device, from moe_expert_histogram_scan);
  *              clamped to [0, M_cap] inside the kernels
  * y_perm       [M_cap, H] dt, rows [0, offsets[E_local]) written
- * ws           holds h [M_cap, I] dt
+ * ws           holds h [M_cap, I] dt; for bf16 also the fp32 partial sums
+ *              of split-K tiles (used when every expert has at most 64
+ *              rows; summed in a fixed order, so results are deterministic)
  * Limits: 0 <= E_local <= 256 (0 is a no-op); bf16: H % 128 == 0 and
  * I % 128 == 0; fp32: H % 4 == 0 and I % 4 == 0.
  */

@@ -4,14 +4,18 @@
 // Two persistent launches per call:
 //   gate/up:  h[R] = bf16( silu(X_R W_gate^T) * (X_R W_up^T) )   (dual GEMM)
 //   down:     y[R] = bf16( h[R] W_down^T )
-// for each local expert's row range R = [offsets[e], offsets[e+1]).
+// for each local expert's row range R = [offsets[e], offsets[e+1]), each
+// followed by a small reduction that finishes split-K tiles (it returns at
+// once when the GEMM split nothing).
 //
 // Per-expert row counts live only on the device, so each block rebuilds the
 // tile list from `offsets` (a scan over at most 256 experts) and walks it
-// with a grid stride. An expert with M_e <= 32 rows gets 32-row tiles (its
-// cost is streaming its weights once); larger experts get 128-row tiles.
-// Within an expert, consecutive tile indices share a weight column block, so
-// blocks running at the same time read the same weights.
+// with a grid stride. Rows are cut into 256-row tiles plus one 64-, 128- or
+// 256-row remainder tile (row_tiles, tile_class). Within an expert,
+// consecutive tile indices share a weight column block, so blocks running at
+// the same time read the same weights.
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -52,7 +56,21 @@ struct GemmArgs {
   bf16_t* C;              // [M_cap, N]
   const int32_t* offsets; // [E_local + 1]
   int E_local, M_cap, N, K;
+  // Split-K workspace (see the kernel): fp32 partials (part_cap floats) and
+  // the plan the reduction reads. part == nullptr disables split-K.
+  float* part;
+  long long part_cap;
+  int32_t* plan;
 };
+
+// Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
+// plan[0] = S (1: nothing was split), plan[1] = R (rows of split experts),
+// plan[kPlanHead + j] = row of C that compact row j belongs to.
+constexpr int kPlanHead = 64;
+constexpr int kMaxSplit = 8;
+constexpr int kMinSplitChunks = 8;   // K chunks per split, at least
+constexpr int kSplitOverhead = 4;    // per-tile cost of a split tile, in K chunks (fill, epilogue, reduce)
+constexpr long long kPartCapFloats = 16ll << 20;  // 64 MB of fp32 partials at most
 
 __device__ __forceinline__ float silu_mul(float g, float u) {
   const float sig = 1.0f / (1.0f + expf(-g));
@@ -71,8 +89,12 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
 // K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
 // memory into NS swizzled LDS stages (see pipeline).
-template <int BM, int BN, int WAVES_M, bool DUAL>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0) {
+// SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums go to
+// pbase[b * pstride + r * N + n] (r: row within the tile) instead of C.
+template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
+                                          int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
+                                          size_t pstride = 0) {
   using St = Stages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -97,10 +119,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
 
+  if (kc1 < 0) kc1 = K / kBK;
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    dma_rows<AR, kWaves, kBK>(A, K, kc * kBK, a_rows, live, st, wave, lane);
-    dma_rows<BN, kWaves, kBK>(B0, K, kc * kBK, BN, live, st + AR * kBK, wave, lane);
-    if (DUAL) dma_rows<BN, kWaves, kBK>(B1, K, kc * kBK, BN, live, st + (AR + BN) * kBK, wave, lane);
+    const int col = (kc0 + kc) * kBK;
+    dma_rows<AR, kWaves, kBK>(A, K, col, a_rows, live, st, wave, lane);
+    dma_rows<BN, kWaves, kBK>(B0, K, col, BN, live, st + AR * kBK, wave, lane);
+    if (DUAL) dma_rows<BN, kWaves, kBK>(B1, K, col, BN, live, st + (AR + BN) * kBK, wave, lane);
   };
   // Fragments of k-step s+1 are read from LDS before the MFMAs of k-step s
   // are issued, so the MFMAs never wait on the read that feeds them.
@@ -144,13 +168,33 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
       __builtin_amdgcn_sched_barrier(0);  // each k-step is its own scheduling region
     }
   };
-  pipeline<St::NS, St::LOADS>(K / kBK, smem, St::ELEMS, issue, compute);
+  pipeline<St::NS, St::LOADS>(kc1 - kc0, smem, St::ELEMS, issue, compute);
 
   // Epilogue. The MFMAs computed transposed 32x32 blocks (weights as the A
   // operand): register v of lane l holds output column 8 * (v / 4) +
   // 4 * (l / 32) + (v % 4) of the block for row (token) l % 32, so each lane
   // owns 4 consecutive columns per group g = v / 4 and stores them as one
-  // 8-byte write.
+  // 8-byte write (or, for a split-K partial, one 16-byte fp32 write).
+  if (SPLIT) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int r = wm * WM + i * 32 + (lane & 31);  // row within the tile
+      if (m0 + r < m_end) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          float* prow = pbase + b * pstride + (size_t)r * N + n0 + wn * WN + 4 * (lane >> 5);
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<float4*>(prow + j * 32 + 8 * g) =
+                  make_float4(acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
+                              acc[b][i][j][4 * g + 3]);
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int row = m0 + wm * WM + i * 32 + (lane & 31);
@@ -199,59 +243,107 @@ __device__ __forceinline__ int tile_class(int left) { return left > 128 ? 2 : (l
 // column block run at the same time on one XCD: every weight byte comes from
 // HBM about once, and the rows (a few hundred MB at most) come from the
 // last-level cache.
+//
+// Split-K. When every expert has at most 64 rows (decode, or one lightly
+// loaded expert), the cost is streaming the weights, and a launch with fewer
+// tiles than blocks leaves CUs idle. Each tile is then cut into S K ranges
+// whose fp32 sums go to the workspace; split_reduce_kernel adds the S
+// partials of each output in a fixed order (so results do not depend on
+// timing) and applies the epilogue. S in {1, 2, 4, 8} minimises
+// rounds(S) * (chunks per split + a fixed per-tile cost), each split keeping
+// at least kMinSplitChunks K chunks, and only if the partials fit. Every
+// block sees the same offsets, so every block makes the same choice.
+template <int NV>
+__device__ __forceinline__ void block_scan(int (&v)[NV], int (&excl)[NV], int (&total)[NV], int (*s_tot)[kWaves]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int inc[NV];
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    inc[q] = v[q];
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int n = __shfl_up(inc[q], off, kWave);
+      if (lane >= off) inc[q] += n;
+    }
+    if (lane == 63) s_tot[q][wave] = inc[q];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wave) base += s_tot[q][w];
+      tot += s_tot[q][w];
+    }
+    excl[q] = base + inc[q] - v[q];
+    total[q] = tot;
+  }
+}
+
 template <bool DUAL>
 __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a) {
-  using S = GemmShapes<DUAL>;
-  __shared__ __align__(16) bf16_t smem[S::kSmem];
+  using Sh = GemmShapes<DUAL>;
+  constexpr int NB = DUAL ? 2 : 1;
+  __shared__ __align__(16) bf16_t smem[Sh::kSmem];
   __shared__ int s_start[kMaxExperts + 1];
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
-  __shared__ int s_tot[kWaves];
+  __shared__ int s_srow0[kMaxExperts];
+  __shared__ int s_tot[3][kWaves];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int E = a.E_local;
+  const int tid = threadIdx.x;
+  const int E = a.E_local, G = gridDim.x;
 
-  // Tile list: rows of each expert, clamped so no access leaves [0, M_cap).
-  int tiles = 0;
+  // Rows of each expert, clamped so no access leaves [0, M_cap).
+  int rows = 0;
   if (tid < E) {
     int o0 = a.offsets[tid], o1 = a.offsets[tid + 1];
     o0 = min(max(o0, 0), a.M_cap);
     o1 = min(max(o1, o0), a.M_cap);
-    const int rows = o1 - o0;
+    rows = o1 - o0;
     s_row0[tid] = o0;
     s_rows[tid] = rows;
-    tiles = row_tiles(rows) * (a.N / 128);  // counted at 128 columns; halved below for 256
   }
-  // exclusive scan of tile counts over experts
-  int inc = tiles;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    int n = __shfl_up(inc, off, kWave);
-    if (lane >= off) inc += n;
-  }
-  if (lane == 63) s_tot[wave] = inc;
-  __syncthreads();
-  int base = 0, total = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    if (w < wave) base += s_tot[w];
-    total += s_tot[w];
-  }
+  // tiles at 128 columns, rows of small experts, experts above 64 rows
+  int v[3] = {row_tiles(rows) * (a.N / 128), rows <= kSmallM ? rows : 0, rows > kSmallM ? 1 : 0};
+  int ex[3], tot[3];
+  block_scan<3>(v, ex, tot, s_tot);
+  const int T0 = tot[0], R = tot[1], n_big = tot[2];
+
   // Single-output GEMM: 256-column tiles halve the bytes moved per MFMA but
   // halve the tile count; use them only when every CU still gets about four
-  // tiles, so the last partial round costs little. Every block sees the same
-  // offsets, so every block makes the same choice.
-  const bool wide = !DUAL && (a.N % 256 == 0) && (total / 2 >= 4 * (int)gridDim.x);
-  if (wide) {
-    total /= 2;
-    base /= 2;
-    inc /= 2;
-    tiles /= 2;
+  // tiles, so the last partial round costs little.
+  const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 4 * G);
+  int S = 1;
+  if (!wide && n_big == 0 && T0 > 0 && a.part != nullptr) {
+    const int nK = a.K / kBK;
+    long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
+    for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; sp *= 2) {
+      if ((long long)NB * sp * R * a.N > a.part_cap) break;
+      const long long c = (long long)((sp * T0 + G - 1) / G) * ((nK + sp - 1) / sp + kSplitOverhead);
+      if (c < best) {
+        best = c;
+        S = sp;
+      }
+    }
   }
-  if (tid < E) s_start[tid] = base + inc - tiles;
+  const int mul = wide ? 1 : S, div = wide ? 2 : 1;  // tile count per 128-column tile
+  const int total = T0 * mul / div;
+  if (tid < E) {
+    s_start[tid] = ex[0] * mul / div;
+    s_srow0[tid] = ex[1];
+  }
   __syncthreads();
+  if (blockIdx.x == 0) {
+    if (tid == 0) {
+      a.plan[0] = S;
+      a.plan[1] = R;
+    }
+    if (S > 1 && tid < E)
+      for (int r = 0; r < s_rows[tid]; ++r) a.plan[kPlanHead + s_srow0[tid] + r] = s_row0[tid] + r;
+  }
 
-  const int G = gridDim.x;
   const int per_xcd = G >> 3;
   const int slot = (G & 7) ? (int)blockIdx.x : ((int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3));
   for (int tile = slot; tile < total; tile += G) {
@@ -264,12 +356,23 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     }
     const int e = lo;
     const int local = tile - s_start[e];
-    const int rows = s_rows[e];
-    const int n_mt = row_tiles(rows);
+    const int er = s_rows[e];
+    if (S > 1) {
+      // split tile: S consecutive tiles share a column block (every expert
+      // here has one row tile of at most 64 rows)
+      const int nt = local / S, sp = local - nt * S;
+      const int nK = a.K / kBK;
+      const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
+      float* pbase = a.part + ((size_t)sp * R + s_srow0[e]) * a.N;
+      gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, s_row0[e], s_row0[e] + er, nt * 128, kc0, kc1, pbase,
+                                        (size_t)S * R * a.N);
+      continue;
+    }
+    const int n_mt = row_tiles(er);
     // row tile fastest: all row tiles of a weight column block run together
     const int nt = local / n_mt, mt = local - nt * n_mt;
     const int m0 = s_row0[e] + mt * 256;
-    const int left = rows - mt * 256;  // rows from m0 to the expert's end, >= 1
+    const int left = er - mt * 256;  // rows from m0 to the expert's end, >= 1
     const int cls = tile_class(left);
     const int m_end = m0 + (left < 256 ? left : 256);
     if (!DUAL && wide) {
@@ -287,6 +390,48 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
       else
         gemm_tile<256, 128, 4, DUAL>(a, smem, e, m0, m_end, nt * 128);
     }
+  }
+}
+
+// Sums the S split-K partials of every row of a split launch in split order,
+// applies the epilogue (SiLU(gate) * up for the dual GEMM) and writes bf16
+// rows of C. Does nothing when the GEMM before it split nothing.
+template <bool DUAL>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part,
+                                                           const int32_t* __restrict__ plan, int N,
+                                                           bf16_t* __restrict__ C) {
+  const int S = plan[0];
+  if (S <= 1) return;
+  const int R = plan[1];
+  const int n4 = N / 4;
+  const size_t items = (size_t)R * n4, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
+  for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (size_t)gridDim.x * 256) {
+    const int j = (int)(it / n4), c = (int)(it % n4) * 4;
+    const float* p = part + (size_t)j * N + c;
+    float4 g = *reinterpret_cast<const float4*>(p);
+    for (int sp = 1; sp < S; ++sp) {
+      const float4 q = *reinterpret_cast<const float4*>(p + sp * sstride);
+      g.x += q.x;
+      g.y += q.y;
+      g.z += q.z;
+      g.w += q.w;
+    }
+    if (DUAL) {
+      float4 u = *reinterpret_cast<const float4*>(p + bstride);
+      for (int sp = 1; sp < S; ++sp) {
+        const float4 q = *reinterpret_cast<const float4*>(p + bstride + sp * sstride);
+        u.x += q.x;
+        u.y += q.y;
+        u.z += q.z;
+        u.w += q.w;
+      }
+      g = make_float4(silu_mul_fast(g.x, u.x), silu_mul_fast(g.y, u.y), silu_mul_fast(g.z, u.z),
+                      silu_mul_fast(g.w, u.w));
+    }
+    uint2 packed;
+    packed.x = pack_bf16x2(g.x, g.y);
+    packed.y = pack_bf16x2(g.z, g.w);
+    *reinterpret_cast<uint2*>(C + (size_t)plan[kPlanHead + j] * N + c) = packed;
   }
 }
 
@@ -347,9 +492,37 @@ __global__ void set_offsets_kernel(int32_t* offsets, int m) {
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-size_t ffn_ws_bytes(int M_cap, int I, bool bf16) {
-  const size_t h = (size_t)M_cap * I * (bf16 ? 2 : 4);
-  return ((h + 255) / 256) * 256 + 256;
+static size_t round256(size_t n) { return ((n + 255) / 256) * 256; }
+
+// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials. Partial
+// rows exist only for experts of at most 64 rows, so R <= 64 E_local (and
+// <= M_cap for offsets that are a valid scan), and S <= 8. The kernel splits
+// only when its partials fit in part_cap.
+struct FfnWs {
+  size_t h, plan, part;  // byte offsets
+  long long part_cap;    // floats
+  size_t bytes;
+};
+
+static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
+  FfnWs w{};
+  const size_t h = round256((size_t)M_cap * I * (bf16 ? 2 : 4));
+  w.h = 0;
+  if (!bf16) {
+    w.bytes = h + 256;
+    return w;
+  }
+  const long long r_max = std::min<long long>(M_cap, (long long)kSmallM * E_local);
+  const long long need = (long long)kMaxSplit * r_max * std::max(2LL * I, (long long)H);
+  w.part_cap = std::min(need, kPartCapFloats);
+  w.plan = h;
+  w.part = w.plan + round256((size_t)(kPlanHead + (size_t)kSmallM * E_local) * 4);
+  w.bytes = w.part + round256((size_t)w.part_cap * 4) + 256;
+  return w;
+}
+
+size_t ffn_ws_bytes(int M_cap, int E_local, int H, int I, bool bf16) {
+  return ffn_ws_layout(M_cap, E_local, H, I, bf16).bytes;
 }
 
 static int device_cu_count() {
@@ -368,7 +541,9 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
                       void* ws, hipStream_t s) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
-  void* h = ws;
+  const FfnWs L = ffn_ws_layout(M_cap, E_local, H, I, bf16);
+  char* wsb = static_cast<char*>(ws);
+  void* h = wsb + L.h;
   if (!bf16) {
     const size_t n1 = (size_t)M_cap * I, n2 = (size_t)M_cap * H;
     gateup_f32_kernel<<<(unsigned)((n1 + 255) / 256), 256, 0, s>>>(
@@ -383,23 +558,43 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
     return hipGetLastError();
   }
   const int cus = device_cu_count();
-  // Upper bound on tiles: every expert could need one partial tile plus
-  // ceil(rows / 32) full ones. The grid is a multiple of 8 (one share per XCD).
+  // Upper bound on unsplit tiles: every expert could need one partial tile
+  // plus ceil(rows / 64) full ones. The grid is a multiple of 8 (one share
+  // per XCD). A split launch has S times the tiles of a launch with fewer
+  // tiles than blocks, so the grid covers at least 8 of those.
   auto grid_for = [&](int N) {
-    const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128);
+    const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128) * kMaxSplit;
     long long g = cus;  // one 8-wave block per CU
     if (ub < g) g = ub;
     if (g >= 8) g &= ~7LL;
     return (unsigned)(g < 1 ? 1 : g);
   };
+  float* part = reinterpret_cast<float*>(wsb + L.part);
+  int32_t* plan = reinterpret_cast<int32_t*>(wsb + L.plan);
+  // reduce grid: one float4 column group per thread over at most
+  // min(M_cap, 64 E_local) rows, grid-stride beyond 4 blocks per CU
+  auto reduce_grid = [&](int N) {
+    const long long r_max = std::min<long long>(M_cap, (long long)kSmallM * E_local);
+    const long long items = r_max * (N / 4);
+    long long g = (items + 255) / 256;
+    if (g > 4LL * cus) g = 4LL * cus;
+    return (unsigned)(g < 1 ? 1 : g);
+  };
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
-              static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H};
+              static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
+              part, L.part_cap, plan};
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  split_reduce_kernel<true><<<reduce_grid(I), 256, 0, s>>>(part, plan, I, static_cast<bf16_t*>(h));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
-              static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I};
+              static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan};
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
   return hipGetLastError();
 }
 

@@ -22,7 +22,7 @@ hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map,
 hipError_t launch_combine(const void* y, const float* w, const int32_t* dest, int T, int k, int H, int M_cap,
                           bool bf16, void* out, hipStream_t s);
 
-size_t ffn_ws_bytes(int M_cap, int I, bool bf16);
+size_t ffn_ws_bytes(int M_cap, int E_local, int H, int I, bool bf16);
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
                       const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
                       void* ws, hipStream_t s);

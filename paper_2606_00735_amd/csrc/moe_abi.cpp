@@ -145,7 +145,7 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
   moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
   if (st != MOE_OK) return st;
   if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
-  const size_t need = moe::ffn_ws_bytes(M_cap, I, dt == MOE_BF16);
+  const size_t need = moe::ffn_ws_bytes(M_cap, E_local, H, I, dt == MOE_BF16);
   if (ws == nullptr) {
     *ws_bytes = need;
     return MOE_OK;
@@ -187,7 +187,7 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
   moe_status st = ffn_shape_ok(1, H, I, max_m, dt);
   if (st != MOE_OK) return st;
   const bool bf16 = dt == MOE_BF16;
-  const size_t ffn_ws = moe::ffn_ws_bytes(max_m, I, bf16);
+  const size_t ffn_ws = moe::ffn_ws_bytes(max_m, 1, H, I, bf16);
   const size_t need = ffn_ws + 256;
   if (ws == nullptr) {
     *ws_bytes = need;

@@ -184,6 +184,51 @@ def test_ffn_stage_on_oracle_inputs():
     G.check_bf16(G.down(y)[:m], r["y_perm"], "stage y")
 
 
+SPLIT_CASES = [
+    # (H, I, rows per local expert): every expert has at most 64 rows and the
+    # GEMMs have fewer tiles than CUs, so both take the split-K path
+    (1024, 2048, [1, 64, 0, 30], 4),       # gate/up S = 2, down S = 4
+    (4096, 14336, [64], 8),                # Mixtral-shaped expert: gate/up S = 2, down S = 8
+    (4096, 14336, [1], 8),
+    (1024, 2048, [65, 3, 0, 1], 1),        # one expert above 64 rows: no split
+]
+
+
+def _down_split_factor(ws, M_cap, I):
+    """S of the last (down) GEMM, from the split-K plan that follows h in the
+    workspace (white-box: shows which path a case exercised)."""
+    off = ((M_cap * I * 2 + 255) // 256) * 256
+    return int(ws[off:off + 4].view(torch.int32).item())
+
+
+@pytest.mark.parametrize("H,I,rows,S_down", SPLIT_CASES,
+                         ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}" for h, i, r, _ in SPLIT_CASES])
+def test_ffn_split_k(H, I, rows, S_down):
+    banner("stage ffn split-K", H, I, rows, "seed 5")
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="split", H=H, I=I, E=len(rows), k=1,
+                                E_local=len(rows))
+    wg, wu, wd = make_experts(shape, list(range(len(rows))), seed=5)
+    m = sum(rows)
+    x, *_ = make_router(shape, m, 0.0, seed=5)
+    offsets = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    M_cap = m + 3
+    xp = np.zeros((M_cap, H), np.float32)
+    xp[:m] = x
+    h_ref, y_ref = O.grouped_swiglu_ffn(x, wg, wu, wd, offsets, bf16=True)
+    dg, du, dd = (G.up(w, torch.bfloat16) for w in (wg, wu, wd))
+    dx, doff = G.up(xp, torch.bfloat16), G.up_i32(offsets)
+    y, ws = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff)
+    torch.cuda.synchronize()
+    assert _down_split_factor(ws, M_cap, I) == S_down
+    h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
+    G.check_bf16(h, h_ref, "split h")
+    G.check_bf16(G.down(y)[:m], y_ref, "split y", scale=G.down_scale(h_ref, wd, offsets))
+    # the split partials are summed in a fixed order: a second call is bitwise equal
+    y2, _ = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y2[:m], y[:m])
+
+
 def test_combine_stage_on_oracle_inputs():
     banner("stage combine qwen3")
     li = make_layer("qwen3", 64, 1.0, seed=4)
