@@ -118,6 +118,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// s_waitcnt lgkmcnt(0) (vmcnt and expcnt left unconstrained): every LDS
+// read of this wave has returned its data.
+__device__ __forceinline__ void wait_lgkmcnt0() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));
+}
+
 // Workgroup barrier for the LDS pipelines. __syncthreads() adds a release
 // fence, which makes the compiler drain every outstanding global load
 // (vmcnt(0)) before the barrier, prefetches included. The pipelines instead
@@ -158,6 +164,64 @@ __device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, 
   }
   // The last steps issued placeholder loads into stages nobody reads; they
   // must land before the caller reuses the LDS (or refills the stages).
+  wait_vmcnt<0>();
+  lds_barrier();  // all waves are done reading and no load is in flight
+}
+
+// The same pipeline for consumers that read their operands from LDS one
+// k-step ahead of the MFMAs that use them, across chunk boundaries too. A
+// chunk holds KS k-steps (KS even); read(stage, s, buf) loads the fragments of
+// k-step s into register buffer buf, mma(buf) issues one k-step's MFMAs from
+// buffer buf (k-step s always uses buffer s % 2), and mix() orders the LDS
+// reads and MFMAs of one k-step (sched_group_barrier hints).
+//
+// The wait for chunk c+1 and the barrier come before the last k-step of
+// chunk c, whose operands are already in registers: after the barrier the
+// wave issues the next load, the first reads of chunk c+1 and the MFMAs of
+// that last k-step together, so the MFMAs never wait for a read issued after
+// a barrier. Before the barrier each wave waits for its own reads of chunk c
+// (lgkmcnt), so the load issued into that stage right after it cannot
+// overwrite data still being read. NS-1 chunks are in flight during each
+// chunk's MFMAs, as in pipeline(). On return no load is in flight and every
+// wave is done with the stages.
+template <int NS, int LOADS, int KS, class Issue, class Read, class Mma, class Mix>
+__device__ __forceinline__ void pipeline_xk(int nK, bf16_t* smem, int stage_elems, Issue&& issue, Read&& read,
+                                            Mma&& mma, Mix&& mix) {
+  static_assert(NS >= 2 && NS <= 8, "stages");
+  static_assert(KS >= 2 && KS % 2 == 0, "k-steps per chunk");
+  wait_vmcnt<0>();  // nothing older (e.g. a previous tile's stores) is left in the count
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i) issue(i, i < nK, smem + i * stage_elems);
+  wait_vmcnt<LOADS * (NS - 2)>();  // chunk 0 landed
+  lds_barrier();
+  issue(NS - 1, NS - 1 < nK, smem + (NS - 1) * stage_elems);  // stage NS-1 holds nothing yet
+  read(smem, 0, 0);
+  int cur = 0;
+  for (int c = 0; c < nK; ++c) {
+    const bf16_t* st = smem + cur * stage_elems;
+    const int nxt = (cur + 1 == NS) ? 0 : cur + 1;
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s + 1 < KS; ++s) {
+      read(st, s + 1, (s + 1) & 1);
+      mma(s & 1);
+      mix();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // chunks c+1 .. c+NS-1 are in flight
+    wait_lgkmcnt0();                 // this wave's reads of chunk c returned
+    wait_vmcnt<LOADS * (NS - 2)>();  // chunk c+1 landed
+    lds_barrier();                   // every wave: chunk c+1 landed, chunk c read
+    issue(c + NS, c + NS < nK, smem + cur * stage_elems);
+    __builtin_amdgcn_sched_barrier(0);
+    // first fragments of chunk c+1 (after the last chunk: an unused read of a
+    // stage that holds a placeholder load; LDS reads cannot fault)
+    read(smem + nxt * stage_elems, 0, 0);
+    mma((KS - 1) & 1);
+    mix();
+    __builtin_amdgcn_sched_barrier(0);
+    cur = nxt;
+  }
   wait_vmcnt<0>();
   lds_barrier();  // all waves are done reading and no load is in flight
 }

@@ -87,8 +87,8 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 }
 
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
-// K range: 4 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
-// memory into NS swizzled LDS stages (see pipeline).
+// K range: 8 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
+// memory into NS swizzled LDS stages (see pipeline_xk).
 // SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums go to
 // pbase[b * pstride + r * N + n] (r: row within the tile) instead of C.
 template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
@@ -126,49 +126,41 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
     dma_rows<BN, kWaves, kBK>(B0, K, col, BN, live, st + AR * kBK, wave, lane);
     if (DUAL) dma_rows<BN, kWaves, kBK>(B1, K, col, BN, live, st + (AR + BN) * kBK, wave, lane);
   };
-  // Fragments of k-step s+1 are read from LDS before the MFMAs of k-step s
-  // are issued, so the MFMAs never wait on the read that feeds them.
-  auto compute = [&](const bf16_t* st) {
-    bf16x8_t af[2][MI], bfr[2][NB][NI];
-    auto read = [&](int s, int buf) {
-      const int chunk = 2 * s + (lane >> 5);
+  // Operands of k-step s+1 are read from LDS while the MFMAs of k-step s
+  // run (register double buffering), across chunks too (pipeline_xk).
+  bf16x8_t af[2][MI], bfr[2][NB][NI];
+  auto read = [&](const bf16_t* st, int s, int buf) {
+    const int chunk = 2 * s + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < MI; ++i) af[buf][i] = lds_frag<kBK>(st, wm * WM + i * 32 + (lane & 31), chunk);
+    for (int i = 0; i < MI; ++i) af[buf][i] = lds_frag<kBK>(st, wm * WM + i * 32 + (lane & 31), chunk);
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int j = 0; j < NI; ++j)
-          bfr[buf][b][j] = lds_frag<kBK>(st + (AR + b * BN) * kBK, wn * WN + j * 32 + (lane & 31), chunk);
-    };
+      for (int j = 0; j < NI; ++j)
+        bfr[buf][b][j] = lds_frag<kBK>(st + (AR + b * BN) * kBK, wn * WN + j * 32 + (lane & 31), chunk);
+  };
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[buf][b][j], af[buf][i], acc[b][i][j], 0, 0, 0);
+  };
+  // issue order within a k-step: one MFMA, one LDS read, ...
+  auto mix = [&]() {
     constexpr int NREAD = MI + NB * NI, NMFMA = NB * MI * NI;
     constexpr int PAIRS = NREAD < NMFMA ? NREAD : NMFMA;
-    read(0, 0);
 #pragma unroll
-    for (int s = 0; s < kBK / 16; ++s) {
-      const bool next = s + 1 < kBK / 16;
-      if (next) read(s + 1, (s + 1) & 1);
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int i = 0; i < MI; ++i)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[s & 1][b][j], af[s & 1][i], acc[b][i][j], 0,
-                                                                   0, 0);
-      // issue order: one MFMA of this step, one LDS read of the next, ...
-      if (next) {
-#pragma unroll
-        for (int q = 0; q < PAIRS; ++q) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-        }
-        if (NMFMA > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - PAIRS, 0);
-        if (NREAD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - PAIRS, 0);
-      }
-      __builtin_amdgcn_sched_barrier(0);  // each k-step is its own scheduling region
+    for (int q = 0; q < PAIRS; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
     }
+    if (NMFMA > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - PAIRS, 0);
+    if (NREAD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - PAIRS, 0);
   };
-  pipeline<St::NS, St::LOADS>(kc1 - kc0, smem, St::ELEMS, issue, compute);
+  pipeline_xk<St::NS, St::LOADS, kBK / 16>(kc1 - kc0, smem, St::ELEMS, issue, read, mma, mix);
 
   // Epilogue. The MFMAs computed transposed 32x32 blocks (weights as the A
   // operand): register v of lane l holds output column 8 * (v / 4) +
