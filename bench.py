@@ -10,8 +10,8 @@ workload is the Mixtral-8x7B-shaped layer (H=4096, I=14336, 8 experts all on
 this GPU, top-2, bf16) at T=4096 tokens with rank-bias skew alpha=1.0.
 
 Prints ONE JSON line: whole-layer throughput (algorithmic TFLOP/s), per-stage
-HIP-event times, the roofline of the dominant step (the grouped SwiGLU FFN,
-two kernel launches), a skew table, the per-expert latency-vs-load sweep,
+HIP-event times, the roofline of the dominant step (the grouped SwiGLU FFN
+call: two GEMM launches, each followed by its split-K reduction), a skew table, the per-expert latency-vs-load sweep,
 and the CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -95,8 +95,8 @@ def traffic_from_profile(workload_key):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU's expert shard; runs on more than one GPU are not "
-              "part of this build (the expert-parallel exchange is a design note only).", file=sys.stderr)
+        print("bench.py measures one GPU's share of the expert-parallel layer and runs on one GPU "
+              "only (--gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -184,7 +184,7 @@ def main():
     mfma_bound = w["ffn_flops"] / (peak_f * 1e12) >= w["ffn_bytes"] / (PEAK_HBM_GBPS * 1e9)
     wkey = f"{args.config}-T{T}-a{args.alpha:g}-s{args.seed}"
     roofline = {
-        "kernel": "moe_grouped_swiglu_ffn (gate/up + down launches)",
+        "kernel": "moe_grouped_swiglu_ffn (gate/up and down GEMMs + split-K reductions)",
         "bound": "mfma" if mfma_bound else "hbm",
         "achieved": round(ffn_tflops if mfma_bound else ffn_gbps, 3),
         "peak": peak_f if mfma_bound else PEAK_HBM_GBPS,
