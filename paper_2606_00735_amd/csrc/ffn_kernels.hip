@@ -241,7 +241,7 @@ __device__ __forceinline__ int tile_class(int left) { return left > 128 ? 2 : (l
 // tiles than blocks leaves CUs idle. Each tile is then cut into S K ranges
 // whose fp32 sums go to the workspace; split_reduce_kernel adds the S
 // partials of each output in a fixed order (so results do not depend on
-// timing) and applies the epilogue. S in {1, 2, 4, 8} minimises
+// timing) and applies the epilogue. S in 1..8 minimises
 // rounds(S) * (chunks per split + a fixed per-tile cost), each split keeping
 // at least kMinSplitChunks K chunks, and only if the partials fit. Every
 // block sees the same offsets, so every block makes the same choice.
@@ -311,7 +311,7 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
   if (!wide && n_big == 0 && T0 > 0 && a.part != nullptr) {
     const int nK = a.K / kBK;
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
-    for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; sp *= 2) {
+    for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
       if ((long long)NB * sp * R * a.N > a.part_cap) break;
       const long long c = (long long)((sp * T0 + G - 1) / G) * ((nK + sp - 1) / sp + kSplitOverhead);
       if (c < best) {
@@ -578,15 +578,19 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  split_reduce_kernel<true><<<reduce_grid(I), 256, 0, s>>>(part, plan, I, static_cast<bf16_t*>(h));
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // A GEMM can split only if its K range holds two splits of kMinSplitChunks.
+  const bool split_gu = H / kBK >= 2 * kMinSplitChunks, split_dn = I / kBK >= 2 * kMinSplitChunks;
+  if (split_gu) {
+    split_reduce_kernel<true><<<reduce_grid(I), 256, 0, s>>>(part, plan, I, static_cast<bf16_t*>(h));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan};
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
+  if (split_dn) split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
   return hipGetLastError();
 }
 

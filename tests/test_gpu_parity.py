@@ -191,6 +191,10 @@ SPLIT_CASES = [
     (4096, 14336, [64], 8),                # Mixtral-shaped expert: gate/up S = 2, down S = 8
     (4096, 14336, [1], 8),
     (1024, 2048, [65, 3, 0, 1], 1),        # one expert above 64 rows: no split
+    (7168, 2048, [1, 33], 2),              # DSV3-shaped experts: gate/up S = 8, down S = 2
+    (7168, 2048, [1], 4),                  # one DSV3-shaped expert: gate/up S = 8, down S = 4
+    (5120, 8192, [1], 6),                  # Maverick-shaped expert: gate/up S = 4, down S = 6
+    (2048, 768, [5], 1),                   # Qwen3-shaped: gate/up S = 4; the down GEMM (K = 768) cannot split
 ]
 
 
