@@ -1,7 +1,8 @@
-"""CPU oracle for the MoE expert-shard layer. TEST INFRASTRUCTURE ONLY.
+"""CPU oracles for the MoE expert-shard layer and for ViBE's placement control
+path. TEST INFRASTRUCTURE ONLY.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package. It shares no code with the HIP path
 (``paper_2606_00735_amd``) and the HIP path never imports it.
 """
-from . import moe_oracle, bruteforce  # noqa: F401
+from . import moe_oracle, bruteforce, placement_oracle  # noqa: F401
