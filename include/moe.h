@@ -198,6 +198,105 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up,
                           void* y_scratch, void* ws, size_t* ws_bytes,
                           float* us_out, float* us_all, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Placement control path (Section 4.2, Algorithms 1 and 2): the per-GPU
+ * latency model f_g, the latency-aware greedy placement, the drift detector
+ * and the incremental swap solver, for L MoE layers of E experts on G GPUs.
+ *
+ * Latency models: G models of nk knots each, knots_n [G, nk] and knots_t
+ * [G, nk] fp64 (DEVICE arrays), knots_n strictly increasing and positive,
+ * knots_t non-decreasing (moe_fit_latency_model builds them). f(n) = 0 for
+ * n <= 0, knots_t[0] for 0 < n <= knots_n[0], linear between knots, and the
+ * last segment's slope beyond the last knot (knots_t[0] n / knots_n[0] with
+ * one knot). Knots that break these rules give unspecified placements but no
+ * out-of-bounds access.
+ *
+ * Determinism: every decision is taken in fp64 with separately rounded
+ * operations and sums in ascending index order; ties go to the lower GPU
+ * index and, among experts, to the lower expert id. Limits: 1 <= E <= 1024,
+ * 1 <= G <= 64, 1 <= nk <= 64, L >= 0 (0 is a no-op).
+ * ---------------------------------------------------------------------- */
+
+/*
+ * moe_fit_latency_model - knots of f_g from measured points (HOST only,
+ * launches nothing).
+ *
+ * Section 4.2.1: f_g(n) maps token load to kernel latency. loads [n] (HOST,
+ * distinct, positive) and latencies [n] (HOST, finite) are the measured
+ * points, e.g. one moe_load_sweep; the knots are the loads in ascending
+ * order and the running maximum of the latencies in that order, so f is
+ * monotone. knots_n, knots_t: HOST [n] outputs. 1 <= n <= 64.
+ */
+moe_status moe_fit_latency_model(const int32_t* loads, const float* latencies, int n,
+                                 double* knots_n, double* knots_t);
+
+/*
+ * moe_place_greedy - initial latency-aware placement (Algorithm 1, Phase 2).
+ *
+ * Per layer l: N = sum_e w[l,e]; speeds s_g = 1 / f_g(N / E) (1 when N = 0);
+ * token targets tau_g = N s_g / sum_h s_h; experts in descending load order
+ * (ascending id among equal loads) each go to the GPU with the largest
+ * tau_g - n_g among those holding fewer than `cap` experts (cap = 0: no
+ * limit), whose load n_g then grows by the expert's load.
+ *
+ * w        [L, E] fp64 per-expert loads (DEVICE)
+ * assign   [L, E] int32 (DEVICE): the GPU of each expert
+ * loads    [L, G] fp64 (DEVICE) or NULL: final n_g
+ * targets  [L, G] fp64 (DEVICE) or NULL: tau_g
+ * cap: 0, or cap * G >= E.
+ */
+moe_status moe_place_greedy(const double* w, int L, int E, const double* knots_n,
+                            const double* knots_t, int G, int nk, int cap, int32_t* assign,
+                            double* loads, double* targets, hipStream_t stream);
+
+/*
+ * moe_place_incremental - incremental placement update (Algorithm 2).
+ *
+ * Per layer, starting from `assign` (DEVICE [L, E] int32, in/out; entries
+ * outside [0, G) are read as GPU 0): while the largest f_g(n_g) exceeds
+ * (1 + eps) times the mean of f_g(n_g) over the G GPUs, take the slowest GPU
+ * g+ and the fastest g- and apply the swap of one expert of g+ with one of
+ * g- that lowers max(f_g+(n_g+), f_g-(n_g-)) the most (first in ascending
+ * expert ids on ties); stop when none lowers it or after max_swaps swaps.
+ * Expert counts per GPU are kept.
+ *
+ * w        [L, E] fp64 loads (DEVICE)
+ * n_swaps  [L] int32 (DEVICE) or NULL: swaps applied per layer
+ * eps >= 0 finite; 0 <= max_swaps <= 1 << 20.
+ */
+moe_status moe_place_incremental(const double* w, int L, int E, const double* knots_n,
+                                 const double* knots_t, int G, int nk, double eps, int max_swaps,
+                                 int32_t* assign, int32_t* n_swaps, hipStream_t stream);
+
+/*
+ * moe_window_push - add one forward pass's per-layer expert counts to a
+ * sliding window (Section 4.2.4: load vectors averaged over a window of
+ * samples).
+ *
+ * ring [window, L, E] int32 and sums [L, E] fp64 (DEVICE) are the caller's
+ * state, zeroed by the caller before the first push; slot = the ring entry
+ * this pass replaces (the caller cycles it 0, 1, ..., window - 1, 0, ...).
+ * sums += counts - ring[slot]; ring[slot] = counts. Exact for counts below
+ * 2^53 / window. counts [L, E] int32 (DEVICE), e.g. the histogram's counts
+ * of each layer. 1 <= window, 0 <= slot < window.
+ */
+moe_status moe_window_push(const int32_t* counts, int32_t* ring, double* sums, int L, int E,
+                           int window, int slot, hipStream_t stream);
+
+/*
+ * moe_drift_distance - drift test (Section 4.2.4).
+ *
+ * d[l] = 1 - w_cur[l].w_ref[l] / (|w_cur[l]| |w_ref[l]|) (0 if both vectors
+ * are zero, 1 if exactly one is), sums in ascending expert id; *trigger =
+ * 1 if any d[l] > delta, else 0.
+ *
+ * w_cur, w_ref [L, E] fp64 (DEVICE; window sums or means: the distance does
+ * not depend on scale); d [L] fp64 (DEVICE); trigger [1] int32 (DEVICE) or
+ * NULL. delta finite. L <= 65536.
+ */
+moe_status moe_drift_distance(const double* w_cur, const double* w_ref, int L, int E, double delta,
+                              double* d, int32_t* trigger, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -3,7 +3,9 @@
 The computation ViBE (arXiv 2606.00735) balances across GPUs: top-k gating,
 the per-expert activation profile, dispatch permutation, grouped SwiGLU
 expert FFN, weighted combine, and the per-expert latency-vs-load sweep from
-which the per-GPU performance model f_g(n) is fitted. Every step runs in the
+which the per-GPU performance model f_g(n) is fitted, and ViBE's placement
+control path on top of it (latency-aware greedy placement, drift detector,
+incremental swap solver). Every step runs in the
 HIP kernels of ``libmoe.so`` (C ABI in ``include/moe.h``); this package only
 marshals torch tensors into those calls.
 """
@@ -15,11 +17,16 @@ from ._lib import (  # noqa: F401
     ffn_ws_bytes,
     hist_ws_bytes,
     load_library,
+    moe_drift_distance,
     moe_expert_histogram_scan,
+    moe_fit_latency_model,
     moe_gate_topk,
     moe_grouped_swiglu_ffn,
     moe_layer,
     moe_load_sweep,
     moe_permute,
+    moe_place_greedy,
+    moe_place_incremental,
     moe_unpermute_combine,
+    moe_window_push,
 )

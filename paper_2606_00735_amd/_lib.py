@@ -22,7 +22,9 @@ MOE_F32, MOE_BF16 = 0, 1
 MAX_EXPERTS, MAX_TOPK = 256, 16
 
 EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert_histogram_scan",
-            "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep")
+            "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep",
+            "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_window_push",
+            "moe_drift_distance")
 
 
 class MoeError(RuntimeError):
@@ -63,6 +65,17 @@ def load_library(path: str = LIB_PATH):
     L.moe_unpermute_combine.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P]
     L.moe_load_sweep.restype = _I
     L.moe_load_sweep.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P, _P]
+    _D = ctypes.c_double
+    L.moe_fit_latency_model.restype = _I
+    L.moe_fit_latency_model.argtypes = [_P, _P, _I, _P, _P]
+    L.moe_place_greedy.restype = _I
+    L.moe_place_greedy.argtypes = [_P, _I, _I, _P, _P, _I, _I, _I, _P, _P, _P, _P]
+    L.moe_place_incremental.restype = _I
+    L.moe_place_incremental.argtypes = [_P, _I, _I, _P, _P, _I, _I, _D, _I, _P, _P, _P]
+    L.moe_window_push.restype = _I
+    L.moe_window_push.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P]
+    L.moe_drift_distance.restype = _I
+    L.moe_drift_distance.argtypes = [_P, _P, _I, _I, _D, _P, _P, _P]
     if L.moe_abi_version() != 1:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
@@ -293,3 +306,83 @@ def ffn_hidden(ws, M_cap, I, dtype):
     """View of the expert hidden activations h [M_cap, I] held in an FFN workspace."""
     es = 2 if dtype == torch.bfloat16 else 4
     return ws[: M_cap * I * es].view(dtype).view(M_cap, I)
+
+
+# ---------------------------------------------------------------------------
+# Placement control path (latency model, greedy placement, drift, swaps)
+# ---------------------------------------------------------------------------
+def moe_fit_latency_model(loads, latencies):
+    """Knots (n, t) of a monotone latency model from measured points (host)."""
+    L = load_library()
+    ld = np.ascontiguousarray(np.asarray(loads, dtype=np.int32))
+    lt = np.ascontiguousarray(np.asarray(latencies, dtype=np.float32))
+    if ld.shape != lt.shape or ld.ndim != 1:
+        raise ValueError("loads and latencies must be 1-D of equal length")
+    kn = np.zeros(len(ld), np.float64)
+    kt = np.zeros(len(ld), np.float64)
+    st = L.moe_fit_latency_model(ld.ctypes.data_as(_P), lt.ctypes.data_as(_P), len(ld), kn.ctypes.data_as(_P),
+                                 kt.ctypes.data_as(_P))
+    _check("moe_fit_latency_model", st)
+    return kn, kt
+
+
+def _models(knots_n, knots_t):
+    if knots_n.dim() != 2 or knots_n.shape != knots_t.shape:
+        raise ValueError("knots_n and knots_t must both be [G, nk]")
+    return _dev(knots_n, "knots_n", torch.float64), _dev(knots_t, "knots_t", torch.float64), *knots_n.shape
+
+
+def moe_place_greedy(w, knots_n, knots_t, cap=0, assign=None, loads=None, targets=None):
+    """Latency-aware greedy placement of every layer. Returns (assign [L,E] int32,
+    loads [L,G] fp64, targets [L,G] fp64)."""
+    L = load_library()
+    nl, E = w.shape
+    kn, kt, G, nk = _models(knots_n, knots_t)
+    assign = torch.empty((nl, E), dtype=torch.int32, device=w.device) if assign is None else assign
+    loads = torch.empty((nl, G), dtype=torch.float64, device=w.device) if loads is None else loads
+    targets = torch.empty((nl, G), dtype=torch.float64, device=w.device) if targets is None else targets
+    st = L.moe_place_greedy(_dev(w, "w", torch.float64), nl, E, kn, kt, G, nk, cap,
+                            _dev(assign, "assign", torch.int32), _dev(loads, "loads", torch.float64),
+                            _dev(targets, "targets", torch.float64), _stream())
+    _check("moe_place_greedy", st)
+    return assign, loads, targets
+
+
+def moe_place_incremental(w, knots_n, knots_t, assign, eps=0.03, max_swaps=1 << 16, n_swaps=None):
+    """Swap-based placement update of every layer; `assign` is updated in place.
+    Returns n_swaps [L] int32."""
+    L = load_library()
+    nl, E = w.shape
+    kn, kt, G, nk = _models(knots_n, knots_t)
+    n_swaps = torch.empty(nl, dtype=torch.int32, device=w.device) if n_swaps is None else n_swaps
+    st = L.moe_place_incremental(_dev(w, "w", torch.float64), nl, E, kn, kt, G, nk, float(eps), int(max_swaps),
+                                 _dev(assign, "assign", torch.int32), _dev(n_swaps, "n_swaps", torch.int32),
+                                 _stream())
+    _check("moe_place_incremental", st)
+    return n_swaps
+
+
+def moe_window_push(counts, ring, sums, slot):
+    """sums += counts - ring[slot]; ring[slot] = counts (all on the GPU)."""
+    L = load_library()
+    window, nl, E = ring.shape
+    if tuple(counts.shape) != (nl, E) or tuple(sums.shape) != (nl, E):
+        raise ValueError("counts and sums must be [L, E] like ring[slot]")
+    st = L.moe_window_push(_dev(counts, "counts", torch.int32), _dev(ring, "ring", torch.int32),
+                           _dev(sums, "sums", torch.float64), nl, E, window, int(slot), _stream())
+    _check("moe_window_push", st)
+
+
+def moe_drift_distance(w_cur, w_ref, delta=0.05, d=None, trigger=None):
+    """Cosine distance per layer and the drift trigger. Returns (d [L], trigger [1])."""
+    L = load_library()
+    nl, E = w_cur.shape
+    if tuple(w_ref.shape) != (nl, E):
+        raise ValueError("w_ref must match w_cur")
+    d = torch.empty(nl, dtype=torch.float64, device=w_cur.device) if d is None else d
+    trigger = torch.empty(1, dtype=torch.int32, device=w_cur.device) if trigger is None else trigger
+    st = L.moe_drift_distance(_dev(w_cur, "w_cur", torch.float64), _dev(w_ref, "w_ref", torch.float64), nl, E,
+                              float(delta), _dev(d, "d", torch.float64), _dev(trigger, "trigger", torch.int32),
+                              _stream())
+    _check("moe_drift_distance", st)
+    return d, trigger

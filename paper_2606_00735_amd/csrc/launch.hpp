@@ -28,4 +28,14 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       void* ws, hipStream_t s);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
+hipError_t launch_place_greedy(const double* W, int L, int E, const double* kn, const double* kt, int G, int nk,
+                               int cap, int32_t* assign, double* loads, double* targets, hipStream_t s);
+hipError_t launch_place_incremental(const double* W, int L, int E, const double* kn, const double* kt, int G,
+                                    int nk, double eps, int max_swaps, int32_t* assign, int32_t* n_swaps,
+                                    hipStream_t s);
+hipError_t launch_window_push(const int32_t* counts, int32_t* ring, double* sums, int L, int E, int slot,
+                              hipStream_t s);
+hipError_t launch_drift_distance(const double* w_cur, const double* w_ref, int L, int E, double delta, double* d,
+                                 int32_t* trigger, hipStream_t s);
+
 }  // namespace moe

@@ -5,7 +5,9 @@
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdint>
+#include <numeric>
 #include <vector>
 
 #include "../../include/moe.h"
@@ -258,6 +260,89 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
   if (result != MOE_OK) (void)hipStreamSynchronize(stream);
   for (auto& e : ev) (void)hipEventDestroy(e);
   return result;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Placement control path
+// ---------------------------------------------------------------------------
+namespace {
+
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
+
+moe_status place_shape_ok(const double* w, int L, int E, const double* kn, const double* kt, int G, int nk) {
+  if (L < 0 || E < 1 || G < 1 || nk < 1) return MOE_ERR_INVALID_ARG;
+  if (E > 1024 || G > 64 || nk > 64) return MOE_ERR_UNSUPPORTED;
+  if (L == 0) return MOE_OK;
+  if (!w || !kn || !kt) return MOE_ERR_INVALID_ARG;
+  if (!aligned8(w) || !aligned8(kn) || !aligned8(kt)) return MOE_ERR_INVALID_ARG;
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+moe_status moe_fit_latency_model(const int32_t* loads, const float* latencies, int n, double* knots_n,
+                                 double* knots_t) {
+  if (!loads || !latencies || !knots_n || !knots_t || n < 1 || n > 64) return MOE_ERR_INVALID_ARG;
+  std::vector<int> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  std::sort(order.begin(), order.end(), [&](int a, int b) { return loads[a] < loads[b]; });
+  double run = -INFINITY;
+  for (int i = 0; i < n; ++i) {
+    const int j = order[i];
+    if (loads[j] <= 0 || !std::isfinite(latencies[j])) return MOE_ERR_INVALID_ARG;
+    if (i > 0 && loads[j] == loads[order[i - 1]]) return MOE_ERR_INVALID_ARG;
+    run = std::max(run, static_cast<double>(latencies[j]));
+    knots_n[i] = static_cast<double>(loads[j]);
+    knots_t[i] = run;
+  }
+  return MOE_OK;
+}
+
+moe_status moe_place_greedy(const double* w, int L, int E, const double* knots_n, const double* knots_t, int G,
+                            int nk, int cap, int32_t* assign, double* loads, double* targets,
+                            hipStream_t stream) {
+  moe_status st = place_shape_ok(w, L, E, knots_n, knots_t, G, nk);
+  if (st != MOE_OK) return st;
+  if (cap < 0 || (cap > 0 && (long long)cap * G < E)) return MOE_ERR_INVALID_ARG;
+  if (L == 0) return MOE_OK;
+  if (!assign || !aligned4(assign) || (loads && !aligned8(loads)) || (targets && !aligned8(targets)))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_place_greedy(w, L, E, knots_n, knots_t, G, nk, cap, assign, loads, targets, stream));
+}
+
+moe_status moe_place_incremental(const double* w, int L, int E, const double* knots_n, const double* knots_t,
+                                 int G, int nk, double eps, int max_swaps, int32_t* assign, int32_t* n_swaps,
+                                 hipStream_t stream) {
+  moe_status st = place_shape_ok(w, L, E, knots_n, knots_t, G, nk);
+  if (st != MOE_OK) return st;
+  if (!std::isfinite(eps) || eps < 0.0 || max_swaps < 0 || max_swaps > (1 << 20)) return MOE_ERR_INVALID_ARG;
+  if (L == 0) return MOE_OK;
+  if (!assign || !aligned4(assign) || (n_swaps && !aligned4(n_swaps))) return MOE_ERR_INVALID_ARG;
+  return hip_status(
+      moe::launch_place_incremental(w, L, E, knots_n, knots_t, G, nk, eps, max_swaps, assign, n_swaps, stream));
+}
+
+moe_status moe_window_push(const int32_t* counts, int32_t* ring, double* sums, int L, int E, int window, int slot,
+                           hipStream_t stream) {
+  if (L < 0 || E < 1 || window < 1 || slot < 0 || slot >= window) return MOE_ERR_INVALID_ARG;
+  if (L == 0) return MOE_OK;
+  if (!counts || !ring || !sums || !aligned4(counts) || !aligned4(ring) || !aligned8(sums))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_window_push(counts, ring, sums, L, E, slot, stream));
+}
+
+moe_status moe_drift_distance(const double* w_cur, const double* w_ref, int L, int E, double delta, double* d,
+                              int32_t* trigger, hipStream_t stream) {
+  if (L < 0 || L > 65536 || E < 1 || !std::isfinite(delta)) return MOE_ERR_INVALID_ARG;
+  if (L > 0 && (!w_cur || !w_ref || !d || !aligned8(w_cur) || !aligned8(w_ref) || !aligned8(d)))
+    return MOE_ERR_INVALID_ARG;
+  if (trigger && !aligned4(trigger)) return MOE_ERR_INVALID_ARG;
+  if (L == 0 && !trigger) return MOE_OK;
+  return hip_status(moe::launch_drift_distance(w_cur, w_ref, L, E, delta, d, trigger, stream));
 }
 
 }  // extern "C"

@@ -166,3 +166,59 @@ def test_binding_refuses_cpu_tensors():
     w = torch.zeros(8, 128, dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU"):
         moe.moe_gate_topk(x, w, None, 2)
+
+
+# ---------------------------------------------------------------- placement path
+D8 = ctypes.c_void_p(0x10000)       # 8-byte aligned fake device pointer, never dereferenced
+
+
+def test_fit_latency_model_matches_oracle_bitwise():
+    from oracle import placement_oracle as P
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        n = int(rng.integers(1, 20))
+        loads = rng.choice(np.arange(1, 9000), n, replace=False)
+        lat = rng.uniform(1, 1000, n).astype(np.float32)
+        kn, kt = moe.moe_fit_latency_model(loads, lat)
+        rn, rt = P.fit_latency_model(loads.tolist(), lat.astype(np.float64).tolist())
+        assert np.array_equal(kn, rn) and np.array_equal(kt, rt)
+
+
+@pytest.mark.parametrize("loads,lats", [([1, 1], [1.0, 2.0]), ([0, 2], [1.0, 2.0]), ([1, 2], [1.0, np.nan]),
+                                        ([], [])])
+def test_fit_latency_model_rejects(L, loads, lats):
+    ld = np.asarray(loads, np.int32)
+    lt = np.asarray(lats, np.float32)
+    out = np.zeros(max(1, len(ld)))
+    st = L.moe_fit_latency_model(ld.ctypes.data_as(ctypes.c_void_p), lt.ctypes.data_as(ctypes.c_void_p), len(ld),
+                                 out.ctypes.data_as(ctypes.c_void_p), out.ctypes.data_as(ctypes.c_void_p))
+    assert st == INVALID
+
+
+@pytest.mark.parametrize("Lyr,E,G,nk,cap,expect", [
+    (4, 0, 8, 4, 0, INVALID),        # E < 1
+    (4, 2000, 8, 4, 0, UNSUPPORTED),  # E > 1024
+    (4, 64, 65, 4, 0, UNSUPPORTED),   # G > 64
+    (4, 64, 8, 65, 0, UNSUPPORTED),   # nk > 64
+    (4, 64, 8, 4, 7, INVALID),        # cap * G < E
+    (4, 64, 8, 4, -1, INVALID),
+    (-1, 64, 8, 4, 0, INVALID),
+    (0, 64, 8, 4, 0, 0),              # L = 0: no-op
+])
+def test_place_greedy_validation(L, Lyr, E, G, nk, cap, expect):
+    st = L.moe_place_greedy(D8, Lyr, E, D8, D8, G, nk, cap, FAKE, None, None, None)
+    assert st == expect
+
+
+def test_place_incremental_and_drift_validation(L):
+    assert L.moe_place_incremental(D8, 4, 64, D8, D8, 8, 4, -0.1, 10, FAKE, None, None) == INVALID
+    assert L.moe_place_incremental(D8, 4, 64, D8, D8, 8, 4, float("nan"), 10, FAKE, None, None) == INVALID
+    assert L.moe_place_incremental(D8, 4, 64, D8, D8, 8, 4, 0.03, -1, FAKE, None, None) == INVALID
+    assert L.moe_place_incremental(D8, 4, 64, D8, D8, 8, 4, 0.03, 10, None, None, None) == INVALID
+    assert L.moe_place_incremental(D8, 0, 64, D8, D8, 8, 4, 0.03, 10, None, None, None) == 0
+    assert L.moe_drift_distance(D8, D8, 4, 0, 0.05, D8, None, None) == INVALID
+    assert L.moe_drift_distance(D8, D8, 4, 8, float("inf"), D8, None, None) == INVALID
+    assert L.moe_drift_distance(MISALIGNED, D8, 4, 8, 0.05, D8, None, None) == INVALID
+    assert L.moe_window_push(FAKE, FAKE, D8, 4, 8, 10, 10, None) == INVALID   # slot >= window
+    assert L.moe_window_push(FAKE, FAKE, D8, 4, 8, 0, 0, None) == INVALID     # window < 1
+    assert L.moe_window_push(None, None, None, 0, 8, 10, 3, None) == 0        # L = 0: no-op
