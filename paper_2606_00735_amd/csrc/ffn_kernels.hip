@@ -61,6 +61,7 @@ struct GemmArgs {
   float* part;
   long long part_cap;
   int32_t* plan;
+  int plan_rows;  // rows the plan's row map holds
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -237,14 +238,17 @@ __device__ __forceinline__ int tile_class(int left) { return left > 128 ? 2 : (l
 // last-level cache.
 //
 // Split-K. When every expert has at most 64 rows (decode, or one lightly
-// loaded expert), the cost is streaming the weights, and a launch with fewer
-// tiles than blocks leaves CUs idle. Each tile is then cut into S K ranges
-// whose fp32 sums go to the workspace; split_reduce_kernel adds the S
-// partials of each output in a fixed order (so results do not depend on
-// timing) and applies the epilogue. S in 1..8 minimises
-// rounds(S) * (chunks per split + a fixed per-tile cost), each split keeping
-// at least kMinSplitChunks K chunks, and only if the partials fit. Every
-// block sees the same offsets, so every block makes the same choice.
+// loaded expert) the cost is streaming the weights, and a launch with fewer
+// tiles than blocks leaves CUs idle (a few experts of a few hundred rows, as
+// in the middle of the load sweep). In both cases each tile may be cut into
+// S K ranges whose fp32 sums go to the workspace (rows numbered compactly in
+// expert order); split_reduce_kernel adds the S partials of each output in a
+// fixed order (so results do not depend on timing) and applies the
+// epilogue. S in 1..8 minimises rounds(S) * (chunks per split + a fixed
+// per-tile cost), each split keeping at least kMinSplitChunks K chunks, and
+// only if the partials fit and their bytes stay below the weight bytes the
+// launch streams. Every block sees the same offsets, so every block makes
+// the same choice.
 template <int NV>
 __device__ __forceinline__ void block_scan(int (&v)[NV], int (&excl)[NV], int (&total)[NV], int (*s_tot)[kWaves]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -282,7 +286,7 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
   __shared__ int s_srow0[kMaxExperts];
-  __shared__ int s_tot[3][kWaves];
+  __shared__ int s_tot[4][kWaves];
 
   const int tid = threadIdx.x;
   const int E = a.E_local, G = gridDim.x;
@@ -297,22 +301,25 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     s_row0[tid] = o0;
     s_rows[tid] = rows;
   }
-  // tiles at 128 columns, rows of small experts, experts above 64 rows
-  int v[3] = {row_tiles(rows) * (a.N / 128), rows <= kSmallM ? rows : 0, rows > kSmallM ? 1 : 0};
-  int ex[3], tot[3];
-  block_scan<3>(v, ex, tot, s_tot);
-  const int T0 = tot[0], R = tot[1], n_big = tot[2];
+  // tiles at 128 columns, rows, experts above 64 rows, experts with rows
+  int v[4] = {row_tiles(rows) * (a.N / 128), rows, rows > kSmallM ? 1 : 0, rows > 0 ? 1 : 0};
+  int ex[4], tot[4];
+  block_scan<4>(v, ex, tot, s_tot);
+  const int T0 = tot[0], R = tot[1], n_big = tot[2], n_active = tot[3];
 
   // Single-output GEMM: 256-column tiles halve the bytes moved per MFMA but
   // halve the tile count; use them only when every CU still gets about four
   // tiles, so the last partial round costs little.
   const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 4 * G);
   int S = 1;
-  if (!wide && n_big == 0 && T0 > 0 && a.part != nullptr) {
+  if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
     const int nK = a.K / kBK;
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
     for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
-      if ((long long)NB * sp * R * a.N > a.part_cap) break;
+      // partials must fit, and their fp32 write + read must not outweigh the
+      // weights the launch streams (large row tiles are compute bound)
+      const long long pfl = (long long)NB * sp * R * a.N;
+      if (pfl > a.part_cap || pfl * 4 > (long long)NB * a.N * a.K * 2 * n_active) break;
       const long long c = (long long)((sp * T0 + G - 1) / G) * ((nK + sp - 1) / sp + kSplitOverhead);
       if (c < best) {
         best = c;
@@ -349,18 +356,27 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     const int e = lo;
     const int local = tile - s_start[e];
     const int er = s_rows[e];
+    const int n_mt = row_tiles(er);
     if (S > 1) {
-      // split tile: S consecutive tiles share a column block (every expert
-      // here has one row tile of at most 64 rows)
-      const int nt = local / S, sp = local - nt * S;
+      // split tile: S consecutive tiles share a row tile and a column block
+      const int sp = local % S, rest = local / S;
+      const int nt = rest / n_mt, mt = rest - nt * n_mt;
       const int nK = a.K / kBK;
       const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
-      float* pbase = a.part + ((size_t)sp * R + s_srow0[e]) * a.N;
-      gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, s_row0[e], s_row0[e] + er, nt * 128, kc0, kc1, pbase,
-                                        (size_t)S * R * a.N);
+      const int m0 = s_row0[e] + mt * 256;
+      const int left = er - mt * 256;
+      const int m_end = m0 + (left < 256 ? left : 256);
+      float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
+      const size_t ps = (size_t)S * R * a.N;
+      const int cls = tile_class(left);
+      if (cls == 0)
+        gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+      else if (cls == 1)
+        gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+      else
+        gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
       continue;
     }
-    const int n_mt = row_tiles(er);
     // row tile fastest: all row tiles of a weight column block run together
     const int nt = local / n_mt, mt = local - nt * n_mt;
     const int m0 = s_row0[e] + mt * 256;
@@ -486,13 +502,14 @@ __global__ void set_offsets_kernel(int32_t* offsets, int m) {
 // ---------------------------------------------------------------------------
 static size_t round256(size_t n) { return ((n + 255) / 256) * 256; }
 
-// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials. Partial
-// rows exist only for experts of at most 64 rows, so R <= 64 E_local (and
-// <= M_cap for offsets that are a valid scan), and S <= 8. The kernel splits
-// only when its partials fit in part_cap.
+// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials. A split
+// launch has R <= M_cap partial rows for offsets that are a valid scan (and
+// R <= 64 E_local when every expert is small), and S <= 8. The kernel splits
+// only when R fits the plan's row map and its partials fit in part_cap.
 struct FfnWs {
   size_t h, plan, part;  // byte offsets
   long long part_cap;    // floats
+  int plan_rows;         // rows of the plan's row map
   size_t bytes;
 };
 
@@ -504,11 +521,11 @@ static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
     w.bytes = h + 256;
     return w;
   }
-  const long long r_max = std::min<long long>(M_cap, (long long)kSmallM * E_local);
-  const long long need = (long long)kMaxSplit * r_max * std::max(2LL * I, (long long)H);
+  const long long need = (long long)kMaxSplit * M_cap * std::max(2LL * I, (long long)H);
   w.part_cap = std::min(need, kPartCapFloats);
+  w.plan_rows = std::max(M_cap, kSmallM * E_local);
   w.plan = h;
-  w.part = w.plan + round256((size_t)(kPlanHead + (size_t)kSmallM * E_local) * 4);
+  w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
   w.bytes = w.part + round256((size_t)w.part_cap * 4) + 256;
   return w;
 }
@@ -566,15 +583,14 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   // reduce grid: one float4 column group per thread over at most
   // min(M_cap, 64 E_local) rows, grid-stride beyond 4 blocks per CU
   auto reduce_grid = [&](int N) {
-    const long long r_max = std::min<long long>(M_cap, (long long)kSmallM * E_local);
-    const long long items = r_max * (N / 4);
+    const long long items = (long long)L.plan_rows * (N / 4);
     long long g = (items + 255) / 256;
     if (g > 4LL * cus) g = 4LL * cus;
     return (unsigned)(g < 1 ? 1 : g);
   };
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
-              part, L.part_cap, plan};
+              part, L.part_cap, plan, L.plan_rows};
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -586,7 +602,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
     if (e != hipSuccess) return e;
   }
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
-              static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan};
+              static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan, L.plan_rows};
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -185,12 +185,14 @@ def test_ffn_stage_on_oracle_inputs():
 
 
 SPLIT_CASES = [
-    # (H, I, rows per local expert): every expert has at most 64 rows and the
-    # GEMMs have fewer tiles than CUs, so both take the split-K path
+    # (H, I, rows per local expert, S of the down GEMM): experts of at most 64
+    # rows, or launches with fewer tiles than CUs, take the split-K path
     (1024, 2048, [1, 64, 0, 30], 4),       # gate/up S = 2, down S = 4
     (4096, 14336, [64], 8),                # Mixtral-shaped expert: gate/up S = 2, down S = 8
     (4096, 14336, [1], 8),
-    (1024, 2048, [65, 3, 0, 1], 1),        # one expert above 64 rows: no split
+    (1024, 2048, [65, 3, 0, 1], 4),        # a 65-row expert, but fewer tiles than CUs: still split
+    (7168, 2048, [256], 4),                # a 256-row DSV3-shaped expert: gate/up S = 8, down S = 4
+    (5120, 8192, [400, 100, 32], 3),       # Maverick-shaped experts of mixed size: down S = 3
     (7168, 2048, [1, 33], 2),              # DSV3-shaped experts: gate/up S = 8, down S = 2
     (7168, 2048, [1], 4),                  # one DSV3-shaped expert: gate/up S = 8, down S = 4
     (5120, 8192, [1], 6),                  # Maverick-shaped expert: gate/up S = 4, down S = 6
