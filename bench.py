@@ -254,10 +254,118 @@ def main():
                                 "gbps": [round((e_bytes + 2.0 * m * H * 2) / (u * 1e-6) / 1e9, 1) for m, u in
                                          zip(SWEEP_MS, med)]}
 
+    placement_inputs = None
+    if not args.no_extras:
+        result["placement"], placement_inputs = placement_section(moe, args.seed)
+
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
+        if placement_inputs is not None:
+            result["cpu_baseline"]["placement"] = placement_oracle_timing(*placement_inputs)
 
     print(json.dumps(result), flush=True)
+
+
+PLACE_LAYERS, PLACE_GPUS, PLACE_T = 58, 8, 4096
+PLACE_SWEEP_MS = [1, 8, 64, 256, 1024, 4096]
+
+
+def placement_section(moe, seed):
+    """ViBE's placement control path on this GPU for a DSV3-shaped model:
+    58 MoE layers x 256 experts over 8 GPUs (32 slots each), f_g fitted from a
+    sweep of one DSV3-shaped expert on this GPU and scaled per GPU by up to
+    7 % (seeded), synthetic activation matrices with the rank-bias skew
+    (alpha = 1) before and after a routing drift (8 rank swaps per layer).
+    Times are HIP-event medians of the GPU calls; predicted layer latencies
+    come from moe_placement_cost."""
+    import numpy as np
+    import torch
+    from synth import CONFIGS, make_activation_matrix, make_experts, make_router
+
+    shape = CONFIGS["dsv3_shard"]
+    Lyr, G, E, k = PLACE_LAYERS, PLACE_GPUS, shape.E, shape.k
+    cap = E // G
+    up = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(dt).contiguous()
+    g1, u1, d1 = make_experts(shape, [0], seed=seed)
+    e_bytes = 3 * shape.H * shape.I * 2
+    n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
+    rep = lambda a: up(a).repeat(n_rot, 1, 1).contiguous()
+    xs = up(make_router(shape, max(PLACE_SWEEP_MS), 0.0, seed=seed)[0])
+    med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), PLACE_SWEEP_MS, warmup=3, iters=10)
+    kn, kt = moe.moe_fit_latency_model(PLACE_SWEEP_MS, med)
+    scale = 1.0 + 0.07 * np.random.default_rng(seed + 7).random(G)
+    KN, KT = np.tile(kn, (G, 1)), np.outer(scale, kt)
+    W1 = make_activation_matrix(Lyr, E, PLACE_T, k, 1.0, seed)
+    W2 = make_activation_matrix(Lyr, E, PLACE_T, k, 1.0, seed, rank_swaps=8)
+    d = lambda a, dt=torch.float64: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(dt).contiguous()
+    dW1, dW2, dKN, dKT = d(W1), d(W2), d(KN), d(KT)
+    eKN, eKT = d(np.tile([1.0, 2.0], (G, 1))), d(np.tile([1.0, 2.0], (G, 1)))   # EPLB: f(n) = n
+
+    def timed(fn, reps=20):
+        fn()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ev]) * 1e3)
+
+    vibe, _, _ = moe.moe_place_greedy(dW1, dKN, dKT, cap=cap)
+    eplb, _, _ = moe.moe_place_greedy(dW1, eKN, eKT, cap=cap)
+    contig = d(np.tile(np.arange(E) // cap, (Lyr, 1)), torch.int32)
+    t_greedy = timed(lambda: moe.moe_place_greedy(dW1, dKN, dKT, cap=cap, assign=vibe))
+    upd = vibe.clone()
+    swaps = moe.moe_place_incremental(dW2, dKN, dKT, upd, eps=0.03)
+    copies = iter([vibe.clone() for _ in range(21)])   # each timed call starts from the same placement
+    t_incr = timed(lambda: moe.moe_place_incremental(dW2, dKN, dKT, next(copies), eps=0.03))
+    t_drift = timed(lambda: moe.moe_drift_distance(dW2, dW1, delta=0.05))
+    ring = torch.zeros((100, Lyr, E), dtype=torch.int32, device="cuda")
+    sums = torch.zeros((Lyr, E), dtype=torch.float64, device="cuda")
+    cnt = d(W1, torch.int32)
+    t_push = timed(lambda: moe.moe_window_push(cnt, ring, sums, 0))
+    dist, trig = moe.moe_drift_distance(dW2, dW1, delta=0.05)
+
+    def total(W, A):
+        _, lat, latg = moe.moe_placement_cost(W, A, dKN, dKT)
+        return (round(float(lat.max(dim=1).values.sum().item()), 1),
+                round(float(latg.max(dim=1).values.sum().item()), 1))
+
+    pred = {"contiguous": total(dW1, contig), "eplb": total(dW1, eplb), "vibe": total(dW1, vibe),
+            "after_drift_kept": total(dW2, vibe), "after_drift_incremental": total(dW2, upd),
+            "after_drift_fresh_greedy": total(dW2, moe.moe_place_greedy(dW2, dKN, dKT, cap=cap)[0])}
+    sw = swaps.cpu().numpy()
+    out = {
+        "workload": f"{Lyr} MoE layers x {E} experts on {G} GPUs ({cap} slots each), DSV3-shaped expert "
+                    f"f_g from this GPU's sweep x (1 + 0.07 u_g), T={PLACE_T} tokens top-{k} per layer, alpha=1",
+        "f_knots": {"n": [int(v) for v in kn], "us": [round(float(v), 2) for v in kt]},
+        "gpu_speed_scale": [round(float(v), 4) for v in scale],
+        "greedy_us": round(t_greedy, 2), "incremental_us": round(t_incr, 2),
+        "drift_distance_us": round(t_drift, 2), "window_push_us": round(t_push, 2),
+        "drift_max_distance": round(float(dist.max().item()), 4), "drift_trigger": int(trig.item()),
+        "swaps_per_layer": {"mean": round(float(sw.mean()), 2), "max": int(sw.max())},
+        "moved_by_fresh_greedy_per_layer": round(float(
+            (moe.moe_place_greedy(dW2, dKN, dKT, cap=cap)[0] != vibe).sum(dim=1).float().mean().item()), 1),
+        "predicted_sum_of_layer_latency_us": {k2: {"max_f_of_load": v[0], "max_sum_f_per_expert": v[1]}
+                                              for k2, v in pred.items()},
+    }
+    return out, (W1, W2, KN, KT, cap)
+
+
+def placement_oracle_timing(W1, W2, KN, KT, cap, layers=8):
+    """The placement oracle on the first `layers` layers of the same inputs."""
+    from oracle import placement_oracle as PO
+    t = time.perf_counter()
+    starts = [PO.greedy_placement(W1[l], KN, KT, cap=cap)[0] for l in range(layers)]
+    t_g = time.perf_counter() - t
+    t = time.perf_counter()
+    for l in range(layers):
+        PO.incremental_update(starts[l], W2[l], KN, KT, eps=0.03)
+    t_i = time.perf_counter() - t
+    return {"greedy_ms_per_layer": round(t_g / layers * 1e3, 3),
+            "incremental_ms_per_layer": round(t_i / layers * 1e3, 3), "cores": 1,
+            "sample": f"first {layers} of {W1.shape[0]} layers (pure Python, one thread)"}
 
 
 def cpu_baseline(li, target_s):

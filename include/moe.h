@@ -269,6 +269,23 @@ moe_status moe_place_incremental(const double* w, int L, int E, const double* kn
                                  int32_t* assign, int32_t* n_swaps, hipStream_t stream);
 
 /*
+ * moe_placement_cost - predicted cost of a placement (Section 4.2.3).
+ *
+ * Per layer l and GPU g: loads[l,g] = n_g = sum of w[l,e] over the experts
+ * with assign[l,e] == g (ascending e), lat[l,g] = f_g(n_g), and
+ * lat_grouped[l,g] = sum of f_g(w[l,e]) over the same experts (the reading
+ * in which each expert runs as its own group). The layer latency the paper
+ * minimises is max_g lat[l,g]. Experts with assign outside [0, G) count
+ * nowhere.
+ *
+ * w [L, E] fp64, assign [L, E] int32, loads / lat_grouped [L, G] fp64 or
+ * NULL, lat [L, G] fp64 (all DEVICE).
+ */
+moe_status moe_placement_cost(const double* w, const int32_t* assign, int L, int E,
+                              const double* knots_n, const double* knots_t, int G, int nk,
+                              double* loads, double* lat, double* lat_grouped, hipStream_t stream);
+
+/*
  * moe_window_push - add one forward pass's per-layer expert counts to a
  * sliding window (Section 4.2.4: load vectors averaged over a window of
  * samples).

@@ -27,6 +27,7 @@ from ._lib import (  # noqa: F401
     moe_permute,
     moe_place_greedy,
     moe_place_incremental,
+    moe_placement_cost,
     moe_unpermute_combine,
     moe_window_push,
 )

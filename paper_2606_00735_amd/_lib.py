@@ -23,8 +23,8 @@ MAX_EXPERTS, MAX_TOPK = 256, 16
 
 EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert_histogram_scan",
             "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep",
-            "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_window_push",
-            "moe_drift_distance")
+            "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_placement_cost",
+            "moe_window_push", "moe_drift_distance")
 
 
 class MoeError(RuntimeError):
@@ -72,6 +72,8 @@ def load_library(path: str = LIB_PATH):
     L.moe_place_greedy.argtypes = [_P, _I, _I, _P, _P, _I, _I, _I, _P, _P, _P, _P]
     L.moe_place_incremental.restype = _I
     L.moe_place_incremental.argtypes = [_P, _I, _I, _P, _P, _I, _I, _D, _I, _P, _P, _P]
+    L.moe_placement_cost.restype = _I
+    L.moe_placement_cost.argtypes = [_P, _P, _I, _I, _P, _P, _I, _I, _P, _P, _P, _P]
     L.moe_window_push.restype = _I
     L.moe_window_push.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P]
     L.moe_drift_distance.restype = _I
@@ -360,6 +362,19 @@ def moe_place_incremental(w, knots_n, knots_t, assign, eps=0.03, max_swaps=1 << 
                                  _stream())
     _check("moe_place_incremental", st)
     return n_swaps
+
+
+def moe_placement_cost(w, assign, knots_n, knots_t):
+    """Per layer and GPU: loads n_g, f_g(n_g) and sum_{e in S_g} f_g(w_e).
+    Returns (loads, lat, lat_grouped), each [L, G] fp64."""
+    L = load_library()
+    nl, E = w.shape
+    kn, kt, G, nk = _models(knots_n, knots_t)
+    out = [torch.empty((nl, G), dtype=torch.float64, device=w.device) for _ in range(3)]
+    st = L.moe_placement_cost(_dev(w, "w", torch.float64), _dev(assign, "assign", torch.int32), nl, E, kn, kt, G, nk,
+                              *[_dev(o, "out", torch.float64) for o in out], _stream())
+    _check("moe_placement_cost", st)
+    return tuple(out)
 
 
 def moe_window_push(counts, ring, sums, slot):

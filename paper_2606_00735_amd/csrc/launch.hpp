@@ -33,6 +33,9 @@ hipError_t launch_place_greedy(const double* W, int L, int E, const double* kn, 
 hipError_t launch_place_incremental(const double* W, int L, int E, const double* kn, const double* kt, int G,
                                     int nk, double eps, int max_swaps, int32_t* assign, int32_t* n_swaps,
                                     hipStream_t s);
+hipError_t launch_placement_cost(const double* W, const int32_t* assign, int L, int E, const double* kn,
+                                 const double* kt, int G, int nk, double* loads, double* lat, double* lat_grouped,
+                                 hipStream_t s);
 hipError_t launch_window_push(const int32_t* counts, int32_t* ring, double* sums, int L, int E, int slot,
                               hipStream_t s);
 hipError_t launch_drift_distance(const double* w_cur, const double* w_ref, int L, int E, double delta, double* d,

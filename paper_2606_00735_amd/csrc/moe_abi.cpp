@@ -326,6 +326,19 @@ moe_status moe_place_incremental(const double* w, int L, int E, const double* kn
       moe::launch_place_incremental(w, L, E, knots_n, knots_t, G, nk, eps, max_swaps, assign, n_swaps, stream));
 }
 
+moe_status moe_placement_cost(const double* w, const int32_t* assign, int L, int E, const double* knots_n,
+                              const double* knots_t, int G, int nk, double* loads, double* lat, double* lat_grouped,
+                              hipStream_t stream) {
+  moe_status st = place_shape_ok(w, L, E, knots_n, knots_t, G, nk);
+  if (st != MOE_OK) return st;
+  if (L == 0) return MOE_OK;
+  if (!assign || !lat || !aligned4(assign) || !aligned8(lat) || (loads && !aligned8(loads)) ||
+      (lat_grouped && !aligned8(lat_grouped)))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(
+      moe::launch_placement_cost(w, assign, L, E, knots_n, knots_t, G, nk, loads, lat, lat_grouped, stream));
+}
+
 moe_status moe_window_push(const int32_t* counts, int32_t* ring, double* sums, int L, int E, int window, int slot,
                            hipStream_t stream) {
   if (L < 0 || E < 1 || window < 1 || slot < 0 || slot >= window) return MOE_ERR_INVALID_ARG;

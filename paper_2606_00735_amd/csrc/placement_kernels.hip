@@ -273,6 +273,35 @@ __global__ __launch_bounds__(kPlaceThreads) void place_incremental_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Predicted cost of a placement (Section 4.2.3): per layer and GPU, the load
+// n_g = sum_{e in S_g} w_e (ascending e), f_g(n_g), and the grouped reading
+// sum_{e in S_g} f_g(w_e). The layer latency is the maximum over GPUs.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kWave) void placement_cost_kernel(const double* __restrict__ W,
+                                                               const int32_t* __restrict__ assign, int E,
+                                                               const double* __restrict__ knots_n,
+                                                               const double* __restrict__ knots_t, int G, int nk,
+                                                               double* __restrict__ loads,
+                                                               double* __restrict__ lat,
+                                                               double* __restrict__ lat_grouped) {
+  const int l = blockIdx.x, g = threadIdx.x;
+  if (g >= G) return;
+  const double* w = W + (size_t)l * E;
+  const int32_t* a = assign + (size_t)l * E;
+  const double* kn = knots_n + (size_t)g * nk;
+  const double* kt = knots_t + (size_t)g * nk;
+  double n = 0.0, grouped = 0.0;
+  for (int e = 0; e < E; ++e)
+    if (a[e] == g) {
+      n += w[e];
+      grouped += latency_at(kn, kt, nk, w[e]);
+    }
+  if (loads) loads[(size_t)l * G + g] = n;
+  lat[(size_t)l * G + g] = latency_at(kn, kt, nk, n);
+  if (lat_grouped) lat_grouped[(size_t)l * G + g] = grouped;
+}
+
+// ---------------------------------------------------------------------------
 // Drift detector (Section 4.2.4): window sums and cosine distance per layer.
 // ---------------------------------------------------------------------------
 __global__ void window_push_kernel(const int32_t* __restrict__ counts, int32_t* __restrict__ ring_slot,
@@ -327,6 +356,14 @@ hipError_t launch_place_incremental(const double* W, int L, int E, const double*
                                     hipStream_t s) {
   if (L == 0) return hipSuccess;
   place_incremental_kernel<<<L, kPlaceThreads, 0, s>>>(W, E, kn, kt, G, nk, eps, max_swaps, assign, n_swaps);
+  return hipGetLastError();
+}
+
+hipError_t launch_placement_cost(const double* W, const int32_t* assign, int L, int E, const double* kn,
+                                 const double* kt, int G, int nk, double* loads, double* lat, double* lat_grouped,
+                                 hipStream_t s) {
+  if (L == 0) return hipSuccess;
+  placement_cost_kernel<<<L, kWave, 0, s>>>(W, assign, E, kn, kt, G, nk, loads, lat, lat_grouped);
   return hipGetLastError();
 }
 

@@ -8,6 +8,7 @@ from .moe_inputs import (  # noqa: F401
     CONFIGS,
     LayerInputs,
     LayerShape,
+    make_activation_matrix,
     make_layer,
     make_router,
     make_experts,

@@ -230,3 +230,33 @@ def make_layer(shape, T: int, alpha: float, seed: int = 0,
     if with_experts:
         li.w_gate, li.w_up, li.w_down = make_experts(shape, local, seed)
     return li
+
+
+def make_activation_matrix(L: int, E: int, T: int, k: int, alpha: float, seed: int,
+                           rank_swaps: int = 0, drift_seed: int = 1):
+    """Per-layer expert loads W [L, E] (float64 counts) of T tokens routed top-k.
+
+    Layer l has its own seeded rank permutation; token t picks the k experts
+    with the largest -alpha * ln(rank_e) + g_te, g i.i.d. standard Gumbel (a
+    synthetic router with the rank-bias skew). ``rank_swaps`` > 0 exchanges
+    the ranks of that many random expert pairs per layer first (a routing
+    drift: other experts become hot), drawn from ``drift_seed``.
+    """
+    root = np.random.SeedSequence(seed)
+    kids = root.spawn(2 * L)
+    dkids = np.random.SeedSequence(drift_seed).spawn(L)
+    W = np.zeros((L, E), np.float64)
+    for l in range(L):
+        g = np.random.Generator(np.random.PCG64(kids[2 * l]))
+        rank = g.permutation(E).astype(np.int64) + 1
+        if rank_swaps:
+            d = np.random.Generator(np.random.PCG64(dkids[l]))
+            for _ in range(rank_swaps):
+                i, j = d.choice(E, 2, replace=False)
+                rank[i], rank[j] = rank[j], rank[i]
+        prior = -float(alpha) * np.log(rank.astype(np.float64))
+        t = np.random.Generator(np.random.PCG64(kids[2 * l + 1]))
+        score = prior[None, :] + t.gumbel(size=(T, E))
+        top = np.argpartition(-score, k - 1, axis=1)[:, :k]
+        W[l] = np.bincount(top.ravel(), minlength=E)
+    return W

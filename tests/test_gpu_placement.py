@@ -151,3 +151,21 @@ def test_full_size_dsv3_like():
         ra, rs = P.incremental_update(a[l], W2[l], kn, kt, eps=0.03)
         assert np.array_equal(ad[l], ra) and ns[l] == rs, f"layer {l}"
     print("  swaps per layer: max", int(ns.max()), "mean", float(ns.mean()), flush=True)
+
+
+def test_placement_cost_matches_oracle():
+    banner("placement cost")
+    Lyr, E, G = 10, 256, 8
+    W = loads(Lyr, E, seed=4, integer=False)
+    kn, kt = sweep_like_models(G, seed=5)
+    rng = np.random.default_rng(6)
+    A = rng.integers(0, G, (Lyr, E)).astype(np.int32)
+    n, lat, latg = moe.moe_placement_cost(dev(W), dev(A, torch.int32), dev(kn), dev(kt))
+    torch.cuda.synchronize()
+    n, lat, latg = n.cpu().numpy(), lat.cpu().numpy(), latg.cpu().numpy()
+    for l in range(Lyr):
+        rn = P.gpu_loads(A[l], W[l], G)
+        assert np.array_equal(n[l], rn)
+        assert np.array_equal(lat[l], [P.latency(kn[g], kt[g], rn[g]) for g in range(G)])
+        assert lat[l].max() == P.layer_latency(A[l], W[l], kn, kt)
+        assert latg[l].max() == P.layer_latency(A[l], W[l], kn, kt, grouped=True)
