@@ -307,10 +307,10 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
   block_scan<4>(v, ex, tot, s_tot);
   const int T0 = tot[0], R = tot[1], n_big = tot[2], n_active = tot[3];
 
-  // Single-output GEMM: 256-column tiles halve the bytes moved per MFMA but
-  // halve the tile count; use them only when every CU still gets about four
-  // tiles, so the last partial round costs little.
-  const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 4 * G);
+  // Single-output GEMM: 256-column tiles move a third fewer bytes per MFMA
+  // than 128-column ones but halve the tile count; use them when every CU
+  // still gets at least two of them.
+  const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 2 * G);
   int S = 1;
   if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
     const int nK = a.K / kBK;
