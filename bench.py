@@ -158,8 +158,11 @@ def main():
             ev[5].record()
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        stage = {n: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)])) * 1e3
-                 for i, n in enumerate(names)}
+        per = {n: np.array([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)]) * 1e3
+               for i, n in enumerate(names)}
+        stage = {n: float(v.mean()) for n, v in per.items()}
+        spread = {n: [round(float(np.percentile(v, q)), 2) for q in (10, 50, 90)] for n, v in per.items()}
+        run_timed.spread = spread
         return (t1 - t0) * 1e3 / steps, stage
 
     if args.calib_copy_mib > 0:
@@ -216,6 +219,7 @@ def main():
         "us_per_layer": round(us, 2),
         "layer_gbps": round(w["layer_bytes"] / (us * 1e-6) / 1e9, 1),
         "stages_us": {n: round(v, 2) for n, v in stage.items()},
+        "stages_us_p10_p50_p90": run_timed.spread,
         "roofline": roofline,
         "gen_s": round(t_gen, 1),
     }
@@ -256,6 +260,8 @@ def main():
 
     placement_inputs = None
     if not args.no_extras:
+        result["reference_peaks"] = reference_peaks(torch, np, w, T, H, I, dt)
+        result["sclk"] = read_sclk()
         result["placement"], placement_inputs = placement_section(moe, args.seed)
 
     if not args.no_cpu:
@@ -264,6 +270,55 @@ def main():
             result["cpu_baseline"]["placement"] = placement_oracle_timing(*placement_inputs)
 
     print(json.dumps(result), flush=True)
+
+
+def reference_peaks(torch, np, w, T, H, I, dt):
+    """Achievable peaks on this GPU, for context next to the datasheet
+    denominators: a 1 GiB device-to-device copy (torch), and the vendor dense
+    GEMMs (torch.matmul, hipBLASLt) of the FFN's shapes at M = M_loc."""
+    def timed(fn, reps=10):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    t_copy = timed(lambda: dst.copy_(src))
+    del src, dst
+    out = {"copy_1GiB_GBps": round(2 * n / t_copy / 1e9, 1)}
+    m = int(w["m_loc"])
+    if dt == torch.bfloat16 and m > 0:
+        a1 = torch.randn(m, H, device="cuda", dtype=dt)
+        b1 = torch.randn(H, 2 * I, device="cuda", dtype=dt)
+        a2 = torch.randn(m, I, device="cuda", dtype=dt)
+        b2 = torch.randn(I, H, device="cuda", dtype=dt)
+        t1 = timed(lambda: torch.matmul(a1, b1))
+        t2 = timed(lambda: torch.matmul(a2, b2))
+        out["vendor_dense_gemm_us"] = {"gate_up_shape": round(t1 * 1e6, 1), "down_shape": round(t2 * 1e6, 1),
+                                       "sum": round((t1 + t2) * 1e6, 1),
+                                       "tflops": round(6.0 * m * H * I / (t1 + t2) / 1e12, 1)}
+        del a1, b1, a2, b2
+    return out
+
+
+def read_sclk():
+    """Current shader clock as rocm-smi reports it (None if unavailable)."""
+    import subprocess
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
+    except Exception:
+        return None
+    for line in r.stdout.splitlines():
+        if "sclk" in line:
+            return line.split(":", 1)[-1].strip()
+    return None
 
 
 PLACE_LAYERS, PLACE_GPUS, PLACE_T = 58, 8, 4096
