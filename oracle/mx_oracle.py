@@ -13,8 +13,9 @@ conversion from higher precision):
                      E4M3's largest power of two), clamped to [-127, 127];
                      an all-zero block takes s = -127
     element          q_i = RNE_E4M3( clamp(v_i / 2^s, -448, 448) )
-(round to nearest, ties to even; a value that rounds to zero gets the code
-0x00, never -0). Dequantised value = E4M3(q_i) * 2^s.
+(round to nearest, ties to even; E4M3 has a signed zero, and a value that
+rounds to zero keeps its sign, as in IEEE 754 rounding). Dequantised value =
+E4M3(q_i) * 2^s.
 
 The expert FFN in MXFP8 (the bf16 layer of ``moe_oracle`` with FP8
 operands): x rows and weights quantised per block of 32 along H (gate/up)
@@ -71,7 +72,7 @@ def e4m3_encode(v) -> np.ndarray:
     pick_hi = np.where(_VALS[hi] == a, True, pick_hi)
     idx = np.where(pick_hi, hi, lo)
     code = _CODES[idx].astype(np.int64)
-    code = np.where(np.signbit(v) & (code != 0), code | 0x80, code)
+    code = np.where(np.signbit(v), code | 0x80, code)
     return code.astype(np.uint8)
 
 

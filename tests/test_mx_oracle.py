@@ -25,9 +25,9 @@ def test_decode_table_matches_torch():
 
 
 def test_encode_round_trips_every_finite_code():
-    codes = np.array([c for c in range(256) if (c & 0x7F) != 0x7F and c != 0x80])
-    assert np.array_equal(X.e4m3_encode(X.e4m3_decode(codes)), codes)
-    assert X.e4m3_encode(-0.0) == 0 and X.e4m3_encode(-2.0 ** -12) == 0       # zero is never -0
+    codes = np.array([c for c in range(256) if (c & 0x7F) != 0x7F])
+    assert np.array_equal(X.e4m3_encode(X.e4m3_decode(codes)), codes)           # -0 included
+    assert X.e4m3_encode(-2.0 ** -12) == 0x80 and X.e4m3_encode(2.0 ** -12) == 0  # signed zero
 
 
 def test_encode_matches_torch_including_ties():
@@ -37,7 +37,6 @@ def test_encode_matches_torch_including_ties():
     mids = (vals[:-1] + vals[1:]) / 2                        # exact midpoints: ties to even
     v = np.concatenate([v, mids, -mids]).astype(np.float32)
     mine, ref = X.e4m3_encode(v.astype(np.float64)), torch_e4m3(v)
-    ref = np.where(ref == 0x80, 0, ref)                      # torch keeps -0; zero here is +0
     assert np.array_equal(mine, ref)
 
 
