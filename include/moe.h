@@ -174,6 +174,86 @@ moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const 
                                  hipStream_t stream);
 
 /*
+ * MXFP8 expert FFN (FP8 experts).
+ *
+ * The paper serves its models in FP8 (Table 2a) without naming a scaling
+ * scheme. These entry points use OCP Microscaling FP8 (MXFP8), the block
+ * scaling gfx950's scaled MFMA consumes directly: elements are FP8 E4M3 (OCP
+ * encoding: bias 7, no infinities, S.1111.111 NaN, largest finite 448), and
+ * every 32 consecutive elements along the reduction dimension share one E8M0
+ * scale code c, the power of two 2^(c - 127).
+ *
+ * Quantisation of a 32-element block v (OCP MX conversion): shared exponent
+ * s = floor(log2(max |v_i|)) - 8 clamped to [-127, 127] (an all-zero block
+ * takes -127), code c = s + 127, element q_i = E4M3 of v_i / 2^s clamped to
+ * +-448 and rounded to nearest, ties to even (a value that rounds to zero
+ * keeps its sign).
+ *
+ * Layout of an MXFP8 matrix with R rows and reduction length K (K % 128 == 0):
+ *   codes  [R, K]        uint8, row-major (16-byte aligned)
+ *   scales [K/128, R]    uint32, chunk-major: dword (k, r) holds the codes of
+ *                        row r for elements [128 k, 128 k + 128), byte b
+ *                        (little-endian) for elements [128 k + 32 b, +32)
+ * A batch of B such matrices (expert weights) is codes [B, R, K] and scales
+ * [B, K/128, R].
+ */
+
+/*
+ * moe_mx_quantize - MXFP8 quantisation of `batch` matrices of `rows` x K.
+ *
+ * x      [batch, rows, K] dt (bf16 or fp32)
+ * codes  [batch, rows, K] uint8, all written
+ * scales [batch, K/128, rows] uint32, all written
+ * Limits: K % 128 == 0; batch * rows * K <= 2^40.
+ */
+moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, uint8_t* codes,
+                           uint32_t* scales, hipStream_t stream);
+
+/*
+ * moe_grouped_swiglu_mx - the gate/up half of the MXFP8 expert FFN.
+ *
+ * For local slot l and rows R = [offsets[l], offsets[l+1]) (clamped to
+ * [0, M_cap]):
+ *   G = X[R] Wg[l]^T, U = X[R] Wu[l]^T  from the MXFP8 operands (scaled MFMA,
+ *                                        fp32 accumulation)
+ *   h = silu(G) * U                      (fp32)
+ *   (hq, hs)[R] = MXFP8 quantisation of h along I (rules above)
+ * xq [M_cap, H], xs [H/128, M_cap]; wgq, wuq [E_local, I, H],
+ * wgs, wus [E_local, H/128, I]; hq [M_cap, I], hs [I/128, M_cap]: rows R of
+ * every local expert written, the rest untouched.
+ * Limits: 0 <= E_local <= 256; H % 128 == 0, I % 128 == 0; H, I <= 2^20.
+ */
+moe_status moe_grouped_swiglu_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
+                                 const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
+                                 const int32_t* offsets, int E_local, int H, int I, int M_cap,
+                                 uint8_t* hq, uint32_t* hs, hipStream_t stream);
+
+/*
+ * moe_grouped_gemm_mx - grouped MXFP8 GEMM with bf16 output: for local slot l,
+ * c[R] = bf16( A[R] B[l]^T ) (fp32 accumulation), R as above.
+ * aq [M_cap, K], as [K/128, M_cap]; bq [E_local, N, K], bs [E_local, K/128, N];
+ * c [M_cap, N] bf16, rows R written. The down projection of the MXFP8 FFN.
+ * Limits: 0 <= E_local <= 256; N % 128 == 0, K % 128 == 0; N, K <= 2^20.
+ */
+moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq,
+                               const uint32_t* bs, const int32_t* offsets, int E_local, int N,
+                               int K, int M_cap, void* c, hipStream_t stream);
+
+/*
+ * moe_grouped_swiglu_ffn_mx - the MXFP8 expert FFN (the FP8 counterpart of
+ * moe_grouped_swiglu_ffn): moe_grouped_swiglu_mx into the workspace, then
+ * moe_grouped_gemm_mx with W_down (wdq [E_local, H, I], wds
+ * [E_local, I/128, H]) into y_perm [M_cap, H] bf16.
+ * ws holds h codes [M_cap, I] at offset 0 and their scales [I/128, M_cap]
+ * at offset M_cap * I rounded up to 256 bytes.
+ */
+moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
+                                     const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
+                                     const uint8_t* wdq, const uint32_t* wds,
+                                     const int32_t* offsets, int E_local, int H, int I, int M_cap,
+                                     void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
  * moe_load_sweep - per-expert latency versus token load.
  *
  * Algorithm 1 Phase 1 / Section 4.2.1: profile the expert computation over a

@@ -99,10 +99,12 @@ def mx_dequantize(codes, scales, block: int = 32) -> np.ndarray:
     return v.reshape(c.shape)
 
 
-def grouped_swiglu_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets):
+def grouped_swiglu_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets, parts=False):
     """Per local expert l, rows [offsets[l], offsets[l+1]) of the MX-quantised
     x_perm. Returns (h codes [M,I], h scales [M,I/32], h fp32 before
-    quantisation [M,I], y [M,H] fp32 holding bf16 values, |h||W_down|^T [M,H]).
+    quantisation [M,I], y [M,H] fp32 holding bf16 values, |h||W_down|^T [M,H]);
+    with parts=True also a dict of the fp64 G, U and their term magnitudes
+    |X||W_gate|^T, |X||W_up|^T (for error bounds).
     """
     offsets = np.asarray(offsets, np.int64)
     m = int(offsets[-1])
@@ -112,13 +114,18 @@ def grouped_swiglu_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets):
     h32 = np.zeros((m, I), F32)
     y = np.zeros((m, H), F32)
     mag = np.zeros((m, H))
+    P = {k: np.zeros((m, I)) for k in ("G", "U", "magG", "magU")}
     for s in range(len(offsets) - 1):
         r0, r1 = int(offsets[s]), int(offsets[s + 1])
         if r1 == r0:
             continue
         X = mx_dequantize(xq[r0:r1], xs[r0:r1])
-        G = (X @ mx_dequantize(wgq[s], wgs[s]).T).astype(F32)
-        U = (X @ mx_dequantize(wuq[s], wus[s]).T).astype(F32)
+        Wg, Wu = mx_dequantize(wgq[s], wgs[s]), mx_dequantize(wuq[s], wus[s])
+        G64, U64 = X @ Wg.T, X @ Wu.T
+        if parts:
+            P["G"][r0:r1], P["U"][r0:r1] = G64, U64
+            P["magG"][r0:r1], P["magU"][r0:r1] = np.abs(X) @ np.abs(Wg).T, np.abs(X) @ np.abs(Wu).T
+        G, U = G64.astype(F32), U64.astype(F32)
         with np.errstate(over="ignore"):
             sig = (F32(1.0) / (F32(1.0) + np.exp(-G))).astype(F32)
         h = ((G * sig).astype(F32) * U).astype(F32)
@@ -128,4 +135,6 @@ def grouped_swiglu_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets):
         Wd = mx_dequantize(wdq[s], wds[s])
         y[r0:r1] = bf16_rne((Hd @ Wd.T).astype(F32))
         mag[r0:r1] = np.abs(Hd) @ np.abs(Wd).T
+    if parts:
+        return hq, hs, h32, y, mag, P
     return hq, hs, h32, y, mag

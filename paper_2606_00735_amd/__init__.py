@@ -5,7 +5,8 @@ the per-expert activation profile, dispatch permutation, grouped SwiGLU
 expert FFN, weighted combine, and the per-expert latency-vs-load sweep from
 which the per-GPU performance model f_g(n) is fitted, and ViBE's placement
 control path on top of it (latency-aware greedy placement, drift detector,
-incremental swap solver). Every step runs in the
+incremental swap solver), and an MXFP8 (FP8 E4M3 with E8M0 block
+scales) variant of the expert FFN. Every step runs in the
 HIP kernels of ``libmoe.so`` (C ABI in ``include/moe.h``); this package only
 marshals torch tensors into those calls.
 """
@@ -13,7 +14,9 @@ from ._lib import (  # noqa: F401
     EXPORTED,
     LIB_PATH,
     MoeError,
+    MxTensor,
     ffn_hidden,
+    ffn_mx_ws_bytes,
     ffn_ws_bytes,
     hist_ws_bytes,
     load_library,
@@ -21,9 +24,13 @@ from ._lib import (  # noqa: F401
     moe_expert_histogram_scan,
     moe_fit_latency_model,
     moe_gate_topk,
+    moe_grouped_gemm_mx,
     moe_grouped_swiglu_ffn,
+    moe_grouped_swiglu_ffn_mx,
+    moe_grouped_swiglu_mx,
     moe_layer,
     moe_load_sweep,
+    moe_mx_quantize,
     moe_permute,
     moe_place_greedy,
     moe_place_incremental,

@@ -24,7 +24,8 @@ MAX_EXPERTS, MAX_TOPK = 256, 16
 EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert_histogram_scan",
             "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep",
             "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_placement_cost",
-            "moe_window_push", "moe_drift_distance")
+            "moe_window_push", "moe_drift_distance", "moe_mx_quantize", "moe_grouped_swiglu_mx",
+            "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx")
 
 
 class MoeError(RuntimeError):
@@ -78,6 +79,14 @@ def load_library(path: str = LIB_PATH):
     L.moe_window_push.argtypes = [_P, _P, _P, _I, _I, _I, _I, _P]
     L.moe_drift_distance.restype = _I
     L.moe_drift_distance.argtypes = [_P, _P, _I, _I, _D, _P, _P, _P]
+    L.moe_mx_quantize.restype = _I
+    L.moe_mx_quantize.argtypes = [_P, _I, _I, _I, _I, _P, _P, _P]
+    L.moe_grouped_swiglu_mx.restype = _I
+    L.moe_grouped_swiglu_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P]
+    L.moe_grouped_gemm_mx.restype = _I
+    L.moe_grouped_gemm_mx.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P]
+    L.moe_grouped_swiglu_ffn_mx.restype = _I
+    L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _PSZ, _P]
     if L.moe_abi_version() != 1:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
@@ -401,3 +410,113 @@ def moe_drift_distance(w_cur, w_ref, delta=0.05, d=None, trigger=None):
                               _stream())
     _check("moe_drift_distance", st)
     return d, trigger
+
+
+# ---------------------------------------------------------------------------
+# MXFP8 expert FFN
+# ---------------------------------------------------------------------------
+class MxTensor:
+    """An MXFP8 operand: E4M3 codes [.., R, K] uint8 and scale dwords
+    [.., K/128, R] int32 (byte b of dword (k, r): the E8M0 code of elements
+    [128 k + 32 b, +32) of row r)."""
+
+    def __init__(self, codes, scales):
+        if codes.dtype != torch.uint8 or scales.dtype != torch.int32:
+            raise ValueError("MXFP8 codes are uint8 and scales int32")
+        R, K = codes.shape[-2:]
+        if tuple(scales.shape[-2:]) != (K // 128, R) or codes.shape[:-2] != scales.shape[:-2]:
+            raise ValueError("scales must be [.., K/128, R] for codes [.., R, K]")
+        self.codes, self.scales = codes, scales
+
+    @property
+    def shape(self):
+        return tuple(self.codes.shape)
+
+
+def moe_mx_quantize(x, out=None):
+    """MXFP8 quantisation of x [R, K] or [B, R, K] (bf16 or fp32) along K."""
+    L = load_library()
+    xb = x.unsqueeze(0) if x.dim() == 2 else x
+    B, R, K = xb.shape
+    if out is None:
+        out = MxTensor(torch.empty(x.shape, dtype=torch.uint8, device=x.device),
+                       torch.empty(tuple(x.shape[:-2]) + (K // 128, R), dtype=torch.int32, device=x.device))
+    st = L.moe_mx_quantize(_dev(x, "x"), _dtype_code(x), B, R, K, _dev(out.codes, "codes", torch.uint8),
+                           _dev(out.scales, "scales", torch.int32), _stream())
+    _check("moe_mx_quantize", st)
+    return out
+
+
+def _mx_dev(t, name, shape):
+    if not isinstance(t, MxTensor):
+        raise TypeError(f"{name} must be an MxTensor")
+    if t.shape != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {t.shape}")
+    return _dev(t.codes, name + ".codes", torch.uint8), _dev(t.scales, name + ".scales", torch.int32)
+
+
+def moe_grouped_swiglu_mx(x, w_gate, w_up, offsets, h=None):
+    """Gate/up half of the MXFP8 FFN: h = MXFP8(silu(x Wg^T) * (x Wu^T)) per local expert."""
+    L = load_library()
+    M_cap, H = x.shape
+    E_local, I, _ = w_gate.shape
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    dev = x.codes.device
+    if h is None:
+        h = MxTensor(torch.empty((M_cap, I), dtype=torch.uint8, device=dev),
+                     torch.empty((I // 128, M_cap), dtype=torch.int32, device=dev))
+    st = L.moe_grouped_swiglu_mx(*_mx_dev(x, "x", (M_cap, H)), *_mx_dev(w_gate, "w_gate", (E_local, I, H)),
+                                 *_mx_dev(w_up, "w_up", (E_local, I, H)), _dev(offsets, "offsets", torch.int32),
+                                 E_local, H, I, M_cap, *_mx_dev(h, "h", (M_cap, I)), _stream())
+    _check("moe_grouped_swiglu_mx", st)
+    return h
+
+
+def moe_grouped_gemm_mx(a, b, offsets, c=None):
+    """Grouped MXFP8 GEMM: c[R] = bf16(a[R] b[l]^T) per local expert l."""
+    L = load_library()
+    M_cap, K = a.shape
+    E_local, N, _ = b.shape
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    if c is None:
+        c = torch.empty((M_cap, N), dtype=torch.bfloat16, device=a.codes.device)
+    st = L.moe_grouped_gemm_mx(*_mx_dev(a, "a", (M_cap, K)), *_mx_dev(b, "b", (E_local, N, K)),
+                               _dev(offsets, "offsets", torch.int32), E_local, N, K, M_cap,
+                               _dev(c, "c", torch.bfloat16), _stream())
+    _check("moe_grouped_gemm_mx", st)
+    return c
+
+
+def ffn_mx_ws_bytes(E_local, H, I, M_cap):
+    L = load_library()
+    n = ctypes.c_size_t(0)
+    st = L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, E_local, H, I, M_cap,
+                                     None, None, ctypes.byref(n), None)
+    _check("moe_grouped_swiglu_ffn_mx", st)
+    return n.value
+
+
+def moe_grouped_swiglu_ffn_mx(x, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):
+    """MXFP8 expert FFN. Returns (y_perm [M_cap, H] bf16, ws); ws holds h codes
+    [M_cap, I] at byte 0 and h scales [I/128, M_cap] after them (256-aligned)."""
+    L = load_library()
+    M_cap, H = x.shape
+    E_local, I, _ = w_gate.shape
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    dev = x.codes.device
+    if ws is None:
+        ws = torch.empty(ffn_mx_ws_bytes(E_local, H, I, M_cap), dtype=torch.uint8, device=dev)
+    if y_perm is None:
+        y_perm = torch.empty((M_cap, H), dtype=torch.bfloat16, device=dev)
+    n = ctypes.c_size_t(ws.numel())
+    st = L.moe_grouped_swiglu_ffn_mx(*_mx_dev(x, "x", (M_cap, H)), *_mx_dev(w_gate, "w_gate", (E_local, I, H)),
+                                     *_mx_dev(w_up, "w_up", (E_local, I, H)),
+                                     *_mx_dev(w_down, "w_down", (E_local, H, I)),
+                                     _dev(offsets, "offsets", torch.int32), E_local, H, I, M_cap,
+                                     _dev(y_perm, "y_perm", torch.bfloat16), _dev(ws, "ws", torch.uint8),
+                                     ctypes.byref(n), _stream())
+    _check("moe_grouped_swiglu_ffn_mx", st)
+    return y_perm, ws

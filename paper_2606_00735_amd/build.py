@@ -16,8 +16,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmoe.so")
 
-SOURCES = ["route_kernels.hip", "ffn_kernels.hip", "placement_kernels.hip", "moe_abi.cpp"]
-HEADERS = ["common.hpp", "launch.hpp"]
+SOURCES = ["route_kernels.hip", "ffn_kernels.hip", "mx_kernels.hip", "placement_kernels.hip", "moe_abi.cpp"]
+HEADERS = ["common.hpp", "launch.hpp", "mx.hpp"]
 
 
 def hipcc() -> str:

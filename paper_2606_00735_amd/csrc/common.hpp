@@ -79,6 +79,33 @@ __device__ __forceinline__ void dma16(const void* gaddr, const bf16_t* lds) {
                : "memory");
 }
 
+// The same loads with a wave-uniform 64-bit base in SGPRs and a 32-bit
+// per-lane byte offset (global address = base + offset): one VGPR per load
+// instead of two. dma16s moves 16 bytes per lane, dma4s 4 bytes (lane i
+// writes LDS bytes [4 i, 4 i + 4) past `lds`).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+  return reinterpret_cast<const void*>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, const void* lds) {
+  const uint32_t m0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(m0)
+               : "memory");
+}
+
+__device__ __forceinline__ void dma4s(const void* sbase, uint32_t voff, const void* lds) {
+  const uint32_t m0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(m0)
+               : "memory");
+}
+
 // Loads rows [0, R) (BK bf16 each, starting at column `col0`) of a row-major
 // matrix with row stride `ld` into a swizzled LDS tile. Rows at or beyond
 // `row_limit` re-read row `row_limit - 1` (their results are never stored),
@@ -184,7 +211,12 @@ __device__ __forceinline__ void pipeline(int nK, bf16_t* smem, int stage_elems, 
 // overwrite data still being read. NS-1 chunks are in flight during each
 // chunk's MFMAs, as in pipeline(). On return no load is in flight and every
 // wave is done with the stages.
-template <int NS, int LOADS, int KS, class Issue, class Read, class Mma, class Mix>
+//
+// MMA_FIRST puts each k-step's MFMAs before the reads of the next k-step in
+// program order (the issue order is still set by mix()). A consumer can then
+// refill an operand register right after its last MFMA of the k-step instead
+// of keeping a second buffer for it.
+template <int NS, int LOADS, int KS, bool MMA_FIRST = false, class Issue, class Read, class Mma, class Mix>
 __device__ __forceinline__ void pipeline_xk(int nK, bf16_t* smem, int stage_elems, Issue&& issue, Read&& read,
                                             Mma&& mma, Mix&& mix) {
   static_assert(NS >= 2 && NS <= 8, "stages");
@@ -203,8 +235,13 @@ __device__ __forceinline__ void pipeline_xk(int nK, bf16_t* smem, int stage_elem
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s + 1 < KS; ++s) {
-      read(st, s + 1, (s + 1) & 1);
-      mma(s & 1);
+      if (MMA_FIRST) {
+        mma(s & 1);
+        read(st, s + 1, (s + 1) & 1);
+      } else {
+        read(st, s + 1, (s + 1) & 1);
+        mma(s & 1);
+      }
       mix();
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -216,8 +253,13 @@ __device__ __forceinline__ void pipeline_xk(int nK, bf16_t* smem, int stage_elem
     __builtin_amdgcn_sched_barrier(0);
     // first fragments of chunk c+1 (after the last chunk: an unused read of a
     // stage that holds a placeholder load; LDS reads cannot fault)
-    read(smem + nxt * stage_elems, 0, 0);
-    mma((KS - 1) & 1);
+    if (MMA_FIRST) {
+      mma((KS - 1) & 1);
+      read(smem + nxt * stage_elems, 0, 0);
+    } else {
+      read(smem + nxt * stage_elems, 0, 0);
+      mma((KS - 1) & 1);
+    }
     mix();
     __builtin_amdgcn_sched_barrier(0);
     cur = nxt;

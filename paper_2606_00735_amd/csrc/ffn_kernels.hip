@@ -18,6 +18,7 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "mx.hpp"
 
 namespace moe {
 
@@ -62,6 +63,14 @@ struct GemmArgs {
   long long part_cap;
   int32_t* plan;
   int plan_rows;  // rows the plan's row map holds
+  // MXFP8 GEMMs (grouped_gemm_mx_kernel): A, B0, B1 hold E4M3 codes (K bytes
+  // a row, moved as pairs of bf16 slots), As [K/128][M_cap] and
+  // Bs0/Bs1 [E_local][K/128][N] their scale dwords (mx.hpp); the dual GEMM
+  // writes E4M3 codes of h to C and their scale dwords to Cs [N/128][M_cap].
+  const uint32_t* As;
+  const uint32_t* Bs0;
+  const uint32_t* Bs1;
+  uint32_t* Cs;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -212,6 +221,220 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   }
 }
 
+// MXFP8 stages: the same 128-byte tile rows as the bf16 path (a K chunk is
+// 128 E4M3 codes), plus one scale dword per operand row. Every wave loads 64
+// scale rows per chunk (one global_load_lds_dword), so a stage holds
+// kWaves * 64 = 512 scale rows whatever its operand rows.
+template <int BM, int BN, bool DUAL>
+struct MxStages {
+  static constexpr int NB = DUAL ? 2 : 1;
+  static constexpr int AROWS = BM > kDmaRows ? BM : kDmaRows;
+  static constexpr int ROWS = AROWS + NB * BN;
+  static_assert(ROWS <= kWaves * 64, "one scale dword per operand row");
+  static constexpr int SCALE_OFF = ROWS * 2 * kBK;          // bytes
+  static constexpr int STAGE = SCALE_OFF + kWaves * 64 * 4;  // bytes
+  static constexpr int FIT = (152 * 1024) / STAGE;
+  static constexpr int NS = FIT < 2 ? 2 : (FIT > 8 ? 8 : FIT);
+  static constexpr int BYTES = STAGE * NS;
+  static constexpr int LOADS = ROWS / kDmaRows + 1;  // code rows, then the scale dword
+};
+
+__device__ __forceinline__ uint4 lds16(const bf16_t* lds, int row, int chunk) {
+  return *reinterpret_cast<const uint4*>(lds + row * kBK + swz_chunk<kBK>(row, chunk) * 8);
+}
+
+// One BM x BN MXFP8 tile (two when DUAL) over the whole K range, as
+// gemm_tile but with the scaled MFMA v_mfma_scale_f32_32x32x64_f8f6f4: a
+// k-step is 64 K, two per chunk. Lane l (row l % 32, h = l / 32) supplies
+// K elements [16 h, 16 h + 16) and [32 + 16 h, 48 + 16 h) of the k-step (16-byte
+// chunks 4 s + h and 4 s + 2 + h of k-step s) and the scale code of 32-block h,
+// i.e. byte 2 s + h of its row's scale dword; the instruction reads the code
+// from the low byte of the scale operand.
+// DUAL: h = SiLU(gate) * up is quantised per 32 columns (the 32 values of a
+// row and block sit in lanes l and l ^ 32) and written as E4M3 codes with their
+// scale dwords; otherwise C is written as bf16.
+template <int BM, int BN, int WAVES_M, bool DUAL>
+__device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0) {
+  using St = MxStages<BM, BN, DUAL>;
+  constexpr int NB = DUAL ? 2 : 1;
+  constexpr int WAVES_N = kWaves / WAVES_M;
+  constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int MI = WM / 32, NI = WN / 32;
+  constexpr int AR = St::AROWS;
+  static_assert(MI >= 1 && NI >= 1, "wave tile");
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int h = lane >> 5, r32 = lane & 31;
+  const int K = a.K, N = a.N, nK = K / kMxChunk;  // K: bytes of an operand row
+  const int a_rows = m_end - m0;
+  const char* A = reinterpret_cast<const char*>(a.A) + (size_t)m0 * K;
+  const char* B0 = reinterpret_cast<const char*>(a.B0) + ((size_t)e * N + n0) * K;
+  const char* B1 = DUAL ? reinterpret_cast<const char*>(a.B1) + ((size_t)e * N + n0) * K : nullptr;
+
+  // Loop-invariant byte offsets of this lane's 16-byte pieces (dma16s): one
+  // instruction moves 8 rows of 128 bytes, instruction t of wave w rows
+  // [8 (t kWaves + w), +8); A rows past the tile re-read its last row, as
+  // in dma_rows. Both weight matrices share offsets.
+  constexpr int RPI = 8, LA = AR / (RPI * kWaves), LB = BN / (RPI * kWaves);
+  uint32_t offA[LA], offB[LB];
+#pragma unroll
+  for (int t = 0; t < LA; ++t) {
+    const int r = (t * kWaves + wave) * RPI + lane / 8;
+    const int rr = r < a_rows ? r : a_rows - 1;
+    offA[t] = (uint32_t)(rr * K + swz_chunk<kBK>(r, lane % 8) * 16);
+  }
+#pragma unroll
+  for (int t = 0; t < LB; ++t) {
+    const int r = (t * kWaves + wave) * RPI + lane / 8;
+    offB[t] = (uint32_t)(r * K + swz_chunk<kBK>(r, lane % 8) * 16);
+  }
+  // Scale rows: wave w loads scale rows [64 w, 64 w + 64) of the stage, all
+  // in one operand (AR and BN are multiples of 64): A rows (clamped), the
+  // gate (or only) weight rows, the up weight rows, or a placeholder that
+  // re-reads A's first row.
+  const int q0 = wave * 64;
+  const char* sb_base;
+  size_t s_stride;  // bytes per K chunk
+  uint32_t soff;
+  if (q0 < AR) {
+    sb_base = reinterpret_cast<const char*>(a.As + m0);
+    s_stride = (size_t)a.M_cap * 4;
+    soff = (uint32_t)(min(q0 + lane, a_rows - 1) * 4);
+  } else if (q0 < AR + BN) {
+    sb_base = reinterpret_cast<const char*>(a.Bs0 + (size_t)e * nK * N + n0 + (q0 - AR));
+    s_stride = (size_t)N * 4;
+    soff = (uint32_t)(lane * 4);
+  } else if (DUAL && q0 < AR + 2 * BN) {
+    sb_base = reinterpret_cast<const char*>(a.Bs1 + (size_t)e * nK * N + n0 + (q0 - AR - BN));
+    s_stride = (size_t)N * 4;
+    soff = (uint32_t)(lane * 4);
+  } else {
+    sb_base = reinterpret_cast<const char*>(a.As + m0);
+    s_stride = (size_t)a.M_cap * 4;
+    soff = 0;
+  }
+
+  f32x16_t acc[NB][MI][NI];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
+
+  // A placeholder load (live == false) re-reads the last chunk, which is in
+  // the cache by then, so loads never leave the operands.
+  auto issue = [&](int kc, bool live, bf16_t* st) {
+    const int kcl = live ? kc : nK - 1;
+    char* sl = reinterpret_cast<char*>(st);
+    const void* pa = uniform_ptr(A + (size_t)kcl * kMxChunk);
+#pragma unroll
+    for (int t = 0; t < LA; ++t) dma16s(pa, offA[t], sl + (t * kWaves + wave) * RPI * 128);
+    const void* pb0 = uniform_ptr(B0 + (size_t)kcl * kMxChunk);
+#pragma unroll
+    for (int t = 0; t < LB; ++t) dma16s(pb0, offB[t], sl + (AR + (t * kWaves + wave) * RPI) * 128);
+    if (DUAL) {
+      const void* pb1 = uniform_ptr(B1 + (size_t)kcl * kMxChunk);
+#pragma unroll
+      for (int t = 0; t < LB; ++t) dma16s(pb1, offB[t], sl + (AR + BN + (t * kWaves + wave) * RPI) * 128);
+    }
+    dma4s(uniform_ptr(sb_base + (size_t)kcl * s_stride), soff, sl + St::SCALE_OFF + wave * 256);
+  };
+  // A fragments (and scales) are double buffered; a weight fragment is
+  // refilled for the next k-step once its MI MFMAs of this k-step are issued
+  // (pipeline_xk with MMA_FIRST), which keeps the tile within 256 VGPRs.
+  int32x8_t af[2][MI], bfr[NB][NI];
+  uint32_t sa[2][MI], sb[NB][NI];
+  auto frag = [&](const bf16_t* t, int row, int s) {
+    const uint4 lo = lds16(t, row, 4 * s + h), hi = lds16(t, row, 4 * s + 2 + h);
+    return int32x8_t{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+  };
+  auto read = [&](const bf16_t* st, int s, int buf) {
+    const uint32_t* sc = reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(st) + St::SCALE_OFF);
+    const int sh = 8 * (2 * s + h);
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int row = wm * WM + i * 32 + r32;
+      af[buf][i] = frag(st, row, s);
+      sa[buf][i] = sc[row] >> sh;
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int row = wn * WN + j * 32 + r32;
+        bfr[b][j] = frag(st + (AR + b * BN) * kBK, row, s);
+        sb[b][j] = sc[AR + b * BN + row] >> sh;
+      }
+  };
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          acc[b][i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              bfr[b][j], af[buf][i], acc[b][i][j], 0, 0, 0, (int)sb[b][j], 0, (int)sa[buf][i]);
+  };
+  auto mix = [&]() {
+    constexpr int NREAD = 3 * (MI + NB * NI), NMFMA = NB * MI * NI;
+    constexpr int PAIRS = NREAD < NMFMA ? NREAD : NMFMA;
+#pragma unroll
+    for (int p = 0; p < PAIRS; ++p) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    }
+    if (NMFMA > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - PAIRS, 0);
+    if (NREAD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - PAIRS, 0);
+  };
+  pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(nK, smem, St::STAGE / 2, issue, read, mma, mix);
+
+  // Epilogue: output layout as in gemm_tile (lane l: row l % 32, columns
+  // 8 g + 4 h + (0..3) of each 32-column block).
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int row = m0 + wm * WM + i * 32 + r32;
+    const bool ok = row < m_end;  // the same for lanes l and l ^ 32
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const int col0 = n0 + wn * WN + j * 32;
+      if (DUAL) {
+        float r[16];
+        float amax = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          r[v] = silu_mul_fast(acc[0][i][j][v], acc[NB - 1][i][j][v]);
+          amax = fmaxf(amax, fabsf(r[v]));
+        }
+        amax = fmaxf(amax, __shfl_xor(amax, 32, kWave));
+        const uint32_t code = mx_scale_code(amax);
+        const float inv = mx_inv_scale(code);
+        if (ok) {
+          uint8_t* crow = reinterpret_cast<uint8_t*>(a.C) + (size_t)row * N + col0 + 4 * h;
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<uint32_t*>(crow + 8 * g) =
+                e4m3x4(r[4 * g] * inv, r[4 * g + 1] * inv, r[4 * g + 2] * inv, r[4 * g + 3] * inv);
+          if (h == 0)
+            reinterpret_cast<uint8_t*>(a.Cs + (size_t)(col0 / kMxChunk) * a.M_cap + row)[(col0 / kMxBlock) & 3] =
+                static_cast<uint8_t>(code);
+        }
+      } else if (ok) {
+        bf16_t* crow = a.C + (size_t)row * N + col0 + 4 * h;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          uint2 packed;
+          packed.x = pack_bf16x2(acc[0][i][j][4 * g], acc[0][i][j][4 * g + 1]);
+          packed.y = pack_bf16x2(acc[0][i][j][4 * g + 2], acc[0][i][j][4 * g + 3]);
+          *reinterpret_cast<uint2*>(crow + 8 * g) = packed;
+        }
+      }
+    }
+  }
+}
+
 template <bool DUAL>
 struct GemmShapes {
   // dual: 128 columns per matrix; single: 128 or 256 columns (see the kernel)
@@ -278,10 +501,44 @@ __device__ __forceinline__ void block_scan(int (&v)[NV], int (&excl)[NV], int (&
 }
 
 template <bool DUAL>
-__global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a) {
-  using Sh = GemmShapes<DUAL>;
+struct MxShapes {
+  static constexpr int BNW = DUAL ? 128 : 256;
+  static constexpr int b0 = MxStages<64, BNW, DUAL>::BYTES, b1 = MxStages<128, BNW, DUAL>::BYTES;
+  static constexpr int b2 = MxStages<256, BNW, DUAL>::BYTES, b3 = MxStages<256, 128, DUAL>::BYTES;
+  static constexpr int b4 = MxStages<64, 128, DUAL>::BYTES, b5 = MxStages<128, 128, DUAL>::BYTES;
+  static constexpr int m01 = b0 > b1 ? b0 : b1, m23 = b2 > b3 ? b2 : b3, m45 = b4 > b5 ? b4 : b5;
+  static constexpr int m = m01 > m23 ? m01 : m23;
+  static constexpr int kSmem = (m > m45 ? m : m45) / 2;  // bf16 slots
+};
+
+// One row tile of an unsplit launch: 128 or (single GEMM, wide) 256 columns.
+template <bool DUAL, bool MX, bool WIDE>
+__device__ __forceinline__ void run_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
+                                         int n0) {
+  constexpr int BN = WIDE ? 256 : 128;
+  if constexpr (MX) {
+    if (cls == 0)
+      gemm_tile_mx<64, BN, 2, DUAL>(a, smem, e, m0, m_end, n0);
+    else if (cls == 1)
+      gemm_tile_mx<128, BN, 2, DUAL>(a, smem, e, m0, m_end, n0);
+    else
+      gemm_tile_mx<256, BN, 4, DUAL>(a, smem, e, m0, m_end, n0);
+  } else {
+    if (cls == 0)
+      gemm_tile<64, BN, 2, DUAL>(a, smem, e, m0, m_end, n0);
+    else if (cls == 1)
+      gemm_tile<128, BN, 2, DUAL>(a, smem, e, m0, m_end, n0);
+    else
+      gemm_tile<256, BN, 4, DUAL>(a, smem, e, m0, m_end, n0);
+  }
+}
+
+// Body of the grouped GEMM kernels (bf16, or MXFP8 without split-K).
+template <bool DUAL, bool MX>
+__device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
+  constexpr int kSmem = MX ? MxShapes<DUAL>::kSmem : GemmShapes<DUAL>::kSmem;
   constexpr int NB = DUAL ? 2 : 1;
-  __shared__ __align__(16) bf16_t smem[Sh::kSmem];
+  __shared__ __align__(16) bf16_t smem[kSmem];
   __shared__ int s_start[kMaxExperts + 1];
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
@@ -312,7 +569,7 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
   // still gets at least two of them.
   const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 2 * G);
   int S = 1;
-  if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
+  if (!MX && !wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
     const int nK = a.K / kBK;
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
     for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
@@ -334,7 +591,7 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     s_srow0[tid] = ex[1];
   }
   __syncthreads();
-  if (blockIdx.x == 0) {
+  if (!MX && blockIdx.x == 0) {
     if (tid == 0) {
       a.plan[0] = S;
       a.plan[1] = R;
@@ -357,25 +614,27 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     const int local = tile - s_start[e];
     const int er = s_rows[e];
     const int n_mt = row_tiles(er);
-    if (S > 1) {
-      // split tile: S consecutive tiles share a row tile and a column block
-      const int sp = local % S, rest = local / S;
-      const int nt = rest / n_mt, mt = rest - nt * n_mt;
-      const int nK = a.K / kBK;
-      const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
-      const int m0 = s_row0[e] + mt * 256;
-      const int left = er - mt * 256;
-      const int m_end = m0 + (left < 256 ? left : 256);
-      float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
-      const size_t ps = (size_t)S * R * a.N;
-      const int cls = tile_class(left);
-      if (cls == 0)
-        gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-      else if (cls == 1)
-        gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-      else
-        gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-      continue;
+    if constexpr (!MX) {
+      if (S > 1) {
+        // split tile: S consecutive tiles share a row tile and a column block
+        const int sp = local % S, rest = local / S;
+        const int nt = rest / n_mt, mt = rest - nt * n_mt;
+        const int nK = a.K / kBK;
+        const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
+        const int m0 = s_row0[e] + mt * 256;
+        const int left = er - mt * 256;
+        const int m_end = m0 + (left < 256 ? left : 256);
+        float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
+        const size_t ps = (size_t)S * R * a.N;
+        const int cls = tile_class(left);
+        if (cls == 0)
+          gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+        else if (cls == 1)
+          gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+        else
+          gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+        continue;
+      }
     }
     // row tile fastest: all row tiles of a weight column block run together
     const int nt = local / n_mt, mt = local - nt * n_mt;
@@ -383,22 +642,23 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a)
     const int left = er - mt * 256;  // rows from m0 to the expert's end, >= 1
     const int cls = tile_class(left);
     const int m_end = m0 + (left < 256 ? left : 256);
-    if (!DUAL && wide) {
-      if (cls == 0)
-        gemm_tile<64, 256, 2, DUAL>(a, smem, e, m0, m_end, nt * 256);
-      else if (cls == 1)
-        gemm_tile<128, 256, 2, DUAL>(a, smem, e, m0, m_end, nt * 256);
-      else
-        gemm_tile<256, 256, 4, DUAL>(a, smem, e, m0, m_end, nt * 256);
-    } else {
-      if (cls == 0)
-        gemm_tile<64, 128, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
-      else if (cls == 1)
-        gemm_tile<128, 128, 2, DUAL>(a, smem, e, m0, m_end, nt * 128);
-      else
-        gemm_tile<256, 128, 4, DUAL>(a, smem, e, m0, m_end, nt * 128);
-    }
+    if (!DUAL && wide)
+      run_tile<DUAL, MX, !DUAL>(a, smem, cls, e, m0, m_end, nt * 256);
+    else
+      run_tile<DUAL, MX, false>(a, smem, cls, e, m0, m_end, nt * 128);
   }
+}
+
+template <bool DUAL>
+__global__ __launch_bounds__(kThreads) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  grouped_gemm_body<DUAL, false>(a);
+}
+
+// MXFP8 grouped GEMM: the same tile schedule (no split-K); the dual GEMM
+// writes MXFP8 h, the single one bf16.
+template <bool DUAL>
+__global__ __launch_bounds__(kThreads) void grouped_gemm_mx_kernel(GemmArgs a) {
+  grouped_gemm_body<DUAL, true>(a);
 }
 
 // Sums the S split-K partials of every row of a split launch in split order,
@@ -608,6 +868,75 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   if (e != hipSuccess) return e;
   if (split_dn) split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// MXFP8 expert FFN: gate/up (MXFP8 in, MXFP8 h out), then down (bf16 out)
+// ---------------------------------------------------------------------------
+// One 8-wave block per CU, at most the unsplit tile bound, a multiple of 8.
+static unsigned mx_grid(int M_cap, int E_local, int N) {
+  const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128);
+  long long g = device_cu_count();
+  if (ub < g) g = ub;
+  if (g >= 8) g &= ~7LL;
+  return (unsigned)(g < 1 ? 1 : g);
+}
+
+hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                            const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
+                            int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  GemmArgs g{};
+  g.A = reinterpret_cast<const bf16_t*>(xq);
+  g.B0 = reinterpret_cast<const bf16_t*>(wgq);
+  g.B1 = reinterpret_cast<const bf16_t*>(wuq);
+  g.C = reinterpret_cast<bf16_t*>(hq);
+  g.offsets = offsets;
+  g.E_local = E_local;
+  g.M_cap = M_cap;
+  g.N = I;
+  g.K = H;
+  g.As = xs;
+  g.Bs0 = wgs;
+  g.Bs1 = wus;
+  g.Cs = hs;
+  grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I), kThreads, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
+                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  GemmArgs g{};
+  g.A = reinterpret_cast<const bf16_t*>(aq);
+  g.B0 = reinterpret_cast<const bf16_t*>(bq);
+  g.C = static_cast<bf16_t*>(c);
+  g.offsets = offsets;
+  g.E_local = E_local;
+  g.M_cap = M_cap;
+  g.N = N;
+  g.K = K;
+  g.As = as;
+  g.Bs0 = bs;
+  grouped_gemm_mx_kernel<false><<<mx_grid(M_cap, E_local, N), kThreads, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+// workspace: h codes [M_cap, I] | h scale dwords [I/128][M_cap]
+size_t ffn_mx_ws_bytes(int M_cap, int I) {
+  return round256((size_t)M_cap * I) + round256((size_t)(I / kMxChunk) * M_cap * 4);
+}
+
+hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                         const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
+                         const int32_t* offsets, int E_local, int H, int I, int M_cap, void* y_perm, void* ws,
+                         hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  uint8_t* hq = static_cast<uint8_t*>(ws);
+  uint32_t* hs = reinterpret_cast<uint32_t*>(hq + round256((size_t)M_cap * I));
+  hipError_t e = launch_gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, s);
+  if (e != hipSuccess) return e;
+  return launch_gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, s);
 }
 
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {

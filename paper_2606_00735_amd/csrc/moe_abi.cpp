@@ -265,6 +265,87 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
 }  // extern "C"
 
 // ---------------------------------------------------------------------------
+// MXFP8 expert FFN
+// ---------------------------------------------------------------------------
+namespace {
+
+// Shape limits of the MXFP8 GEMMs: every K and N a multiple of the 128-wide
+// scale chunk, row and byte counts within int / size_t range.
+moe_status mx_gemm_shape_ok(int E_local, int N, int K, int M_cap) {
+  if (E_local < 0 || N < 1 || K < 1 || M_cap < 0) return MOE_ERR_INVALID_ARG;
+  if (E_local > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
+  if (N % 128 != 0 || K % 128 != 0) return MOE_ERR_UNSUPPORTED;
+  // tile offsets (256 rows of K bytes) are 32-bit in the kernels
+  if (N > (1 << 20) || K > (1 << 20)) return MOE_ERR_UNSUPPORTED;
+  if ((long long)M_cap * std::max(N, K) > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+bool mx_operand_ok(const void* codes, const void* scales) {
+  return codes && scales && aligned16(codes) && aligned4(scales);
+}
+
+}  // namespace
+
+extern "C" {
+
+moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, uint8_t* codes,
+                           uint32_t* scales, hipStream_t stream) {
+  if (!valid_dtype(dt) || batch < 0 || rows < 0 || K < 1) return MOE_ERR_INVALID_ARG;
+  if (K % 128 != 0) return MOE_ERR_UNSUPPORTED;
+  if ((long long)batch * rows * K > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
+  if (batch == 0 || rows == 0) return MOE_OK;
+  if (!x || !aligned16(x) || !mx_operand_ok(codes, scales)) return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_mx_quantize(x, dt == MOE_F32, batch, rows, K, codes, scales, stream));
+}
+
+moe_status moe_grouped_swiglu_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                                 const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local,
+                                 int H, int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t stream) {
+  moe_status st = mx_gemm_shape_ok(E_local, I, H, M_cap);
+  if (st != MOE_OK) return st;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) || !mx_operand_ok(hq, hs) ||
+      !offsets || !aligned4(offsets))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, stream));
+}
+
+moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
+                               const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c,
+                               hipStream_t stream) {
+  moe_status st = mx_gemm_shape_ok(E_local, N, K, M_cap);
+  if (st != MOE_OK) return st;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!mx_operand_ok(aq, as) || !mx_operand_ok(bq, bs) || !c || !aligned16(c) || !offsets || !aligned4(offsets))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, M_cap, c, stream));
+}
+
+moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                                     const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq,
+                                     const uint32_t* wds, const int32_t* offsets, int E_local, int H, int I,
+                                     int M_cap, void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream) {
+  moe_status st = mx_gemm_shape_ok(E_local, I, H, M_cap);
+  if (st != MOE_OK) return st;
+  if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
+  const size_t need = moe::ffn_mx_ws_bytes(M_cap, I);
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) ||
+      !mx_operand_ok(wdq, wds) || !y_perm || !aligned16(y_perm) || !aligned16(ws) || !offsets || !aligned4(offsets))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets, E_local, H, I, M_cap, y_perm,
+                                       ws, stream));
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
 // Placement control path
 // ---------------------------------------------------------------------------
 namespace {

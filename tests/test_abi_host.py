@@ -222,3 +222,35 @@ def test_place_incremental_and_drift_validation(L):
     assert L.moe_window_push(FAKE, FAKE, D8, 4, 8, 10, 10, None) == INVALID   # slot >= window
     assert L.moe_window_push(FAKE, FAKE, D8, 4, 8, 0, 0, None) == INVALID     # window < 1
     assert L.moe_window_push(None, None, None, 0, 8, 10, 3, None) == 0        # L = 0: no-op
+
+
+def test_mx_validation_and_query(L):
+    """MXFP8 entry points: shapes off the 128 grid are unsupported, missing or
+    misaligned operands invalid, the workspace query sized for h codes and
+    their scale dwords."""
+    n = ctypes.c_size_t(0)
+    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, 4096, 14336, 8192,
+                                       None, None, ctypes.byref(n), None) == 0
+    assert n.value >= 8192 * 14336 + (14336 // 128) * 8192 * 4
+    for H, I in ((4096, 14300), (4000, 14336)):
+        assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, H, I, 64,
+                                           None, None, ctypes.byref(n), None) == UNSUPPORTED
+    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 300, 128, 128, 64,
+                                       None, None, ctypes.byref(n), None) == UNSUPPORTED
+    n = ctypes.c_size_t(10)
+    assert L.moe_grouped_swiglu_ffn_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 64,
+                                       FAKE, FAKE, ctypes.byref(n), None) == WORKSPACE
+    # quantiser: K % 128, dtype, null and misaligned pointers
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 200, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.moe_mx_quantize(FAKE, 7, 1, 4, 256, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 256, None, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(MISALIGNED, 1, 1, 4, 256, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(None, 1, 0, 4, 256, None, None, None) == 0     # empty: no-op
+    # GEMMs
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 100, 256, 64, FAKE, None) == UNSUPPORTED
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, None, FAKE, FAKE, 2, 128, 256, 64, FAKE, None) == INVALID
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, -1, 128, 256, 64, FAKE, None) == INVALID
+    assert L.moe_grouped_swiglu_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 128, 384, 64, FAKE, None,
+                                   None) == INVALID
+    assert L.moe_grouped_swiglu_mx(None, None, None, None, None, None, None, 0, 128, 384, 64, None, None,
+                                   None) == 0

@@ -1,0 +1,364 @@
+"""GPU parity of the MXFP8 expert FFN (quantiser, gate/up, down, whole FFN)
+against the MXFP8 oracle, through the C ABI.
+
+Rules (fixed before any GPU run):
+* quantisation (codes and scale codes): bit-exact.
+* GEMM outputs: the hardware's FP8 dot products are not exact; a probe of
+  the scaled MFMA put its error at up to 1.5e-4 of the sum of the term
+  magnitudes, so each output may differ from the fp64 result by
+  MFMA_F8_REL = 2^-10 of sum |a_i b_i| (about 6x that), plus one bf16
+  rounding on each side.
+* h (quantised in the gate/up epilogue from fp32 G, U that differ from the
+  oracle's within the rule above): the scale code of each block must be one
+  the oracle allows for some h within the error bound of its block, and each
+  code must lie between the codes of h - bound and h + bound under that
+  scale (quantisation at a fixed scale is monotone). The whole FFN then
+  allows y the effect of every such code difference on top of the GEMM rule.
+
+Inputs: each side quantises the same seeded synthetic values with its own
+code; the tests first check that the codes agree bit for bit.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_00735_amd as moe
+from oracle import mx_oracle as X
+from oracle import moe_oracle as O
+from synth import CONFIGS, make_layer
+from synth.moe_inputs import make_experts, make_router
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+MFMA_F8_REL = 2.0 ** -10
+
+
+def banner(*a):
+    print("CASE", *a, flush=True)
+
+
+def up(a, dtype=torch.bfloat16):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(DEV).to(dtype).contiguous()
+
+
+def gpu_scales(scales, R, K):
+    """Scale dwords [.., K/128, R] -> E8M0 codes [.., R, K/32] (the oracle's layout)."""
+    s = scales.cpu().numpy().view(np.uint8)
+    s = s.reshape(s.shape[:-2] + (K // 128, R, 4))
+    s = np.swapaxes(s, -3, -2)
+    return np.ascontiguousarray(s.reshape(s.shape[:-3] + (R, K // 32)))
+
+
+def oracle_quant(a, chunk=256):
+    """Row-chunked oracle quantisation (the MX blocks lie within rows)."""
+    a = np.asarray(a)
+    q = np.empty(a.shape, np.uint8)
+    s = np.empty(a.shape[:-1] + (a.shape[-1] // 32,), np.uint8)
+    flat_a, flat_q, flat_s = a.reshape(-1, a.shape[-1]), q.reshape(-1, a.shape[-1]), s.reshape(-1, s.shape[-1])
+    for r in range(0, flat_a.shape[0], chunk):
+        flat_q[r:r + chunk], flat_s[r:r + chunk] = X.mx_quantize(flat_a[r:r + chunk])
+    return q, s
+
+
+def check_quant(t, a, what):
+    """GPU MxTensor t == oracle quantisation of a, bit for bit. Returns the oracle's (codes, scales)."""
+    torch.cuda.synchronize()
+    K = a.shape[-1]
+    R = a.shape[-2]
+    q, s = oracle_quant(a)
+    gq = t.codes.cpu().numpy()
+    gs = gpu_scales(t.scales, R, K)
+    bad_s = gs != s
+    assert not bad_s.any(), f"{what}: {bad_s.sum()} scale codes differ, first at {np.argwhere(bad_s)[0]}"
+    bad = gq != q
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{what}: {bad.sum()} codes differ; first {i}: value {a[i]!r} "
+                             f"gpu {gq[i]:#04x} oracle {q[i]:#04x}")
+    return q, s
+
+
+def check_gemm(got, ref, mag, what, extra=0.0):
+    """GEMM rule; `extra` is a further allowance per element (h code differences)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert np.all(np.isfinite(got)), what
+    tol = MFMA_F8_REL * mag + extra + 2.0 ** -7 * np.maximum(np.abs(ref), np.abs(got)) + 1e-30
+    err = np.abs(got - ref)
+    bad = err > tol
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{what}: {bad.sum()} of {bad.size} outside; first {i}: gpu {got[i]} "
+                             f"oracle {ref[i]} mag {mag[i]} tol {tol[i]}")
+    rel = float(np.max(err / np.maximum(mag, 1e-30)))
+    print(f"  {what}: max |err|/mag = {rel:.2e}", flush=True)
+
+
+def h_bounds(P, h32):
+    """Per-element bound on |h_gpu - h_oracle| before quantisation."""
+    G, U = P["G"], P["U"]
+    dG = MFMA_F8_REL * P["magG"] + 2.0 ** -23 * np.abs(G)
+    dU = MFMA_F8_REL * P["magU"] + 2.0 ** -23 * np.abs(U)
+    with np.errstate(over="ignore"):
+        silu = G / (1.0 + np.exp(-G))
+    return 1.1 * dG * (np.abs(U) + dU) + np.abs(silu) * dU + 2.0 ** -20 * np.abs(h32.astype(np.float64)) + 1e-38
+
+
+def q_at(v, code):
+    """Dequantised value of v quantised at scale code `code` (per element)."""
+    sc = np.exp2(code.astype(np.float64) - 127.0)
+    return X.e4m3_decode(X.e4m3_encode(np.clip(v / sc, -X.E4M3_MAX, X.E4M3_MAX))) * sc
+
+
+def scale_code(amax):
+    _, ex = np.frexp(np.where(amax > 0, amax, 1.0))
+    return np.where(amax > 0, ex - 1.0 - 8.0, -127.0).clip(-127.0, 127.0) + 127.0
+
+
+def allowed_h(h32, P):
+    """Interval [lo, hi] around the oracle's h that holds the GPU's h before
+    quantisation, and the range [s_lo, s_hi] of block scale codes it allows."""
+    m, I = h32.shape
+    tol = h_bounds(P, h32)
+    h = h32.astype(np.float64)
+    lo, hi = h - tol, h + tol
+    blk = lambda a: a.reshape(m, I // 32, 32)
+    mag_lo = np.where((lo > 0) | (hi < 0), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
+    s_lo = scale_code(blk(mag_lo).max(-1))
+    s_hi = scale_code(blk(np.maximum(np.abs(lo), np.abs(hi))).max(-1))
+    return lo, hi, s_lo, s_hi
+
+
+def h_deviation(lo, hi, s_lo, s_hi, hq, hs):
+    """Largest |dequantised h_gpu - oracle Hd| any allowed code can give."""
+    Hd = X.mx_dequantize(hq, hs)
+    dev = np.zeros_like(Hd)
+    for s in (s_lo, s_hi):
+        sc = np.repeat(s, 32, axis=1)
+        dev = np.maximum(dev, np.maximum(np.abs(q_at(lo, sc) - Hd), np.abs(q_at(hi, sc) - Hd)))
+    return dev
+
+
+def check_h(ghq, ghs, hq, hs, h32, P, what):
+    """The h rule of the module docstring. Returns per-element |h_gpu - Hd| bound (fp64)."""
+    lo, hi, s_lo, s_hi = allowed_h(h32, P)
+    gs = ghs.astype(np.float64)
+    assert np.all((gs >= s_lo) & (gs <= s_hi)), f"{what}: scale codes outside the allowed range"
+    gsc = np.repeat(gs, 32, axis=1)
+    gv = X.mx_dequantize(ghq, ghs)
+    qlo, qhi = q_at(lo, gsc), q_at(hi, gsc)
+    bad = (gv < qlo) | (gv > qhi)
+    assert not bad.any(), f"{what}: {bad.sum()} h codes outside the bound"
+    diff = float(np.mean(ghq != hq))
+    print(f"  {what}: {diff:.2e} of h codes differ from the oracle's (all within the bound), "
+          f"{float(np.mean(ghs != hs)):.1e} of scales", flush=True)
+    assert diff < 0.02
+    return h_deviation(lo, hi, s_lo, s_hi, hq, hs)
+
+
+# ---------------------------------------------------------------- quantiser
+def all_bf16_values():
+    u = np.arange(65536, dtype=np.uint32)
+    u = u[((u >> 7) & 0xFF) != 0xFF]           # finite values only: 65024 of them
+    return (u << 16).view(np.float32)
+
+
+def test_quantize_every_bf16_value():
+    banner("mx quantize: every finite bf16 value, sorted and shuffled blocks")
+    v = all_bf16_values()
+    for name, arr in (("sorted", v), ("shuffled", np.random.default_rng(0).permutation(v))):
+        a = arr.reshape(-1, 256)
+        t = moe.moe_mx_quantize(up(a))
+        check_quant(t, a, f"bf16 {name}")
+
+
+def test_quantize_f32_ties_clamp_and_zeros():
+    banner("mx quantize fp32: ties, clamp band, zeros, tiny blocks")
+    rng = np.random.default_rng(1)
+    R, K = 96, 384
+    a = (rng.standard_normal((R, K)) * np.exp2(rng.integers(-30, 30, (R, 1)))).astype(np.float32)
+    vals = X.e4m3_decode(np.arange(1, 127))
+    mids = ((vals[:-1] + vals[1:]) / 2)
+    for r in range(0, 32):                      # exact ties after scaling: blocks with amax 448 * 2^s
+        s = float(r - 10)
+        blk = rng.choice(mids, 31) * rng.choice([-1, 1], 31)
+        a[r, :32] = np.concatenate([[448.0], blk]).astype(np.float64) * 2.0 ** s
+    a[32, :] = 0.0
+    a[33, :64] = -0.0
+    a[34, :32] = np.float32(2.0 ** -140)         # fp32 denormals
+    a[35, :32] = 1.9 * 2.0 ** np.arange(32)[::-1] / 2.0 ** 20   # amax mantissa 1.9: the clamp band
+    a[36, :32] = -(2.0 ** -10) * rng.random(32)  # tiny negatives: signed zeros
+    t = moe.moe_mx_quantize(up(a, torch.float32))
+    check_quant(t, a, "f32")
+
+
+def test_quantize_batched_weights_layout():
+    banner("mx quantize batched [3, 256, 384]")
+    a = np.random.default_rng(2).standard_normal((3, 256, 384)).astype(np.float32)
+    a = (torch.from_numpy(a).bfloat16().float()).numpy()
+    t = moe.moe_mx_quantize(up(a))
+    assert tuple(t.scales.shape) == (3, 3, 256)
+    check_quant(t, a, "batched")
+
+
+# ---------------------------------------------------------------- GEMMs
+def _shape(H, I, n):
+    return dataclasses.replace(CONFIGS["qwen3"], name="mx", H=H, I=I, E=n, k=1, E_local=n)
+
+
+def _inputs(H, I, rows, seed, pad=3):
+    shape = _shape(H, I, len(rows))
+    wg, wu, wd = make_experts(shape, list(range(len(rows))), seed=seed)
+    m = sum(rows)
+    x, *_ = make_router(shape, max(m, 1), 0.0, seed=seed)
+    M_cap = m + pad
+    xp = np.zeros((M_cap, H), np.float32)
+    xp[:m] = x[:m]
+    offsets = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    return xp, wg, wu, wd, offsets, m
+
+
+GEMM_CASES = [
+    # (N, K, rows per expert): ragged tails of every tile class, empty experts
+    (768, 2048, [300, 0, 1, 65, 129]),
+    (2048, 7168, [40, 257]),
+    (1024, 512, [8192]),          # 32 row tiles x 8 column tiles
+    (4096, 512, [8192]),          # >= 4 tiles per CU: 256-column tiles
+]
+
+
+@pytest.mark.parametrize("N,K,rows", GEMM_CASES, ids=[f"N{n}-K{k}-rows{'_'.join(map(str, r))}"
+                                                     for n, k, r in GEMM_CASES])
+def test_grouped_gemm_mx(N, K, rows):
+    banner("mx gemm", N, K, rows, "seed 7")
+    _, _, b = make_experts(_shape(N, K, len(rows)), list(range(len(rows))), seed=7)   # [E, N, K]
+    m = sum(rows)
+    offsets = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    xa, *_ = make_router(_shape(K, N, len(rows)), max(m, 1), 0.0, seed=8)             # rows of K
+    a = np.zeros((m + 3, K), np.float32)
+    a[:m] = xa[:m]
+    ta, tb = moe.moe_mx_quantize(up(a)), moe.moe_mx_quantize(up(b))
+    aq, as_ = check_quant(ta, a, "a")
+    bq, bs = check_quant(tb, b, "b")
+    c = moe.moe_grouped_gemm_mx(ta, tb, torch.from_numpy(offsets).to(DEV))
+    torch.cuda.synchronize()
+    got = c.float().cpu().numpy()[:m]
+    sample = np.arange(m) if m <= 2048 else np.random.default_rng(0).choice(m, 512, replace=False)
+    ad = X.mx_dequantize(aq[sample], as_[sample])
+    eid = np.searchsorted(offsets, sample, side="right") - 1
+    ref = np.zeros((len(sample), N))
+    mag = np.zeros((len(sample), N))
+    for e in np.unique(eid):
+        sel = eid == e
+        bd = X.mx_dequantize(bq[e], bs[e])
+        ref[sel] = ad[sel] @ bd.T
+        mag[sel] = np.abs(ad[sel]) @ np.abs(bd).T
+    ref = O.bf16_rne(ref.astype(np.float32))
+    check_gemm(got[sample], ref, mag, f"gemm N={N} K={K}")
+
+
+FFN_CASES = [
+    (2048, 768, [300, 0, 1, 65, 129]),
+    (7168, 2048, [40, 257]),
+    (1024, 1024, [600, 5]),
+]
+
+
+@pytest.mark.parametrize("H,I,rows", FFN_CASES, ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}"
+                                                   for h, i, r in FFN_CASES])
+def test_ffn_mx(H, I, rows):
+    banner("mx ffn", H, I, rows, "seed 9")
+    xp, wg, wu, wd, offsets, m = _inputs(H, I, rows, seed=9)
+    tx = moe.moe_mx_quantize(up(xp))
+    tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (wg, wu, wd))
+    xq, xs = check_quant(tx, xp, "x")
+    (gq, gs), (uq, us), (dq, ds) = (check_quant(t, w, n) for t, w, n in ((tg, wg, "wg"), (tu, wu, "wu"),
+                                                                         (td, wd, "wd")))
+    doff = torch.from_numpy(offsets).to(DEV)
+    y, ws = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, doff)
+    h = moe.moe_grouped_swiglu_mx(tx, tg, tu, doff)
+    torch.cuda.synchronize()
+    hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq[:m], xs[:m], gq, gs, uq, us, dq, ds, offsets, parts=True)
+    ghq = h.codes.cpu().numpy()[:m]
+    ghs = gpu_scales(h.scales, xp.shape[0], I)[:m]
+    # the FFN's workspace holds the same h as the gate/up entry point
+    M_cap = xp.shape[0]
+    wsn = ws.cpu().numpy()
+    assert np.array_equal(wsn[:M_cap * I].reshape(M_cap, I)[:m], ghq)
+    dev = check_h(ghq, ghs, hq, hs, h32, P, f"h H={H} I={I}")
+    got = y.float().cpu().numpy()[:m]
+    # y: GEMM rule on the oracle's h, plus the effect of every allowed h code difference
+    allow = np.zeros_like(mag)
+    for e in range(len(rows)):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 > r0:
+            Wd = np.abs(X.mx_dequantize(dq[e], ds[e]))
+            allow[r0:r1] = dev[r0:r1] @ Wd.T
+    # the GPU's down GEMM sums |h_gpu| |W_down| <= mag + allow
+    check_gemm(got, y_ref, mag + allow, f"ffn y H={H} I={I}", extra=allow)
+
+
+def test_ffn_mx_rows_of_empty_experts_untouched():
+    banner("mx ffn: rows past offsets[-1] are not written")
+    xp, wg, wu, wd, offsets, m = _inputs(1024, 1024, [0, 70, 0], seed=11, pad=40)
+    tx = moe.moe_mx_quantize(up(xp))
+    tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (wg, wu, wd))
+    y = torch.full((xp.shape[0], 1024), 7.0, dtype=torch.bfloat16, device=DEV)
+    moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, torch.from_numpy(offsets).to(DEV), y_perm=y)
+    torch.cuda.synchronize()
+    assert torch.all(y[m:] == 7.0)
+    assert torch.all(torch.isfinite(y[:m].float()))
+
+
+# ---------------------------------------------------------------- full size
+def test_ffn_mx_fullsize_mixtral_t4096():
+    """Mixtral-shaped layer at T = 4096, skew 1.0 (8 experts, 8192 routed rows):
+    routing from the oracle, the FFN in the bench's launch configuration,
+    sampled rows of the hottest and the coldest expert checked."""
+    banner("mx ffn fullsize mixtral T=4096 a=1.0 seed 0")
+    li = make_layer("mixtral", 4096, 1.0, seed=0)
+    H, I = li.shape.H, li.shape.I
+    z = O.router_logits(li.x, li.w_router, li.bias)
+    ids = O.topk_select(z, li.shape.k)
+    counts = O.expert_histogram(ids, li.shape.E)
+    offsets = O.local_offsets(counts, li.expert_map)
+    x_perm, _, _ = O.permute(li.x, ids, li.expert_map, offsets)
+    m = int(offsets[-1])
+    tx = moe.moe_mx_quantize(up(x_perm))
+    tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (li.w_gate, li.w_up, li.w_down))
+    y, _ = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, torch.from_numpy(offsets.astype(np.int32)).to(DEV))
+    torch.cuda.synchronize()
+    got = y.float().cpu().numpy()
+    rows_e = np.diff(offsets)
+    hot, cold = int(np.argmax(rows_e)), int(np.argmin(np.where(rows_e > 0, rows_e, 1 << 30)))
+    print(f"  M_loc={m} rows per expert {rows_e.tolist()}", flush=True)
+    for e in (hot, cold):
+        r0, r1 = int(offsets[e]), int(offsets[e + 1])
+        cand = np.unique(np.clip([r0, r0 + 1, r0 + 255, r0 + 256, (r0 + r1) // 2, r1 - 2, r1 - 1], r0, r1 - 1))
+        print(f"  expert {e}: rows {cand.tolist()}: oracle quantisation of its weights", flush=True)
+        xq, xs = check_quant(_Sub(tx, cand), x_perm[cand], f"x rows of expert {e}")
+        wq = [check_quant(_Sub(t, e), w[e], f"{n}[{e}]")
+              for t, w, n in ((tg, li.w_gate, "wg"), (tu, li.w_up, "wu"), (td, li.w_down, "wd"))]
+        (gq, gs), (uq, us), (dq, ds) = wq
+        print(f"  expert {e}: weights bit-exact; oracle FFN rows", flush=True)
+        off1 = np.array([0, len(cand)], np.int32)
+        hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq, xs, gq[None], gs[None], uq[None], us[None],
+                                                             dq[None], ds[None], off1, parts=True)
+        # the GPU's h is not checked here: allow every code the bound permits
+        dev = h_deviation(*allowed_h(h32, P), hq, hs)
+        allow = dev @ np.abs(X.mx_dequantize(dq, ds)).T
+        check_gemm(got[cand], y_ref, mag + allow, f"fullsize y expert {e}", extra=allow)
+
+
+class _Sub:
+    """Rows (or one expert) of a GPU MxTensor, for check_quant."""
+
+    def __init__(self, t, sel):
+        if np.isscalar(sel):
+            self.codes, self.scales = t.codes[sel], t.scales[sel]
+        else:
+            idx = torch.from_numpy(np.asarray(sel, np.int64)).to(DEV)
+            self.codes = t.codes[idx]
+            self.scales = t.scales[:, idx]
