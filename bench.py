@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "MoE layer µs + TFLOP/s / HBM GB/s (% roofline) on one GPU's expert shard vs skew"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
+PEAK_FP8_TFLOPS = 5000.0       # MI355X dense fp8 MFMA
 PEAK_HBM_GBPS = 8000.0         # MI355X HBM3E
 SWEEP_MS = [1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096, 8192]
 MALL_BYTES = 256 << 20
@@ -259,6 +260,16 @@ def main():
                                          zip(SWEEP_MS, med)]}
 
     placement_inputs = None
+    if not args.no_extras and dt == torch.bfloat16:
+        cases = [(T, args.alpha, bufs, stage["grouped_swiglu_ffn"])]
+        for Tb, a in ((min(shape.Ts), 0.0),):
+            if Tb != T:
+                xs, _, bs, _ = make_router(shape, Tb, a, seed=args.seed)
+                bb = make_bufs(Tb, up(xs))
+                bb["bias"] = up(bs, torch.float32)
+                _, st_b = run_timed(up(xs), bb, Tb, max(5, args.steps // 2), 3)
+                cases.append((Tb, a, bb, st_b["grouped_swiglu_ffn"]))
+        result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps)
     if not args.no_extras:
         result["reference_peaks"] = reference_peaks(torch, np, w, T, H, I, dt)
         result["sclk"] = read_sclk()
@@ -270,6 +281,50 @@ def main():
             result["cpu_baseline"]["placement"] = placement_oracle_timing(*placement_inputs)
 
     print(json.dumps(result), flush=True)
+
+
+def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps):
+    """The MXFP8 expert FFN on the routed rows of each case (x_perm, offsets
+    of the bf16 layer): weights quantised once, outside the timing; x_perm
+    quantisation and the FFN timed with HIP events on the current stream."""
+    H, I = shape.H, shape.I
+    tg, tu, td = (moe.moe_mx_quantize(t) for t in (wg, wu, wd))
+    torch.cuda.synchronize()
+    out = []
+    for Tb, a, bb, bf16_us in cases:
+        xp, offs = bb["x_perm"], bb["offsets"]
+        counts = np.diff(offs.cpu().numpy())
+        m = int(counts.sum())
+        active = int((counts > 0).sum())
+        tx = moe.moe_mx_quantize(xp)
+        y, ws = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs)
+        for _ in range(3):
+            moe.moe_mx_quantize(xp, out=tx)
+            moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs, ws=ws, y_perm=y)
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+        for e in ev:
+            e[0].record()
+            moe.moe_mx_quantize(xp, out=tx)
+            e[1].record()
+            moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs, ws=ws, y_perm=y)
+            e[2].record()
+        torch.cuda.synchronize()
+        q_us = float(np.median([e[0].elapsed_time(e[1]) for e in ev])) * 1e3
+        f_us = float(np.median([e[1].elapsed_time(e[2]) for e in ev])) * 1e3
+        flops = 6.0 * m * H * I
+        # weights of active experts (codes + scales), x codes + scales, h out and in, y out (bf16)
+        nbytes = active * 3 * H * I * (1 + 1 / 32) + m * H * (1 + 1 / 32) + 2 * m * I * (1 + 1 / 32) + 2 * m * H
+        tf = flops / (f_us * 1e-6) / 1e12
+        gb = nbytes / (f_us * 1e-6) / 1e9
+        mfma = flops / (PEAK_FP8_TFLOPS * 1e12) >= nbytes / (PEAK_HBM_GBPS * 1e9)
+        out.append({"T": Tb, "alpha": a, "M_loc": m, "active": active, "ffn_us": round(f_us, 2),
+                    "x_quantize_us": round(q_us, 2), "bf16_ffn_us": round(bf16_us, 2),
+                    "speedup_vs_bf16": round(bf16_us / f_us, 3), "tflops": round(tf, 1), "gbps": round(gb, 1),
+                    "bound": "mfma" if mfma else "hbm",
+                    "frac": round(tf / PEAK_FP8_TFLOPS if mfma else gb / PEAK_HBM_GBPS, 4),
+                    "peak": PEAK_FP8_TFLOPS if mfma else PEAK_HBM_GBPS})
+    return {"format": "MXFP8 (E4M3 elements, E8M0 scale per 32 along K), bf16 output", "cases": out}
 
 
 def reference_peaks(torch, np, w, T, H, I, dt):
