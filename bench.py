@@ -46,6 +46,7 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-extras", action="store_true", help="skip the skew table and load sweep")
+    p.add_argument("--mx", action="store_true", help="time the MXFP8 FFN even with --no-extras")
     p.add_argument("--sweep-iters", type=int, default=10)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
     p.add_argument("--calib-copy-mib", type=int, default=0,
@@ -72,7 +73,7 @@ def layer_work(shape, T, counts, local):
 
 def source_sha():
     h = hashlib.sha256()
-    for f in ("ffn_kernels.hip", "common.hpp"):
+    for f in ("ffn_kernels.hip", "common.hpp", "mx.hpp"):
         with open(os.path.join(ROOT, "paper_2606_00735_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -260,16 +261,17 @@ def main():
                                          zip(SWEEP_MS, med)]}
 
     placement_inputs = None
-    if not args.no_extras and dt == torch.bfloat16:
+    if (args.mx or not args.no_extras) and dt == torch.bfloat16:
         cases = [(T, args.alpha, bufs, stage["grouped_swiglu_ffn"])]
-        for Tb, a in ((min(shape.Ts), 0.0),):
+        for Tb, a in (((min(shape.Ts), 0.0),) if not args.no_extras else ()):
             if Tb != T:
                 xs, _, bs, _ = make_router(shape, Tb, a, seed=args.seed)
                 bb = make_bufs(Tb, up(xs))
                 bb["bias"] = up(bs, torch.float32)
                 _, st_b = run_timed(up(xs), bb, Tb, max(5, args.steps // 2), 3)
                 cases.append((Tb, a, bb, st_b["grouped_swiglu_ffn"]))
-        result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps)
+        result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps,
+                                      key=lambda Tb, a: f"{args.config}-T{Tb}-a{a:g}-s{args.seed}-mx")
     if not args.no_extras:
         result["reference_peaks"] = reference_peaks(torch, np, w, T, H, I, dt)
         result["sclk"] = read_sclk()
@@ -283,7 +285,7 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps):
+def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps, key):
     """The MXFP8 expert FFN on the routed rows of each case (x_perm, offsets
     of the bf16 layer): weights quantised once, outside the timing; x_perm
     quantisation and the FFN timed with HIP events on the current stream."""
@@ -323,7 +325,8 @@ def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps):
                     "speedup_vs_bf16": round(bf16_us / f_us, 3), "tflops": round(tf, 1), "gbps": round(gb, 1),
                     "bound": "mfma" if mfma else "hbm",
                     "frac": round(tf / PEAK_FP8_TFLOPS if mfma else gb / PEAK_HBM_GBPS, 4),
-                    "peak": PEAK_FP8_TFLOPS if mfma else PEAK_HBM_GBPS})
+                    "peak": PEAK_FP8_TFLOPS if mfma else PEAK_HBM_GBPS, "algorithmic_bytes": round(nbytes),
+                    "traffic": traffic_from_profile(key(Tb, a))})
     return {"format": "MXFP8 (E4M3 elements, E8M0 scale per 32 along K), bf16 output", "cases": out}
 
 
