@@ -245,7 +245,10 @@ moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint
  * moe_grouped_gemm_mx with W_down (wdq [E_local, H, I], wds
  * [E_local, I/128, H]) into y_perm [M_cap, H] bf16.
  * ws holds h codes [M_cap, I] at offset 0 and their scales [I/128, M_cap]
- * at offset M_cap * I rounded up to 256 bytes.
+ * at offset M_cap * I rounded up to 256 bytes, then the fp32 partial sums
+ * of split-K tiles (used, as in moe_grouped_swiglu_ffn, when every expert has
+ * at most 64 rows or a launch has fewer tiles than CUs; summed in a fixed
+ * order, so results are deterministic).
  */
 moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                                      const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
@@ -277,6 +280,24 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up,
                           const int32_t* Ms, int nM, int warmup, int iters,
                           void* y_scratch, void* ws, size_t* ws_bytes,
                           float* us_out, float* us_all, hipStream_t stream);
+
+/*
+ * moe_load_sweep_mx - moe_load_sweep for the MXFP8 expert FFN (the FP8
+ * kernel the paper's models run, Table 2a): f_g(n) profiled on
+ * moe_grouped_swiglu_ffn_mx with one expert and offsets [0, M].
+ *
+ * xq [maxM, H], xs [H/128, maxM]   MXFP8 input rows (maxM = max of Ms)
+ * wgq, wuq [n_rot, I, H], wgs, wus [n_rot, H/128, I];
+ * wdq [n_rot, H, I], wds [n_rot, I/128, H]   MXFP8 weight copies
+ * y_scratch [maxM, H] bf16; ws, us_out, us_all and limits as moe_load_sweep;
+ * H % 128 == 0, I % 128 == 0.
+ */
+moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
+                             const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
+                             const uint8_t* wdq, const uint32_t* wds, int n_rot, int H, int I,
+                             const int32_t* Ms, int nM, int warmup, int iters, void* y_scratch,
+                             void* ws, size_t* ws_bytes, float* us_out, float* us_all,
+                             hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Placement control path (Section 4.2, Algorithms 1 and 2): the per-GPU

@@ -30,6 +30,7 @@ from ._lib import (  # noqa: F401
     moe_grouped_swiglu_mx,
     moe_layer,
     moe_load_sweep,
+    moe_load_sweep_mx,
     moe_mx_quantize,
     moe_permute,
     moe_place_greedy,

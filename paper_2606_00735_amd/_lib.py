@@ -25,7 +25,7 @@ EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert
             "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep",
             "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_placement_cost",
             "moe_window_push", "moe_drift_distance", "moe_mx_quantize", "moe_grouped_swiglu_mx",
-            "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx")
+            "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx", "moe_load_sweep_mx")
 
 
 class MoeError(RuntimeError):
@@ -85,6 +85,9 @@ def load_library(path: str = LIB_PATH):
     L.moe_grouped_swiglu_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P]
     L.moe_grouped_gemm_mx.restype = _I
     L.moe_grouped_gemm_mx.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P]
+    L.moe_load_sweep_mx.restype = _I
+    L.moe_load_sweep_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P,
+                                    _P]
     L.moe_grouped_swiglu_ffn_mx.restype = _I
     L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _PSZ, _P]
     if L.moe_abi_version() != 1:
@@ -520,3 +523,31 @@ def moe_grouped_swiglu_ffn_mx(x, w_gate, w_up, w_down, offsets, ws=None, y_perm=
                                      ctypes.byref(n), _stream())
     _check("moe_grouped_swiglu_ffn_mx", st)
     return y_perm, ws
+
+
+def moe_load_sweep_mx(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=None, keep_all=False):
+    """Latency vs token load of the MXFP8 FFN on one expert. x: MxTensor [maxM, H];
+    weights: MxTensors [n_rot, I, H] / [n_rot, H, I]. Returns (median_us [nM], all_us or None)."""
+    L = load_library()
+    n_rot, I, H = w_gate.shape
+    Ms = np.ascontiguousarray(np.asarray(Ms, dtype=np.int32))
+    nM = len(Ms)
+    max_m = int(Ms.max())
+    if x.shape != (max_m, H):
+        raise ValueError(f"x must be [{max_m}, {H}] (rows for the largest M)")
+    dev = x.codes.device
+    n = ctypes.c_size_t(0)
+    args = (*_mx_dev(x, "x", (max_m, H)), *_mx_dev(w_gate, "w_gate", (n_rot, I, H)),
+            *_mx_dev(w_up, "w_up", (n_rot, I, H)), *_mx_dev(w_down, "w_down", (n_rot, H, I)), n_rot, H, I,
+            Ms.ctypes.data_as(ctypes.c_void_p), nM, warmup, iters)
+    st = L.moe_load_sweep_mx(*args, None, None, ctypes.byref(n), None, None, _stream())
+    _check("moe_load_sweep_mx", st)
+    ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    y = torch.empty((max_m, H), dtype=torch.bfloat16, device=dev) if y_scratch is None else y_scratch
+    med = np.zeros(nM, np.float32)
+    allv = np.zeros((nM, iters), np.float32) if keep_all else None
+    st = L.moe_load_sweep_mx(*args, _dev(y, "y_scratch", torch.bfloat16), _dev(ws, "ws"), ctypes.byref(n),
+                             med.ctypes.data_as(ctypes.c_void_p),
+                             allv.ctypes.data_as(ctypes.c_void_p) if keep_all else None, _stream())
+    _check("moe_load_sweep_mx", st)
+    return med, allv

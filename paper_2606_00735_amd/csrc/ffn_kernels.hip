@@ -96,6 +96,32 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
   return (g * sig) * u;
 }
 
+// Split-K epilogue shared by the bf16 and MXFP8 tiles: the fp32 sums of
+// output (r, n) of matrix b go to pbase[b * pstride + r * N + n], r the row
+// within the tile; each lane writes its 4 consecutive columns per group as
+// one 16-byte store.
+template <int MI, int NI, int NB, int WM, int WN>
+__device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI], int m0, int m_end, int n0, int N,
+                                               int wm, int wn, int lane, float* pbase, size_t pstride) {
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int r = wm * WM + i * 32 + (lane & 31);  // row within the tile
+    if (m0 + r < m_end) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        float* prow = pbase + b * pstride + (size_t)r * N + n0 + wn * WN + 4 * (lane >> 5);
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<float4*>(prow + j * 32 + 8 * g) =
+                make_float4(acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
+                            acc[b][i][j][4 * g + 3]);
+      }
+    }
+  }
+}
+
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
 // K range: 8 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
 // memory into NS swizzled LDS stages (see pipeline_xk).
@@ -178,23 +204,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   // owns 4 consecutive columns per group g = v / 4 and stores them as one
   // 8-byte write (or, for a split-K partial, one 16-byte fp32 write).
   if (SPLIT) {
-#pragma unroll
-    for (int i = 0; i < MI; ++i) {
-      const int r = wm * WM + i * 32 + (lane & 31);  // row within the tile
-      if (m0 + r < m_end) {
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          float* prow = pbase + b * pstride + (size_t)r * N + n0 + wn * WN + 4 * (lane >> 5);
-#pragma unroll
-          for (int j = 0; j < NI; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-              *reinterpret_cast<float4*>(prow + j * 32 + 8 * g) =
-                  make_float4(acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
-                              acc[b][i][j][4 * g + 3]);
-        }
-      }
-    }
+    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, n0, N, wm, wn, lane, pbase, pstride);
     return;
   }
 #pragma unroll
@@ -253,8 +263,12 @@ __device__ __forceinline__ uint4 lds16(const bf16_t* lds, int row, int chunk) {
 // DUAL: h = SiLU(gate) * up is quantised per 32 columns (the 32 values of a
 // row and block sit in lanes l and l ^ 32) and written as E4M3 codes with their
 // scale dwords; otherwise C is written as bf16.
-template <int BM, int BN, int WAVES_M, bool DUAL>
-__device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0) {
+// SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums go to
+// pbase[b * pstride + r * N + n], as in gemm_tile.
+template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
+__device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
+                                             int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
+                                             size_t pstride = 0) {
   using St = MxStages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -325,8 +339,9 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
 
   // A placeholder load (live == false) re-reads the last chunk, which is in
   // the cache by then, so loads never leave the operands.
+  if (kc1 < 0) kc1 = nK;
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    const int kcl = live ? kc : nK - 1;
+    const int kcl = live ? kc0 + kc : kc1 - 1;
     char* sl = reinterpret_cast<char*>(st);
     const void* pa = uniform_ptr(A + (size_t)kcl * kMxChunk);
 #pragma unroll
@@ -389,7 +404,12 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
     if (NMFMA > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - PAIRS, 0);
     if (NREAD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, NREAD - PAIRS, 0);
   };
-  pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(nK, smem, St::STAGE / 2, issue, read, mma, mix);
+  pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(kc1 - kc0, smem, St::STAGE / 2, issue, read, mma, mix);
+
+  if (SPLIT) {
+    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, n0, N, wm, wn, lane, pbase, pstride);
+    return;
+  }
 
   // Epilogue: output layout as in gemm_tile (lane l: row l % 32, columns
   // 8 g + 4 h + (0..3) of each 32-column block).
@@ -533,7 +553,29 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, bf16_t* smem, int cl
   }
 }
 
-// Body of the grouped GEMM kernels (bf16, or MXFP8 without split-K).
+// One split-K tile (128 columns).
+template <bool DUAL, bool MX>
+__device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
+                                               int n0, int kc0, int kc1, float* pbase, size_t ps) {
+  if constexpr (MX) {
+    if (cls == 0)
+      gemm_tile_mx<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+    else if (cls == 1)
+      gemm_tile_mx<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+    else
+      gemm_tile_mx<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+  } else {
+    if (cls == 0)
+      gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+    else if (cls == 1)
+      gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+    else
+      gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+  }
+}
+
+// Body of the grouped GEMM kernels (bf16 or MXFP8; a K chunk is 64 bf16 or
+// 128 E4M3 elements, 128 bytes of a row either way).
 template <bool DUAL, bool MX>
 __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   constexpr int kSmem = MX ? MxShapes<DUAL>::kSmem : GemmShapes<DUAL>::kSmem;
@@ -568,15 +610,17 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // than 128-column ones but halve the tile count; use them when every CU
   // still gets at least two of them.
   const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 2 * G);
+  constexpr int CK = MX ? kMxChunk : kBK;  // K elements per chunk
+  constexpr int EB = MX ? 1 : 2;           // weight bytes per element (MX scales aside)
   int S = 1;
-  if (!MX && !wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
-    const int nK = a.K / kBK;
+  if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
+    const int nK = a.K / CK;
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
     for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
       // partials must fit, and their fp32 write + read must not outweigh the
       // weights the launch streams (large row tiles are compute bound)
       const long long pfl = (long long)NB * sp * R * a.N;
-      if (pfl > a.part_cap || pfl * 4 > (long long)NB * a.N * a.K * 2 * n_active) break;
+      if (pfl > a.part_cap || pfl * 4 > (long long)NB * a.N * a.K * EB * n_active) break;
       const long long c = (long long)((sp * T0 + G - 1) / G) * ((nK + sp - 1) / sp + kSplitOverhead);
       if (c < best) {
         best = c;
@@ -591,7 +635,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     s_srow0[tid] = ex[1];
   }
   __syncthreads();
-  if (!MX && blockIdx.x == 0) {
+  if (blockIdx.x == 0 && a.plan != nullptr) {
     if (tid == 0) {
       a.plan[0] = S;
       a.plan[1] = R;
@@ -614,27 +658,19 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     const int local = tile - s_start[e];
     const int er = s_rows[e];
     const int n_mt = row_tiles(er);
-    if constexpr (!MX) {
-      if (S > 1) {
-        // split tile: S consecutive tiles share a row tile and a column block
-        const int sp = local % S, rest = local / S;
-        const int nt = rest / n_mt, mt = rest - nt * n_mt;
-        const int nK = a.K / kBK;
-        const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
-        const int m0 = s_row0[e] + mt * 256;
-        const int left = er - mt * 256;
-        const int m_end = m0 + (left < 256 ? left : 256);
-        float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
-        const size_t ps = (size_t)S * R * a.N;
-        const int cls = tile_class(left);
-        if (cls == 0)
-          gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-        else if (cls == 1)
-          gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-        else
-          gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
-        continue;
-      }
+    if (S > 1) {
+      // split tile: S consecutive tiles share a row tile and a column block
+      const int sp = local % S, rest = local / S;
+      const int nt = rest / n_mt, mt = rest - nt * n_mt;
+      const int nK = a.K / CK;
+      const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
+      const int m0 = s_row0[e] + mt * 256;
+      const int left = er - mt * 256;
+      const int m_end = m0 + (left < 256 ? left : 256);
+      float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
+      const size_t ps = (size_t)S * R * a.N;
+      run_split_tile<DUAL, MX>(a, smem, tile_class(left), e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+      continue;
     }
     // row tile fastest: all row tiles of a weight column block run together
     const int nt = local / n_mt, mt = local - nt * n_mt;
@@ -700,6 +736,54 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     packed.x = pack_bf16x2(g.x, g.y);
     packed.y = pack_bf16x2(g.z, g.w);
     *reinterpret_cast<uint2*>(C + (size_t)plan[kPlanHead + j] * N + c) = packed;
+  }
+}
+
+// The MXFP8 gate/up reduction: sums the S partials of gate and up for 32
+// consecutive columns of a row (one thread), applies SiLU(gate) * up as the
+// unsplit epilogue does and quantises the block to E4M3 codes and a scale
+// code (mx.hpp). Does nothing when the GEMM before it split nothing.
+__global__ __launch_bounds__(256) void split_reduce_mx_kernel(const float* __restrict__ part,
+                                                              const int32_t* __restrict__ plan, int N, int M_cap,
+                                                              uint8_t* __restrict__ C8, uint32_t* __restrict__ Cs) {
+  const int S = plan[0];
+  if (S <= 1) return;
+  const int R = plan[1];
+  const int n32 = N / kMxBlock;
+  const size_t items = (size_t)R * n32, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
+  for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (size_t)gridDim.x * 256) {
+    const int j = (int)(it / n32), c = (int)(it % n32) * kMxBlock;
+    const float* p = part + (size_t)j * N + c;
+    float h[kMxBlock];
+    float amax = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kMxBlock / 4; ++q) {
+      float4 g = *reinterpret_cast<const float4*>(p + 4 * q);
+      float4 u = *reinterpret_cast<const float4*>(p + bstride + 4 * q);
+      for (int sp = 1; sp < S; ++sp) {
+        const float4 a = *reinterpret_cast<const float4*>(p + sp * sstride + 4 * q);
+        const float4 b = *reinterpret_cast<const float4*>(p + bstride + sp * sstride + 4 * q);
+        g.x += a.x, g.y += a.y, g.z += a.z, g.w += a.w;
+        u.x += b.x, u.y += b.y, u.z += b.z, u.w += b.w;
+      }
+      h[4 * q] = silu_mul_fast(g.x, u.x);
+      h[4 * q + 1] = silu_mul_fast(g.y, u.y);
+      h[4 * q + 2] = silu_mul_fast(g.z, u.z);
+      h[4 * q + 3] = silu_mul_fast(g.w, u.w);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) amax = fmaxf(amax, fabsf(h[4 * q + t]));
+    }
+    const uint32_t code = mx_scale_code(amax);
+    const float inv = mx_inv_scale(code);
+    const int row = plan[kPlanHead + j];
+    uint32_t w[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) w[q] = e4m3x4(h[4 * q] * inv, h[4 * q + 1] * inv, h[4 * q + 2] * inv, h[4 * q + 3] * inv);
+    uint4* dst = reinterpret_cast<uint4*>(C8 + (size_t)row * N + c);
+    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
+        static_cast<uint8_t>(code);
   }
 }
 
@@ -873,19 +957,59 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
 // ---------------------------------------------------------------------------
 // MXFP8 expert FFN: gate/up (MXFP8 in, MXFP8 h out), then down (bf16 out)
 // ---------------------------------------------------------------------------
-// One 8-wave block per CU, at most the unsplit tile bound, a multiple of 8.
-static unsigned mx_grid(int M_cap, int E_local, int N) {
-  const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128);
+// MXFP8 FFN workspace: h codes [M_cap, I] | h scale dwords [I/128][M_cap] |
+// split-K plan | fp32 partials, sized as for the bf16 FFN.
+struct FfnMxWs {
+  size_t hs, plan, part;  // byte offsets (h codes at 0)
+  long long part_cap;
+  int plan_rows;
+  size_t bytes;
+};
+
+static FfnMxWs ffn_mx_ws_layout(int M_cap, int E_local, int H, int I) {
+  FfnMxWs w{};
+  w.hs = round256((size_t)M_cap * I);
+  w.plan = w.hs + round256((size_t)(I / kMxChunk) * M_cap * 4);
+  const long long need = (long long)kMaxSplit * M_cap * std::max(2LL * I, (long long)H);
+  w.part_cap = std::min(need, kPartCapFloats);
+  w.plan_rows = std::max(M_cap, kSmallM * E_local);
+  w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
+  w.bytes = w.part + round256((size_t)w.part_cap * 4) + 256;
+  return w;
+}
+
+size_t ffn_mx_ws_bytes(int M_cap, int E_local, int H, int I) {
+  return ffn_mx_ws_layout(M_cap, E_local, H, I).bytes;
+}
+
+// One 8-wave block per CU, at most the tile bound (times the largest split
+// when split-K is possible), a multiple of 8.
+static unsigned mx_grid(int M_cap, int E_local, int N, bool split) {
+  const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128) * (split ? kMaxSplit : 1);
   long long g = device_cu_count();
   if (ub < g) g = ub;
   if (g >= 8) g &= ~7LL;
   return (unsigned)(g < 1 ? 1 : g);
 }
 
-hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+static unsigned mx_reduce_grid(int plan_rows, int per_row) {
+  const long long items = (long long)plan_rows * per_row;
+  long long g = (items + 255) / 256;
+  if (g > 4LL * device_cu_count()) g = 4LL * device_cu_count();
+  return (unsigned)(g < 1 ? 1 : g);
+}
+
+// Split-K workspace of one MX GEMM launch (plan == nullptr: no split-K).
+struct MxSplit {
+  float* part;
+  long long part_cap;
+  int32_t* plan;
+  int plan_rows;
+};
+
+static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
-                            int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s) {
-  if (E_local == 0 || M_cap == 0) return hipSuccess;
+                            int I, int M_cap, uint8_t* hq, uint32_t* hs, const MxSplit& sp, hipStream_t s) {
   GemmArgs g{};
   g.A = reinterpret_cast<const bf16_t*>(xq);
   g.B0 = reinterpret_cast<const bf16_t*>(wgq);
@@ -896,17 +1020,26 @@ hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   g.M_cap = M_cap;
   g.N = I;
   g.K = H;
+  g.part = sp.part;
+  g.part_cap = sp.part_cap;
+  g.plan = sp.plan;
+  g.plan_rows = sp.plan_rows;
   g.As = xs;
   g.Bs0 = wgs;
   g.Bs1 = wus;
   g.Cs = hs;
-  grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I), kThreads, 0, s>>>(g);
+  const bool split = sp.plan != nullptr && H / kMxChunk >= 2 * kMinSplitChunks;
+  grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I, split), kThreads, 0, s>>>(g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !split) return e;
+  split_reduce_mx_kernel<<<mx_reduce_grid(sp.plan_rows, I / kMxBlock), 256, 0, s>>>(sp.part, sp.plan, I, M_cap,
+                                                                                     hq, hs);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
-                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s) {
-  if (E_local == 0 || M_cap == 0) return hipSuccess;
+static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
+                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, const MxSplit& sp,
+                          hipStream_t s) {
   GemmArgs g{};
   g.A = reinterpret_cast<const bf16_t*>(aq);
   g.B0 = reinterpret_cast<const bf16_t*>(bq);
@@ -916,15 +1049,32 @@ hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
   g.M_cap = M_cap;
   g.N = N;
   g.K = K;
+  g.part = sp.part;
+  g.part_cap = sp.part_cap;
+  g.plan = sp.plan;
+  g.plan_rows = sp.plan_rows;
   g.As = as;
   g.Bs0 = bs;
-  grouped_gemm_mx_kernel<false><<<mx_grid(M_cap, E_local, N), kThreads, 0, s>>>(g);
+  const bool split = sp.plan != nullptr && K / kMxChunk >= 2 * kMinSplitChunks;
+  grouped_gemm_mx_kernel<false><<<mx_grid(M_cap, E_local, N, split), kThreads, 0, s>>>(g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !split) return e;
+  split_reduce_kernel<false><<<mx_reduce_grid(sp.plan_rows, N / 4), 256, 0, s>>>(sp.part, sp.plan, N,
+                                                                                  static_cast<bf16_t*>(c));
   return hipGetLastError();
 }
 
-// workspace: h codes [M_cap, I] | h scale dwords [I/128][M_cap]
-size_t ffn_mx_ws_bytes(int M_cap, int I) {
-  return round256((size_t)M_cap * I) + round256((size_t)(I / kMxChunk) * M_cap * 4);
+hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                            const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
+                            int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  return gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, MxSplit{}, s);
+}
+
+hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
+                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s) {
+  if (E_local == 0 || M_cap == 0) return hipSuccess;
+  return gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, M_cap, c, MxSplit{}, s);
 }
 
 hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
@@ -932,11 +1082,15 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
                          const int32_t* offsets, int E_local, int H, int I, int M_cap, void* y_perm, void* ws,
                          hipStream_t s) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
-  uint8_t* hq = static_cast<uint8_t*>(ws);
-  uint32_t* hs = reinterpret_cast<uint32_t*>(hq + round256((size_t)M_cap * I));
-  hipError_t e = launch_gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, s);
+  const FfnMxWs L = ffn_mx_ws_layout(M_cap, E_local, H, I);
+  char* w = static_cast<char*>(ws);
+  uint8_t* hq = reinterpret_cast<uint8_t*>(w);
+  uint32_t* hs = reinterpret_cast<uint32_t*>(w + L.hs);
+  const MxSplit sp{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
+                   L.plan_rows};
+  hipError_t e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, sp, s);
   if (e != hipSuccess) return e;
-  return launch_gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, s);
+  return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, sp, s);
 }
 
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {

@@ -35,7 +35,7 @@ hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
                             int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s);
 hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
                           const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s);
-size_t ffn_mx_ws_bytes(int M_cap, int I);
+size_t ffn_mx_ws_bytes(int M_cap, int E_local, int H, int I);
 hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                          const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
                          const int32_t* offsets, int E_local, int H, int I, int M_cap, void* y_perm, void* ws,

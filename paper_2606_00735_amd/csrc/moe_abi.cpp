@@ -66,6 +66,84 @@ moe_status ffn_shape_ok(int E_local, int H, int I, int M_cap, moe_dtype dt) {
   return MOE_OK;
 }
 
+// The timing loop shared by the load sweeps: for each M of Ms, sets
+// offsets = [0, M], then runs `run(rot, M)` warmup + iters times rotating
+// through n_rot weight copies, each timed run bracketed by HIP events.
+template <class Run>
+moe_status sweep_loop(const int32_t* Ms, int nM, int warmup, int iters, int n_rot, int32_t* offsets,
+                      float* us_out, float* us_all, hipStream_t stream, Run&& run) {
+  std::vector<hipEvent_t> ev(2 * (size_t)iters, nullptr);
+  for (auto& e : ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto& d : ev)
+        if (d) (void)hipEventDestroy(d);
+      return MOE_ERR_HIP;
+    }
+  std::vector<float> t(iters);
+  moe_status result = MOE_OK;
+  int rot = 0;
+  for (int mi = 0; mi < nM && result == MOE_OK; ++mi) {
+    const int m = Ms[mi];
+    if (moe::launch_set_offsets(offsets, m, stream) != hipSuccess) {
+      result = MOE_ERR_HIP;
+      break;
+    }
+    for (int it = 0; it < warmup + iters; ++it) {
+      const int r = rot;
+      rot = (rot + 1) % n_rot;
+      const int ti = it - warmup;
+      if (ti >= 0 && hipEventRecord(ev[2 * ti], stream) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      if (run(r, m) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      if (ti >= 0 && hipEventRecord(ev[2 * ti + 1], stream) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+    }
+    if (result != MOE_OK) break;
+    if (hipEventSynchronize(ev[2 * iters - 1]) != hipSuccess) {
+      result = MOE_ERR_HIP;
+      break;
+    }
+    for (int i = 0; i < iters; ++i) {
+      float ms = 0.0f;
+      if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) {
+        result = MOE_ERR_HIP;
+        break;
+      }
+      t[i] = ms * 1000.0f;
+      if (us_all) us_all[(size_t)mi * iters + i] = t[i];
+    }
+    std::vector<float> sorted(t);
+    std::sort(sorted.begin(), sorted.end());
+    us_out[mi] = (iters % 2) ? sorted[iters / 2] : 0.5f * (sorted[iters / 2 - 1] + sorted[iters / 2]);
+  }
+  if (result != MOE_OK) (void)hipStreamSynchronize(stream);
+  for (auto& e : ev) (void)hipEventDestroy(e);
+  return result;
+}
+
+// Shape limits of the MXFP8 GEMMs: every K and N a multiple of the 128-wide
+// scale chunk, row and byte counts within int / size_t range.
+moe_status mx_gemm_shape_ok(int E_local, int N, int K, int M_cap) {
+  if (E_local < 0 || N < 1 || K < 1 || M_cap < 0) return MOE_ERR_INVALID_ARG;
+  if (E_local > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
+  if (N % 128 != 0 || K % 128 != 0) return MOE_ERR_UNSUPPORTED;
+  // tile offsets (256 rows of K bytes) are 32-bit in the kernels
+  if (N > (1 << 20) || K > (1 << 20)) return MOE_ERR_UNSUPPORTED;
+  if ((long long)M_cap * std::max(N, K) > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+bool mx_operand_ok(const void* codes, const void* scales) {
+  return codes && scales && aligned16(codes) && aligned4(scales);
+}
+
 }  // namespace
 
 extern "C" {
@@ -204,62 +282,50 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
   const size_t es = bf16 ? 2 : 4;
   const size_t wmat = (size_t)H * I * es;  // bytes of one expert matrix
   int32_t* offsets = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + ffn_ws);
-  std::vector<hipEvent_t> ev(2 * (size_t)iters, nullptr);
-  for (auto& e : ev)
-    if (hipEventCreate(&e) != hipSuccess) {
-      for (auto& d : ev)
-        if (d) (void)hipEventDestroy(d);
-      return MOE_ERR_HIP;
-    }
-  std::vector<float> t(iters);
-  moe_status result = MOE_OK;
-  int rot = 0;
-  for (int mi = 0; mi < nM && result == MOE_OK; ++mi) {
-    const int m = Ms[mi];
-    if (moe::launch_set_offsets(offsets, m, stream) != hipSuccess) {
-      result = MOE_ERR_HIP;
-      break;
-    }
-    for (int it = 0; it < warmup + iters; ++it) {
-      const char* g = static_cast<const char*>(w_gate) + (size_t)rot * wmat;
-      const char* u = static_cast<const char*>(w_up) + (size_t)rot * wmat;
-      const char* d = static_cast<const char*>(w_down) + (size_t)rot * wmat;
-      rot = (rot + 1) % n_rot;
-      const int ti = it - warmup;
-      if (ti >= 0 && hipEventRecord(ev[2 * ti], stream) != hipSuccess) {
-        result = MOE_ERR_HIP;
-        break;
-      }
-      if (moe::launch_ffn(x, g, u, d, offsets, 1, H, I, m, bf16, y_scratch, ws, stream) != hipSuccess) {
-        result = MOE_ERR_HIP;
-        break;
-      }
-      if (ti >= 0 && hipEventRecord(ev[2 * ti + 1], stream) != hipSuccess) {
-        result = MOE_ERR_HIP;
-        break;
-      }
-    }
-    if (result != MOE_OK) break;
-    if (hipEventSynchronize(ev[2 * iters - 1]) != hipSuccess) {
-      result = MOE_ERR_HIP;
-      break;
-    }
-    for (int i = 0; i < iters; ++i) {
-      float ms = 0.0f;
-      if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) {
-        result = MOE_ERR_HIP;
-        break;
-      }
-      t[i] = ms * 1000.0f;
-      if (us_all) us_all[(size_t)mi * iters + i] = t[i];
-    }
-    std::vector<float> sorted(t);
-    std::sort(sorted.begin(), sorted.end());
-    us_out[mi] = (iters % 2) ? sorted[iters / 2] : 0.5f * (sorted[iters / 2 - 1] + sorted[iters / 2]);
+  return sweep_loop(Ms, nM, warmup, iters, n_rot, offsets, us_out, us_all, stream, [&](int rot, int m) {
+    const char* g = static_cast<const char*>(w_gate) + (size_t)rot * wmat;
+    const char* u = static_cast<const char*>(w_up) + (size_t)rot * wmat;
+    const char* d = static_cast<const char*>(w_down) + (size_t)rot * wmat;
+    return moe::launch_ffn(x, g, u, d, offsets, 1, H, I, m, bf16, y_scratch, ws, stream);
+  });
+}
+
+moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
+                             const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
+                             int n_rot, int H, int I, const int32_t* Ms, int nM, int warmup, int iters,
+                             void* y_scratch, void* ws, size_t* ws_bytes, float* us_out, float* us_all,
+                             hipStream_t stream) {
+  if (Ms == nullptr || nM < 1 || nM > 64 || warmup < 0 || iters < 1 || iters > 10000 || n_rot < 1 ||
+      ws_bytes == nullptr)
+    return MOE_ERR_INVALID_ARG;
+  int max_m = 0;
+  for (int i = 0; i < nM; ++i) {
+    if (Ms[i] < 1 || Ms[i] > (1 << 20)) return MOE_ERR_INVALID_ARG;
+    max_m = std::max(max_m, Ms[i]);
   }
-  if (result != MOE_OK) (void)hipStreamSynchronize(stream);
-  for (auto& e : ev) (void)hipEventDestroy(e);
-  return result;
+  moe_status st = mx_gemm_shape_ok(1, I, H, max_m);
+  if (st != MOE_OK) return st;
+  // x and its scales are laid out for max_m rows, so every run uses
+  // M_cap = max_m with offsets [0, M]
+  const size_t ffn_ws = moe::ffn_mx_ws_bytes(max_m, 1, H, I);
+  const size_t need = ffn_ws + 256;
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) ||
+      !mx_operand_ok(wdq, wds) || !y_scratch || !aligned16(y_scratch) || !aligned16(ws) || !us_out)
+    return MOE_ERR_INVALID_ARG;
+  const size_t wmat = (size_t)H * I;                   // code bytes of one expert matrix
+  const size_t smat = (size_t)(H / 128) * I;           // scale dwords of W_gate / W_up
+  const size_t sdown = (size_t)(I / 128) * H;          // scale dwords of W_down
+  int32_t* offsets = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + ffn_ws);
+  return sweep_loop(Ms, nM, warmup, iters, n_rot, offsets, us_out, us_all, stream, [&](int rot, int m) {
+    return moe::launch_ffn_mx(xq, xs, wgq + rot * wmat, wgs + rot * smat, wuq + rot * wmat, wus + rot * smat,
+                              wdq + rot * wmat, wds + rot * sdown, offsets, 1, H, I, max_m, y_scratch, ws,
+                              stream);
+  });
 }
 
 }  // extern "C"
@@ -267,26 +333,6 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
 // ---------------------------------------------------------------------------
 // MXFP8 expert FFN
 // ---------------------------------------------------------------------------
-namespace {
-
-// Shape limits of the MXFP8 GEMMs: every K and N a multiple of the 128-wide
-// scale chunk, row and byte counts within int / size_t range.
-moe_status mx_gemm_shape_ok(int E_local, int N, int K, int M_cap) {
-  if (E_local < 0 || N < 1 || K < 1 || M_cap < 0) return MOE_ERR_INVALID_ARG;
-  if (E_local > MOE_MAX_EXPERTS) return MOE_ERR_UNSUPPORTED;
-  if (N % 128 != 0 || K % 128 != 0) return MOE_ERR_UNSUPPORTED;
-  // tile offsets (256 rows of K bytes) are 32-bit in the kernels
-  if (N > (1 << 20) || K > (1 << 20)) return MOE_ERR_UNSUPPORTED;
-  if ((long long)M_cap * std::max(N, K) > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
-  return MOE_OK;
-}
-
-bool mx_operand_ok(const void* codes, const void* scales) {
-  return codes && scales && aligned16(codes) && aligned4(scales);
-}
-
-}  // namespace
-
 extern "C" {
 
 moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, uint8_t* codes,
@@ -329,7 +375,7 @@ moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, cons
   moe_status st = mx_gemm_shape_ok(E_local, I, H, M_cap);
   if (st != MOE_OK) return st;
   if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
-  const size_t need = moe::ffn_mx_ws_bytes(M_cap, I);
+  const size_t need = moe::ffn_mx_ws_bytes(M_cap, E_local, H, I);
   if (ws == nullptr) {
     *ws_bytes = need;
     return MOE_OK;

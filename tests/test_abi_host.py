@@ -254,3 +254,22 @@ def test_mx_validation_and_query(L):
                                    None) == INVALID
     assert L.moe_grouped_swiglu_mx(None, None, None, None, None, None, None, 0, 128, 384, 64, None, None,
                                    None) == 0
+
+
+def test_mx_sweep_validation(L):
+    Ms = np.array([1, 8], np.int32)
+    pM = Ms.ctypes.data_as(ctypes.c_void_p)
+    n = ctypes.c_size_t(0)
+    args = [FAKE] * 8
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+                               None) == 0
+    assert n.value >= 8 * 14336
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14300, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+                               None) == UNSUPPORTED
+    assert L.moe_load_sweep_mx(*args, 0, 4096, 14336, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+                               None) == INVALID
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 0, None, None, ctypes.byref(n), None, None,
+                               None) == INVALID
+    n = ctypes.c_size_t(16)
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 3, FAKE, FAKE, ctypes.byref(n), FAKE, None,
+                               None) == WORKSPACE

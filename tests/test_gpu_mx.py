@@ -266,11 +266,10 @@ FFN_CASES = [
 ]
 
 
-@pytest.mark.parametrize("H,I,rows", FFN_CASES, ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}"
-                                                   for h, i, r in FFN_CASES])
-def test_ffn_mx(H, I, rows):
-    banner("mx ffn", H, I, rows, "seed 9")
-    xp, wg, wu, wd, offsets, m = _inputs(H, I, rows, seed=9)
+def _ffn_case(H, I, rows, seed):
+    """The MXFP8 FFN on one case under the rules of the module docstring.
+    Returns the FFN's workspace."""
+    xp, wg, wu, wd, offsets, m = _inputs(H, I, rows, seed=seed)
     tx = moe.moe_mx_quantize(up(xp))
     tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (wg, wu, wd))
     xq, xs = check_quant(tx, xp, "x")
@@ -278,15 +277,14 @@ def test_ffn_mx(H, I, rows):
                                                                          (td, wd, "wd")))
     doff = torch.from_numpy(offsets).to(DEV)
     y, ws = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, doff)
-    h = moe.moe_grouped_swiglu_mx(tx, tg, tu, doff)
     torch.cuda.synchronize()
-    hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq[:m], xs[:m], gq, gs, uq, us, dq, ds, offsets, parts=True)
-    ghq = h.codes.cpu().numpy()[:m]
-    ghs = gpu_scales(h.scales, xp.shape[0], I)[:m]
-    # the FFN's workspace holds the same h as the gate/up entry point
     M_cap = xp.shape[0]
     wsn = ws.cpu().numpy()
-    assert np.array_equal(wsn[:M_cap * I].reshape(M_cap, I)[:m], ghq)
+    hs_off = ((M_cap * I + 255) // 256) * 256
+    ghq = wsn[:M_cap * I].reshape(M_cap, I)[:m]
+    ghs_dw = torch.from_numpy(wsn[hs_off:hs_off + (I // 128) * M_cap * 4].view(np.int32).reshape(I // 128, M_cap))
+    ghs = gpu_scales(ghs_dw, M_cap, I)[:m]
+    hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq[:m], xs[:m], gq, gs, uq, us, dq, ds, offsets, parts=True)
     dev = check_h(ghq, ghs, hq, hs, h32, P, f"h H={H} I={I}")
     got = y.float().cpu().numpy()[:m]
     # y: GEMM rule on the oracle's h, plus the effect of every allowed h code difference
@@ -298,6 +296,66 @@ def test_ffn_mx(H, I, rows):
             allow[r0:r1] = dev[r0:r1] @ Wd.T
     # the GPU's down GEMM sums |h_gpu| |W_down| <= mag + allow
     check_gemm(got, y_ref, mag + allow, f"ffn y H={H} I={I}", extra=allow)
+    # the gate/up entry point alone writes the same h
+    h = moe.moe_grouped_swiglu_mx(tx, tg, tu, doff)
+    torch.cuda.synchronize()
+    same = np.array_equal(h.codes.cpu().numpy()[:m], ghq)
+    return ws, M_cap, same
+
+
+@pytest.mark.parametrize("H,I,rows", FFN_CASES, ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}"
+                                                   for h, i, r in FFN_CASES])
+def test_ffn_mx(H, I, rows):
+    banner("mx ffn", H, I, rows, "seed 9")
+    _, _, same = _ffn_case(H, I, rows, seed=9)
+    assert same, "moe_grouped_swiglu_mx and the FFN's h differ"
+
+
+MX_SPLIT_CASES = [
+    # (H, I, rows per expert, S of the down GEMM), worked out by hand from the
+    # split rule on 256 CUs (K chunks of 128): one 64-row Mixtral-shaped expert
+    # (gate/up S = 2, down S = 8); one 256-row DSV3-shaped expert (gate/up S = 7,
+    # down S = 2: partial bytes equal to the weight bytes are still allowed);
+    # Qwen3-shaped, 5 rows (gate/up S = 2; the down GEMM's 6 chunks cannot
+    # split); Maverick-shaped experts of 400, 100 and 32 rows (down S = 3)
+    (4096, 14336, [64], 8),
+    (7168, 2048, [256], 2),
+    (2048, 768, [5], 1),
+    (5120, 8192, [400, 100, 32], 3),
+]
+
+
+@pytest.mark.parametrize("H,I,rows,S_down", MX_SPLIT_CASES,
+                         ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}" for h, i, r, _ in MX_SPLIT_CASES])
+def test_ffn_mx_split_k(H, I, rows, S_down):
+    banner("mx ffn split-K", H, I, rows, "seed 5")
+    ws, M_cap, _ = _ffn_case(H, I, rows, seed=5)
+    hs_off = ((M_cap * I + 255) // 256) * 256
+    plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
+    assert int(ws[plan_off:plan_off + 4].view(torch.int32).item()) == S_down
+
+
+def test_load_sweep_mx_output_and_timing():
+    """The MXFP8 sweep's last run leaves y for the largest M (rows checked
+    under the FFN rule) and every median is positive."""
+    banner("mx sweep qwen3-shaped expert")
+    H, I = 2048, 768
+    _, wg, wu, wd, _, _ = _inputs(H, I, [1], seed=12)
+    x, *_ = make_router(_shape(H, I, 1), 300, 0.0, seed=12)
+    Ms = [1, 7, 33, 128, 300]
+    rot = 3
+    tx = moe.moe_mx_quantize(up(x))
+    tg, tu, td = (moe.moe_mx_quantize(up(np.repeat(w, rot, 0))) for w in (wg, wu, wd))
+    y = torch.full((300, H), float("nan"), dtype=torch.bfloat16, device=DEV)
+    us, allus = moe.moe_load_sweep_mx(tx, tg, tu, td, Ms, warmup=2, iters=5, y_scratch=y, keep_all=True)
+    print("  sweep us", us.tolist(), flush=True)
+    assert np.all(us > 0) and allus.shape == (5, 5)
+    xq, xs = check_quant(tx, x, "x")
+    (gq, gs), (uq, us_), (dq, ds) = (oracle_quant(w) for w in (wg, wu, wd))
+    hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq, xs, gq, gs, uq, us_, dq, ds, [0, 300], parts=True)
+    dev = h_deviation(*allowed_h(h32, P), hq, hs)
+    allow = dev @ np.abs(X.mx_dequantize(dq[0], ds[0])).T
+    check_gemm(y.float().cpu().numpy(), y_ref, mag + allow, "sweep y", extra=allow)
 
 
 def test_ffn_mx_rows_of_empty_experts_untouched():
