@@ -259,6 +259,22 @@ def main():
                                            zip(SWEEP_MS, med)],
                                 "gbps": [round((e_bytes + 2.0 * m * H * 2) / (u * 1e-6) / 1e9, 1) for m, u in
                                          zip(SWEEP_MS, med)]}
+        if dt == torch.bfloat16:
+            # the same expert in MXFP8 (weights 1 byte + a scale byte per 32)
+            mx_bytes = 3 * H * I * (1 + 1 / 32)
+            n_rot_mx = max(1, -(-2 * MALL_BYTES // int(mx_bytes)))
+            rep_mx = lambda a: moe.moe_mx_quantize(up(a).repeat(n_rot_mx, 1, 1).contiguous())
+            tg, tu, td = rep_mx(g1), rep_mx(u1), rep_mx(d1)
+            med_mx, _ = moe.moe_load_sweep_mx(moe.moe_mx_quantize(xs), tg, tu, td, SWEEP_MS, warmup=3,
+                                              iters=args.sweep_iters)
+            med_mx = [float(v) for v in med_mx]
+            del tg, tu, td
+            result["load_sweep_mx"] = {
+                "M": SWEEP_MS, "us": [round(float(v), 2) for v in med_mx], "n_rot": n_rot_mx,
+                "tflops": [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, u in zip(SWEEP_MS, med_mx)],
+                "gbps": [round((mx_bytes + m * H * (1 + 1 / 32) + 2.0 * m * H) / (u * 1e-6) / 1e9, 1)
+                         for m, u in zip(SWEEP_MS, med_mx)],
+                "speedup_vs_bf16": [round(b / m, 2) for b, m in zip(med, med_mx)]}
 
     placement_inputs = None
     if (args.mx or not args.no_extras) and dt == torch.bfloat16:

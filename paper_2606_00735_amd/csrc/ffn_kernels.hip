@@ -739,51 +739,46 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   }
 }
 
-// The MXFP8 gate/up reduction: sums the S partials of gate and up for 32
-// consecutive columns of a row (one thread), applies SiLU(gate) * up as the
-// unsplit epilogue does and quantises the block to E4M3 codes and a scale
-// code (mx.hpp). Does nothing when the GEMM before it split nothing.
+// The MXFP8 gate/up reduction: sums the S partials of gate and up for 4
+// consecutive columns of a row per thread (16-byte loads, consecutive lanes on
+// consecutive columns), applies SiLU(gate) * up as the unsplit epilogue does,
+// and quantises each 32-column block (the 8 lanes of an aligned lane group:
+// block max by three shuffles, the group's first lane writes the scale code).
+// N % 32 == 0 keeps every group inside one block and the item count a
+// multiple of 8, so a group is wholly in range or wholly out. Does nothing
+// when the GEMM before it split nothing.
 __global__ __launch_bounds__(256) void split_reduce_mx_kernel(const float* __restrict__ part,
                                                               const int32_t* __restrict__ plan, int N, int M_cap,
                                                               uint8_t* __restrict__ C8, uint32_t* __restrict__ Cs) {
   const int S = plan[0];
   if (S <= 1) return;
   const int R = plan[1];
-  const int n32 = N / kMxBlock;
-  const size_t items = (size_t)R * n32, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
+  const int n4 = N / 4;
+  const size_t items = (size_t)R * n4, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
   for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (size_t)gridDim.x * 256) {
-    const int j = (int)(it / n32), c = (int)(it % n32) * kMxBlock;
+    const int j = (int)(it / n4), c = (int)(it % n4) * 4;
     const float* p = part + (size_t)j * N + c;
-    float h[kMxBlock];
-    float amax = 0.0f;
-#pragma unroll
-    for (int q = 0; q < kMxBlock / 4; ++q) {
-      float4 g = *reinterpret_cast<const float4*>(p + 4 * q);
-      float4 u = *reinterpret_cast<const float4*>(p + bstride + 4 * q);
-      for (int sp = 1; sp < S; ++sp) {
-        const float4 a = *reinterpret_cast<const float4*>(p + sp * sstride + 4 * q);
-        const float4 b = *reinterpret_cast<const float4*>(p + bstride + sp * sstride + 4 * q);
-        g.x += a.x, g.y += a.y, g.z += a.z, g.w += a.w;
-        u.x += b.x, u.y += b.y, u.z += b.z, u.w += b.w;
-      }
-      h[4 * q] = silu_mul_fast(g.x, u.x);
-      h[4 * q + 1] = silu_mul_fast(g.y, u.y);
-      h[4 * q + 2] = silu_mul_fast(g.z, u.z);
-      h[4 * q + 3] = silu_mul_fast(g.w, u.w);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) amax = fmaxf(amax, fabsf(h[4 * q + t]));
+    float4 g = *reinterpret_cast<const float4*>(p);
+    float4 u = *reinterpret_cast<const float4*>(p + bstride);
+    for (int sp = 1; sp < S; ++sp) {
+      const float4 a = *reinterpret_cast<const float4*>(p + sp * sstride);
+      const float4 b = *reinterpret_cast<const float4*>(p + bstride + sp * sstride);
+      g.x += a.x, g.y += a.y, g.z += a.z, g.w += a.w;
+      u.x += b.x, u.y += b.y, u.z += b.z, u.w += b.w;
     }
+    const float h0 = silu_mul_fast(g.x, u.x), h1 = silu_mul_fast(g.y, u.y);
+    const float h2 = silu_mul_fast(g.z, u.z), h3 = silu_mul_fast(g.w, u.w);
+    float amax = fmaxf(fmaxf(fabsf(h0), fabsf(h1)), fmaxf(fabsf(h2), fabsf(h3)));
+    amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
+    amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
+    amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
     const uint32_t code = mx_scale_code(amax);
     const float inv = mx_inv_scale(code);
     const int row = plan[kPlanHead + j];
-    uint32_t w[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) w[q] = e4m3x4(h[4 * q] * inv, h[4 * q + 1] * inv, h[4 * q + 2] * inv, h[4 * q + 3] * inv);
-    uint4* dst = reinterpret_cast<uint4*>(C8 + (size_t)row * N + c);
-    dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
-    dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
-    reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
-        static_cast<uint8_t>(code);
+    *reinterpret_cast<uint32_t*>(C8 + (size_t)row * N + c) = e4m3x4(h0 * inv, h1 * inv, h2 * inv, h3 * inv);
+    if ((c & (kMxBlock - 1)) == 0)
+      reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
+          static_cast<uint8_t>(code);
   }
 }
 
@@ -1032,7 +1027,7 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I, split), kThreads, 0, s>>>(g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
-  split_reduce_mx_kernel<<<mx_reduce_grid(sp.plan_rows, I / kMxBlock), 256, 0, s>>>(sp.part, sp.plan, I, M_cap,
+  split_reduce_mx_kernel<<<mx_reduce_grid(sp.plan_rows, I / 4), 256, 0, s>>>(sp.part, sp.plan, I, M_cap,
                                                                                      hq, hs);
   return hipGetLastError();
 }
