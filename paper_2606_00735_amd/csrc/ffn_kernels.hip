@@ -97,19 +97,19 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 }
 
 // Split-K epilogue shared by the bf16 and MXFP8 tiles: the fp32 sums of
-// output (r, n) of matrix b go to pbase[b * pstride + r * N + n], r the row
-// within the tile; each lane writes its 4 consecutive columns per group as
-// one 16-byte store.
+// output (r, c) of matrix b (r, c within the tile) go to
+// pbase[b * pstride + r * ld + col0 + c]; each lane writes its 4 consecutive
+// columns per group as one 16-byte store.
 template <int MI, int NI, int NB, int WM, int WN>
-__device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI], int m0, int m_end, int n0, int N,
-                                               int wm, int wn, int lane, float* pbase, size_t pstride) {
+__device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI], int m0, int m_end, int col0,
+                                               int ld, int wm, int wn, int lane, float* pbase, size_t pstride) {
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int r = wm * WM + i * 32 + (lane & 31);  // row within the tile
     if (m0 + r < m_end) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        float* prow = pbase + b * pstride + (size_t)r * N + n0 + wn * WN + 4 * (lane >> 5);
+        float* prow = pbase + b * pstride + (size_t)r * ld + col0 + wn * WN + 4 * (lane >> 5);
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
@@ -125,12 +125,13 @@ __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI]
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
 // K range: 8 waves, 32x32x16 bf16 MFMA, operands loaded straight from global
 // memory into NS swizzled LDS stages (see pipeline_xk).
-// SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums go to
-// pbase[b * pstride + r * N + n] (r: row within the tile) instead of C.
+// SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums of output
+// (r, c) (r: row within the tile, c: column within the tile) go to
+// pbase[b * pstride + r * pld + pcol0 + c] instead of C.
 template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                           int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
-                                          size_t pstride = 0) {
+                                          size_t pstride = 0, int pld = 0, int pcol0 = 0) {
   using St = Stages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -204,7 +205,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   // owns 4 consecutive columns per group g = v / 4 and stores them as one
   // 8-byte write (or, for a split-K partial, one 16-byte fp32 write).
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, n0, N, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
     return;
   }
 #pragma unroll
@@ -263,12 +264,12 @@ __device__ __forceinline__ uint4 lds16(const bf16_t* lds, int row, int chunk) {
 // DUAL: h = SiLU(gate) * up is quantised per 32 columns (the 32 values of a
 // row and block sit in lanes l and l ^ 32) and written as E4M3 codes with their
 // scale dwords; otherwise C is written as bf16.
-// SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums go to
-// pbase[b * pstride + r * N + n], as in gemm_tile.
+// SPLIT: only K chunks [kc0, kc1) are summed, the fp32 sums written as in
+// gemm_tile.
 template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
 __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                              int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
-                                             size_t pstride = 0) {
+                                             size_t pstride = 0, int pld = 0, int pcol0 = 0) {
   using St = MxStages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -407,7 +408,7 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
   pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(kc1 - kc0, smem, St::STAGE / 2, issue, read, mma, mix);
 
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, n0, N, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
     return;
   }
 
@@ -553,25 +554,56 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, bf16_t* smem, int cl
   }
 }
 
-// One split-K tile (128 columns).
-template <bool DUAL, bool MX>
+// One split-K tile of BN columns (128, or 256 for a wide single GEMM): K
+// chunks [kc0, kc1), fp32 sums to pbase (row stride pld, column base pcol0).
+template <bool DUAL, bool MX, int BN>
 __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
-                                               int n0, int kc0, int kc1, float* pbase, size_t ps) {
+                                               int n0, int kc0, int kc1, float* pbase, size_t ps, int pld,
+                                               int pcol0) {
   if constexpr (MX) {
     if (cls == 0)
-      gemm_tile_mx<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile_mx<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else if (cls == 1)
-      gemm_tile_mx<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile_mx<128, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else
-      gemm_tile_mx<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile_mx<256, BN, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
   } else {
     if (cls == 0)
-      gemm_tile<64, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else if (cls == 1)
-      gemm_tile<128, 128, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile<128, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else
-      gemm_tile<256, 128, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps);
+      gemm_tile<256, BN, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
   }
+}
+
+// Tile `tile` of the unsplit schedule (tiles of `cols` columns): its expert,
+// rows [m0, m_end) and first column.
+struct TileRef {
+  int e, m0, m_end, n0, left;
+};
+
+__device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_start, const int* s_row0,
+                                               const int* s_rows, int cols) {
+  // last expert whose first tile is <= tile (experts with no tiles share
+  // their start with the next one, so the last match is the owner)
+  int lo = 0, hi = E - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (s_start[mid] <= tile) lo = mid; else hi = mid - 1;
+  }
+  TileRef t;
+  t.e = lo;
+  const int local = tile - s_start[lo];
+  const int er = s_rows[lo];
+  const int n_mt = row_tiles(er);
+  // row tile fastest: all row tiles of a weight column block run together
+  const int nt = local / n_mt, mt = local - nt * n_mt;
+  t.m0 = s_row0[lo] + mt * 256;
+  t.left = er - mt * 256;  // rows from m0 to the expert's end, >= 1
+  t.m_end = t.m0 + (t.left < 256 ? t.left : 256);
+  t.n0 = nt * cols;
+  return t;
 }
 
 // Body of the grouped GEMM kernels (bf16 or MXFP8; a K chunk is 64 bf16 or
@@ -612,9 +644,9 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   const bool wide = !DUAL && (a.N % 256 == 0) && (T0 / 2 >= 2 * G);
   constexpr int CK = MX ? kMxChunk : kBK;  // K elements per chunk
   constexpr int EB = MX ? 1 : 2;           // weight bytes per element (MX scales aside)
+  const int nK = a.K / CK;
   int S = 1;
   if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
-    const int nK = a.K / CK;
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
     for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
       // partials must fit, and their fp32 write + read must not outweigh the
@@ -630,6 +662,26 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   }
   const int mul = wide ? 1 : S, div = wide ? 2 : 1;  // tile count per 128-column tile
   const int total = T0 * mul / div;
+  const int cols = wide ? 256 : 128;
+  // Tail split. An unsplit launch runs its tiles in rounds of G; when the
+  // last round is at most half full, its `rem` tiles are each cut into St K
+  // ranges (St <= G / rem) spread over the idle CUs, their fp32 sums kept
+  // per tile ([tile][b][split][256][cols]) and finished by the reduction
+  // launch, which finds each tile's rows and columns in the plan.
+  int St = 1, rem = 0;
+  if (S == 1 && a.part != nullptr && total > 0) {
+    const int r = total % G;
+    int st = r > 0 ? G / r : 1;
+    if (st > kMaxSplit) st = kMaxSplit;
+    const long long per = (long long)NB * 256 * cols;  // floats of one split tile
+    while (st > 1 && (st * kMinSplitChunks > nK || (long long)st * r * per > a.part_cap)) --st;
+    if (st > 1 && 3 * r <= a.plan_rows) {
+      St = st;
+      rem = r;
+    }
+  }
+  const int full = total - rem;
+  const int n_items = full + rem * St;
   if (tid < E) {
     s_start[tid] = ex[0] * mul / div;
     s_srow0[tid] = ex[1];
@@ -639,49 +691,70 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     if (tid == 0) {
       a.plan[0] = S;
       a.plan[1] = R;
+      a.plan[2] = St;
+      a.plan[3] = rem;
+      a.plan[4] = cols;
     }
     if (S > 1 && tid < E)
       for (int r = 0; r < s_rows[tid]; ++r) a.plan[kPlanHead + s_srow0[tid] + r] = s_row0[tid] + r;
+    if (St > 1 && tid < rem) {
+      const TileRef t = decode_tile(full + tid, E, s_start, s_row0, s_rows, cols);
+      a.plan[kPlanHead + 3 * tid] = t.m0;
+      a.plan[kPlanHead + 3 * tid + 1] = t.m_end;
+      a.plan[kPlanHead + 3 * tid + 2] = t.n0;
+    }
   }
 
   const int per_xcd = G >> 3;
   const int slot = (G & 7) ? (int)blockIdx.x : ((int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3));
-  for (int tile = slot; tile < total; tile += G) {
-    // last expert whose first tile is <= tile (experts with no tiles share
-    // their start with the next one, so the last match is the owner)
-    int lo = 0, hi = E - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (s_start[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    const int e = lo;
-    const int local = tile - s_start[e];
-    const int er = s_rows[e];
-    const int n_mt = row_tiles(er);
+  for (int item = slot; item < n_items; item += G) {
     if (S > 1) {
       // split tile: S consecutive tiles share a row tile and a column block
+      int lo = 0, hi = E - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_start[mid] <= item) lo = mid; else hi = mid - 1;
+      }
+      const int e = lo;
+      const int local = item - s_start[e];
+      const int er = s_rows[e];
+      const int n_mt = row_tiles(er);
       const int sp = local % S, rest = local / S;
       const int nt = rest / n_mt, mt = rest - nt * n_mt;
-      const int nK = a.K / CK;
       const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
       const int m0 = s_row0[e] + mt * 256;
       const int left = er - mt * 256;
       const int m_end = m0 + (left < 256 ? left : 256);
       float* pbase = a.part + ((size_t)sp * R + s_srow0[e] + mt * 256) * a.N;
       const size_t ps = (size_t)S * R * a.N;
-      run_split_tile<DUAL, MX>(a, smem, tile_class(left), e, m0, m_end, nt * 128, kc0, kc1, pbase, ps);
+      run_split_tile<DUAL, MX, 128>(a, smem, tile_class(left), e, m0, m_end, nt * 128, kc0, kc1, pbase, ps, a.N,
+                                    nt * 128);
       continue;
     }
-    // row tile fastest: all row tiles of a weight column block run together
-    const int nt = local / n_mt, mt = local - nt * n_mt;
-    const int m0 = s_row0[e] + mt * 256;
-    const int left = er - mt * 256;  // rows from m0 to the expert's end, >= 1
-    const int cls = tile_class(left);
-    const int m_end = m0 + (left < 256 ? left : 256);
+    if (item >= full) {
+      // a split of a tail tile
+      const int u = item - full, pr = u / St, sp = u - pr * St;
+      const TileRef t = decode_tile(full + pr, E, s_start, s_row0, s_rows, cols);
+      const int kc0 = sp * nK / St, kc1 = (sp + 1) * nK / St;
+      const size_t tsz = (size_t)256 * cols;
+      float* pbase = a.part + ((size_t)pr * NB * St + sp) * tsz;
+      if constexpr (!DUAL) {
+        if (wide) {
+          run_split_tile<DUAL, MX, 256>(a, smem, tile_class(t.left), t.e, t.m0, t.m_end, t.n0, kc0, kc1, pbase,
+                                        St * tsz, cols, 0);
+          continue;
+        }
+      }
+      run_split_tile<DUAL, MX, 128>(a, smem, tile_class(t.left), t.e, t.m0, t.m_end, t.n0, kc0, kc1, pbase,
+                                    St * tsz, cols, 0);
+      continue;
+    }
+    const TileRef t = decode_tile(item, E, s_start, s_row0, s_rows, cols);
+    const int cls = tile_class(t.left);
     if (!DUAL && wide)
-      run_tile<DUAL, MX, !DUAL>(a, smem, cls, e, m0, m_end, nt * 256);
+      run_tile<DUAL, MX, !DUAL>(a, smem, cls, t.e, t.m0, t.m_end, t.n0);
     else
-      run_tile<DUAL, MX, false>(a, smem, cls, e, m0, m_end, nt * 128);
+      run_tile<DUAL, MX, false>(a, smem, cls, t.e, t.m0, t.m_end, t.n0);
   }
 }
 
@@ -697,15 +770,67 @@ __global__ __launch_bounds__(kThreads) void grouped_gemm_mx_kernel(GemmArgs a) {
   grouped_gemm_body<DUAL, true>(a);
 }
 
+// Tail tiles of an unsplit launch (see grouped_gemm_body): item `it` of the
+// reduction is (tail tile pr, row rr, 4 columns at c); the tile's rows and
+// first column come from the plan. Returns false for rows past the tile's end.
+struct TailItem {
+  const float* p;  // partials of split 0 of matrix 0
+  size_t tsz;      // floats between splits
+  int row, col;    // output row and column
+};
+
+__device__ __forceinline__ bool tail_item(const float* part, const int32_t* plan, int NB, size_t it,
+                                          TailItem& t) {
+  const int St = plan[2], cols = plan[4];
+  const int c4n = cols / 4;
+  const int pr = (int)(it / ((size_t)256 * c4n));
+  const int rr = (int)((it / c4n) % 256), c = (int)(it % c4n) * 4;
+  const int m0 = plan[kPlanHead + 3 * pr], m_end = plan[kPlanHead + 3 * pr + 1];
+  t.tsz = (size_t)256 * cols;
+  t.p = part + (size_t)pr * NB * St * t.tsz + (size_t)rr * cols + c;
+  t.row = m0 + rr;
+  t.col = plan[kPlanHead + 3 * pr + 2] + c;
+  return t.row < m_end;
+}
+
+__device__ __forceinline__ float4 sum_splits(const float* p, size_t stride, int n) {
+  float4 g = *reinterpret_cast<const float4*>(p);
+  for (int sp = 1; sp < n; ++sp) {
+    const float4 q = *reinterpret_cast<const float4*>(p + sp * stride);
+    g.x += q.x, g.y += q.y, g.z += q.z, g.w += q.w;
+  }
+  return g;
+}
+
 // Sums the S split-K partials of every row of a split launch in split order,
 // applies the epilogue (SiLU(gate) * up for the dual GEMM) and writes bf16
-// rows of C. Does nothing when the GEMM before it split nothing.
+// rows of C; or, after an unsplit launch with a tail split, the same for the
+// tail tiles. Does nothing when the GEMM before it split nothing.
 template <bool DUAL>
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part,
                                                            const int32_t* __restrict__ plan, int N,
                                                            bf16_t* __restrict__ C) {
   const int S = plan[0];
-  if (S <= 1) return;
+  if (S <= 1) {
+    const int St = plan[2];
+    if (St <= 1) return;
+    const size_t items = (size_t)plan[3] * 256 * (plan[4] / 4);
+    for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (size_t)gridDim.x * 256) {
+      TailItem t;
+      if (!tail_item(part, plan, DUAL ? 2 : 1, it, t)) continue;
+      float4 g = sum_splits(t.p, t.tsz, St);
+      if (DUAL) {
+        const float4 u = sum_splits(t.p + St * t.tsz, t.tsz, St);
+        g = make_float4(silu_mul_fast(g.x, u.x), silu_mul_fast(g.y, u.y), silu_mul_fast(g.z, u.z),
+                        silu_mul_fast(g.w, u.w));
+      }
+      uint2 packed;
+      packed.x = pack_bf16x2(g.x, g.y);
+      packed.y = pack_bf16x2(g.z, g.w);
+      *reinterpret_cast<uint2*>(C + (size_t)t.row * N + t.col) = packed;
+    }
+    return;
+  }
   const int R = plan[1];
   const int n4 = N / 4;
   const size_t items = (size_t)R * n4, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
@@ -739,6 +864,23 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   }
 }
 
+// Four h values of columns [c, c + 4) of `row`, quantised with the other 28
+// of their 32-column block, which the 7 other lanes of this lane's aligned
+// group of 8 hold; the group's first lane writes the scale code.
+__device__ __forceinline__ void mx_quant_store4(float h0, float h1, float h2, float h3, int row, int c, int N,
+                                                int M_cap, uint8_t* C8, uint32_t* Cs) {
+  float amax = fmaxf(fmaxf(fabsf(h0), fabsf(h1)), fmaxf(fabsf(h2), fabsf(h3)));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
+  const uint32_t code = mx_scale_code(amax);
+  const float inv = mx_inv_scale(code);
+  *reinterpret_cast<uint32_t*>(C8 + (size_t)row * N + c) = e4m3x4(h0 * inv, h1 * inv, h2 * inv, h3 * inv);
+  if ((c & (kMxBlock - 1)) == 0)
+    reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
+        static_cast<uint8_t>(code);
+}
+
 // The MXFP8 gate/up reduction: sums the S partials of gate and up for 4
 // consecutive columns of a row per thread (16-byte loads, consecutive lanes on
 // consecutive columns), applies SiLU(gate) * up as the unsplit epilogue does,
@@ -751,7 +893,21 @@ __global__ __launch_bounds__(256) void split_reduce_mx_kernel(const float* __res
                                                               const int32_t* __restrict__ plan, int N, int M_cap,
                                                               uint8_t* __restrict__ C8, uint32_t* __restrict__ Cs) {
   const int S = plan[0];
-  if (S <= 1) return;
+  if (S <= 1) {
+    // tail tiles of an unsplit launch; a tile's column count is a multiple
+    // of 32, so the 8 lanes of a block share the tile and the row
+    const int St = plan[2];
+    if (St <= 1) return;
+    const size_t items = (size_t)plan[3] * 256 * (plan[4] / 4);
+    for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (size_t)gridDim.x * 256) {
+      TailItem t;
+      if (!tail_item(part, plan, 2, it, t)) continue;
+      const float4 g = sum_splits(t.p, t.tsz, St), u = sum_splits(t.p + St * t.tsz, t.tsz, St);
+      mx_quant_store4(silu_mul_fast(g.x, u.x), silu_mul_fast(g.y, u.y), silu_mul_fast(g.z, u.z),
+                      silu_mul_fast(g.w, u.w), t.row, t.col, N, M_cap, C8, Cs);
+    }
+    return;
+  }
   const int R = plan[1];
   const int n4 = N / 4;
   const size_t items = (size_t)R * n4, sstride = (size_t)R * N, bstride = (size_t)S * R * N;
@@ -766,19 +922,8 @@ __global__ __launch_bounds__(256) void split_reduce_mx_kernel(const float* __res
       g.x += a.x, g.y += a.y, g.z += a.z, g.w += a.w;
       u.x += b.x, u.y += b.y, u.z += b.z, u.w += b.w;
     }
-    const float h0 = silu_mul_fast(g.x, u.x), h1 = silu_mul_fast(g.y, u.y);
-    const float h2 = silu_mul_fast(g.z, u.z), h3 = silu_mul_fast(g.w, u.w);
-    float amax = fmaxf(fmaxf(fabsf(h0), fabsf(h1)), fmaxf(fabsf(h2), fabsf(h3)));
-    amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
-    amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
-    amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
-    const uint32_t code = mx_scale_code(amax);
-    const float inv = mx_inv_scale(code);
-    const int row = plan[kPlanHead + j];
-    *reinterpret_cast<uint32_t*>(C8 + (size_t)row * N + c) = e4m3x4(h0 * inv, h1 * inv, h2 * inv, h3 * inv);
-    if ((c & (kMxBlock - 1)) == 0)
-      reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
-          static_cast<uint8_t>(code);
+    mx_quant_store4(silu_mul_fast(g.x, u.x), silu_mul_fast(g.y, u.y), silu_mul_fast(g.z, u.z),
+                    silu_mul_fast(g.w, u.w), plan[kPlanHead + j], c, N, M_cap, C8, Cs);
   }
 }
 
@@ -919,14 +1064,10 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   };
   float* part = reinterpret_cast<float*>(wsb + L.part);
   int32_t* plan = reinterpret_cast<int32_t*>(wsb + L.plan);
-  // reduce grid: one float4 column group per thread over at most
-  // min(M_cap, 64 E_local) rows, grid-stride beyond 4 blocks per CU
-  auto reduce_grid = [&](int N) {
-    const long long items = (long long)L.plan_rows * (N / 4);
-    long long g = (items + 255) / 256;
-    if (g > 4LL * cus) g = 4LL * cus;
-    return (unsigned)(g < 1 ? 1 : g);
-  };
+  // reduce grid: one float4 column group per thread, grid-stride over 4
+  // blocks per CU (a split launch has up to max(M_cap, 64 E_local) rows of
+  // N columns to finish, a tail split up to G / 2 tiles of 256 x 256)
+  auto reduce_grid = [&](int) { return (unsigned)(4 * cus); };
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
               part, L.part_cap, plan, L.plan_rows};
@@ -987,12 +1128,8 @@ static unsigned mx_grid(int M_cap, int E_local, int N, bool split) {
   return (unsigned)(g < 1 ? 1 : g);
 }
 
-static unsigned mx_reduce_grid(int plan_rows, int per_row) {
-  const long long items = (long long)plan_rows * per_row;
-  long long g = (items + 255) / 256;
-  if (g > 4LL * device_cu_count()) g = 4LL * device_cu_count();
-  return (unsigned)(g < 1 ? 1 : g);
-}
+// as reduce_grid in launch_ffn
+static unsigned mx_reduce_grid(int, int) { return (unsigned)(4 * device_cu_count()); }
 
 // Split-K workspace of one MX GEMM launch (plan == nullptr: no split-K).
 struct MxSplit {

@@ -335,6 +335,25 @@ def test_ffn_mx_split_k(H, I, rows, S_down):
     assert int(ws[plan_off:plan_off + 4].view(torch.int32).item()) == S_down
 
 
+MX_TAIL_CASES = [
+    # (H, I, rows of one expert, (S, St, rem, cols) of the down GEMM) from the
+    # tail rule on 256 CUs with K chunks of 128: St is held to 2 by K = 16 chunks
+    (2048, 2048, [4608], (1, 2, 32, 128)),
+    (4096, 2048, [8448], (1, 2, 16, 256)),
+]
+
+
+@pytest.mark.parametrize("H,I,rows,plan", MX_TAIL_CASES,
+                         ids=[f"H{h}-I{i}-rows{r[0]}" for h, i, r, _ in MX_TAIL_CASES])
+def test_ffn_mx_tail_split(H, I, rows, plan):
+    banner("mx ffn tail split", H, I, rows, "seed 4")
+    ws, M_cap, _ = _ffn_case(H, I, rows, seed=4)
+    hs_off = ((M_cap * I + 255) // 256) * 256
+    plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
+    got = ws[plan_off:plan_off + 20].view(torch.int32).cpu().numpy()
+    assert (got[0], got[2], got[3], got[4]) == plan, got[:5]
+
+
 def test_load_sweep_mx_output_and_timing():
     """The MXFP8 sweep's last run leaves y for the largest M (rows checked
     under the FFN rule) and every median is positive."""

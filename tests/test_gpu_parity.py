@@ -235,6 +235,42 @@ def test_ffn_split_k(H, I, rows, S_down):
     assert torch.equal(y2[:m], y[:m])
 
 
+TAIL_CASES = [
+    # (H, I, rows of one expert, (S, St, rem, cols) of the down GEMM) worked out
+    # by hand from the tail rule on 256 CUs: an unsplit launch whose last round
+    # holds rem <= 128 tiles cuts each into St = min(8, 256 // rem) K ranges,
+    # fewer if a range would hold under 8 chunks or the partials would not fit
+    (2048, 2048, [4608], (1, 4, 32, 128)),   # 288 tiles of 128 columns: 32 left over, K = 32 chunks
+    (4096, 2048, [8448], (1, 4, 16, 256)),   # 528 tiles of 256 columns: 16 left over
+]
+
+
+@pytest.mark.parametrize("H,I,rows,plan", TAIL_CASES,
+                         ids=[f"H{h}-I{i}-rows{r[0]}" for h, i, r, _ in TAIL_CASES])
+def test_ffn_tail_split(H, I, rows, plan):
+    """The last, partly filled round of an unsplit launch split along K over
+    the idle CUs; the gate/up GEMM of these shapes takes the same path."""
+    banner("stage ffn tail split", H, I, rows, "seed 6")
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="tail", H=H, I=I, E=1, k=1, E_local=1)
+    wg, wu, wd = make_experts(shape, [0], seed=6)
+    m = sum(rows)
+    x, *_ = make_router(shape, m, 0.0, seed=6)
+    offsets = np.array([0, m], np.int32)
+    M_cap = m + 3
+    xp = np.zeros((M_cap, H), np.float32)
+    xp[:m] = x
+    h_ref, y_ref = O.grouped_swiglu_ffn(x, wg, wu, wd, offsets, bf16=True)
+    y, ws = moe.moe_grouped_swiglu_ffn(G.up(xp, torch.bfloat16), G.up(wg, torch.bfloat16),
+                                       G.up(wu, torch.bfloat16), G.up(wd, torch.bfloat16), G.up_i32(offsets))
+    torch.cuda.synchronize()
+    off = ((M_cap * I * 2 + 255) // 256) * 256
+    got = ws[off:off + 20].view(torch.int32).cpu().numpy()
+    assert (got[0], got[2], got[3], got[4]) == plan, got[:5]
+    h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
+    G.check_bf16(h, h_ref, "tail h")
+    G.check_bf16(G.down(y)[:m], y_ref, "tail y", scale=G.down_scale(h_ref, wd, offsets))
+
+
 def test_combine_stage_on_oracle_inputs():
     banner("stage combine qwen3")
     li = make_layer("qwen3", 64, 1.0, seed=4)
