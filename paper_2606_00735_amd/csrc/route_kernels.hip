@@ -278,6 +278,113 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_ksplit_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Router, bf16, for E > 32 when blocks of 128 tokens would leave CUs idle:
+// 8 waves per block of BT = 64 tokens, the FFN GEMM's pipeline
+// (pipeline_xk: operands read one k-step ahead across chunks, NS stages of x
+// rows and router weights in swizzled LDS). Waves tile the BT x E_pad
+// logits as (BT / 32) x (256 / BT) (32 tokens by a share of the experts
+// each). The logits then go through LDS (fp32, BT x E_pad), and each wave
+// selects the top k of BT / 8 tokens with all 64 lanes. Every block loads
+// all E_pad router rows, and the load path, not the MFMAs, bounds both
+// router kernels, so the launcher takes the block size for which one CU
+// loads fewer rows: rounds of blocks x (E_pad + tokens per block).
+// ---------------------------------------------------------------------------
+template <int BT, int NCB>  // E_pad = 32 * NCB, NCB = 4 or 8
+__global__ __launch_bounds__(512) void gate_topk_bf16_wide_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
+    int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
+    float* __restrict__ wts) {
+  static_assert(NCB == 4 || NCB == 8, "E_pad of 128 or 256");
+  static_assert(BT == 64 || BT == 128, "tokens per block");
+  constexpr int WAVES_M = BT / 32, WAVES_N = 8 / WAVES_M;
+  constexpr int EP = NCB * 32, NI = NCB / WAVES_N;
+  constexpr int ROWS = BT + EP;
+  constexpr int STAGE = ROWS * kGateBK;                          // bf16 slots
+  constexpr int NS = (144 * 1024) / (STAGE * 2) > 8 ? 8 : (144 * 1024) / (STAGE * 2);
+  static_assert(NS >= 2, "stages");
+  constexpr int LOADS = ROWS / 64;                               // 1 KB loads per wave per chunk
+  constexpr int SMEM = (NS * STAGE * 2 > BT * EP * 4) ? NS * STAGE * 2 : BT * EP * 4;
+  __shared__ __align__(16) unsigned char smem_raw[SMEM];
+  bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
+  float* tile = reinterpret_cast<float*>(smem_raw);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int r = lane & 31, half = lane >> 5;
+  const int row0 = blockIdx.x * BT;
+  const bf16_t* xa = x + (size_t)row0 * H;
+  const int a_rows = T - row0;
+  const int nK = H / kGateBK;
+
+  f32x16_t acc[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) acc[j] = f32x16_t{};
+
+  auto issue = [&](int kc, bool live, bf16_t* st) {
+    dma_rows<BT, 8, kGateBK>(xa, H, kc * kGateBK, a_rows, live, st, wave, lane);
+    dma_rows<EP, 8, kGateBK>(wr, H, kc * kGateBK, E, live, st + BT * kGateBK, wave, lane);
+  };
+  bf16x8_t af[2], bfr[2][NI];
+  auto read = [&](const bf16_t* st, int s, int buf) {
+    const int chunk = 2 * s + half;
+    af[buf] = lds_frag<kGateBK>(st, wm * 32 + r, chunk);
+#pragma unroll
+    for (int j = 0; j < NI; ++j) bfr[buf][j] = lds_frag<kGateBK>(st + BT * kGateBK, (wn * NI + j) * 32 + r, chunk);
+  };
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < NI; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[buf], bfr[buf][j], acc[j], 0, 0, 0);
+  };
+  auto mix = [&]() {
+#pragma unroll
+    for (int q = 0; q < NI; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  };
+  pipeline_xk<NS, LOADS, kGateBK / 16>(nK, smem, STAGE, issue, read, mma, mix);
+
+  // logits + bias into the LDS tile (the stages are free): register v of lane
+  // (r, half) holds token row 8 (v / 4) + 4 half + (v % 4), expert column r of
+  // its 32-column block
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int col = (wn * NI + j) * 32 + r;
+    const float b = (bias != nullptr && col < E) ? bias[col] : 0.0f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = wm * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+      tile[row * EP + col] = (col < E) ? acc[j][v] + b : -__builtin_huge_valf();
+    }
+  }
+  __syncthreads();
+
+  // wave w selects for tokens w BT / 8 .. (w + 1) BT / 8 - 1; lane g holds
+  // columns q * 64 + g
+  constexpr int NV = EP / 64;
+  for (int t = 0; t < BT / 8; ++t) {
+    const int lr = wave * (BT / 8) + t;
+    const int row = row0 + lr;
+    if (row >= T) break;  // wave-uniform
+    float val[NV];
+#pragma unroll
+    for (int q = 0; q < NV; ++q) val[q] = tile[lr * EP + q * 64 + lane];
+    if (logits != nullptr) {
+#pragma unroll
+      for (int q = 0; q < NV; ++q) {
+        const int col = q * 64 + lane;
+        if (col < E) logits[(size_t)row * E + col] = val[q];
+      }
+    }
+    float sel_v[kMaxTopk];
+    int sel_i[kMaxTopk];
+    topk_group<64, NV>(val, lane, E, k, sel_v, sel_i);
+    write_topk(sel_v, sel_i, lane, k, row, ids, wts);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Router, fp32: one wave per token, lanes over experts, VALU dot products in
 // ascending h.
 // ---------------------------------------------------------------------------
@@ -566,6 +673,28 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
     }
 #undef MOE_GATE_KSPLIT
     return hipGetLastError();
+  }
+  // More than 32 experts: 8-wave blocks of 64 tokens (E_pad of 128 or 256)
+  // when they have each CU load fewer rows than 128-token blocks.
+  if (ncb > 1) {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      int n = 0;
+      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) cus = n;
+    }
+    const int ep = ncb <= 4 ? 128 : 256;
+    auto rows_per_cu = [&](int bt) {
+      const long long blocks = (T + bt - 1) / bt;
+      return ((blocks + cus - 1) / cus) * (long long)(ep + bt);
+    };
+    if (rows_per_cu(64) < rows_per_cu(128)) {
+      const dim3 g((T + 63) / 64);
+      if (ncb <= 4)
+        gate_topk_bf16_wide_kernel<64, 4><<<g, 512, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts);
+      else
+        gate_topk_bf16_wide_kernel<64, 8><<<g, 512, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts);
+      return hipGetLastError();
+    }
   }
   const dim3 grid((T + 127) / 128);
 #define MOE_GATE_CASE(N)                                                                        \

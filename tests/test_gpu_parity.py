@@ -156,6 +156,44 @@ def test_mixed_small_and_large_experts():
     G.compare_layer(li, run_gpu(li), r, "mixed")
 
 
+ROUTER_WIDE = [
+    # (H, E, k, T): which router runs follows the launcher's rule on 256 CUs
+    (512, 256, 8, 4100),      # 8-wave router, 64-token blocks, E_pad 256, ragged last block
+    (1024, 200, 16, 5000),    # 8-wave router, E = 200 of 256, k at its limit
+    (256, 256, 8, 20000),     # 4-wave router, 128-token blocks, E_pad 256
+    (256, 100, 6, 33000),     # 4-wave router, E_pad 128
+    (256, 40, 4, 33000),      # 4-wave router, E = 40 of 64
+    (2048, 128, 8, 4096),     # K-split router
+]
+
+
+@pytest.mark.parametrize("H,E,k,T", ROUTER_WIDE, ids=[f"H{h}-E{e}-k{k}-T{t}" for h, e, k, t in ROUTER_WIDE])
+def test_router_many_tokens(H, E, k, T):
+    """Logits and ids bit-exact, weights to 1e-6, on the many-token router."""
+    banner("router", H, E, k, T, "seed 3")
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="router", H=H, E=E, k=k, E_local=E)
+    x, w, b, _ = make_router(shape, T, 1.0, seed=3)
+    ids, wts, lg = moe.moe_gate_topk(G.up(x, torch.bfloat16), G.up(w, torch.bfloat16), G.up(b, torch.float32), k,
+                                     logits=True)
+    torch.cuda.synchronize()
+    z = O.router_logits(x, w, b)
+    assert np.array_equal(G.down(lg), z), "logits"
+    rid = O.topk_select(z, k)
+    assert np.array_equal(G.down(ids), rid), "ids"
+    np.testing.assert_allclose(G.down(wts), O.topk_weights(z, rid), rtol=1e-6, atol=0)
+
+
+def test_router_many_tokens_ties():
+    """All logits equal: every token takes experts 0..k-1 in order."""
+    banner("router ties E=256 T=4096")
+    shape = dataclasses.replace(CONFIGS["dsv3_shard"], name="router", H=256, E=256, k=8, E_local=256)
+    x, w, b, _ = make_router(shape, 4096, 0.0, seed=1)
+    ids, wts, _ = moe.moe_gate_topk(G.up(x, torch.bfloat16), torch.zeros((256, 256), dtype=torch.bfloat16,
+                                    device="cuda"), torch.zeros(256, dtype=torch.float32, device="cuda"), 8)
+    torch.cuda.synchronize()
+    assert np.all(G.down(ids) == np.arange(8)) and np.allclose(G.down(wts), 1.0 / 8, rtol=1e-6)
+
+
 def test_empty_batch():
     banner("edge T=0")
     d = G.upload_layer(make_layer("tiny", 1, 1.0))
