@@ -226,6 +226,19 @@ def main():
         "gen_s": round(t_gen, 1),
     }
 
+    # MXFP8 FFN on this batch's routed rows (before the skew table, which
+    # reuses these buffers for its other token counts and skews)
+    if (args.mx or not args.no_extras) and dt == torch.bfloat16:
+        cases = [(T, args.alpha, bufs, stage["grouped_swiglu_ffn"])]
+        for Tb, a in (((min(shape.Ts), 0.0),) if not args.no_extras else ()):
+            if Tb != T:
+                xs, _, bs, _ = make_router(shape, Tb, a, seed=args.seed)
+                bb = make_bufs(Tb, up(xs))
+                bb["bias"] = up(bs, torch.float32)
+                _, st_b = run_timed(up(xs), bb, Tb, max(5, args.steps // 2), 3)
+                cases.append((Tb, a, bb, st_b["grouped_swiglu_ffn"]))
+        result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps,
+                                      key=lambda Tb, a: f"{args.config}-T{Tb}-a{a:g}-s{args.seed}-mx")
     if not args.no_extras:
         # skew table: same weights, other token counts and skews of this config
         table = []
@@ -277,17 +290,6 @@ def main():
                 "speedup_vs_bf16": [round(b / m, 2) for b, m in zip(med, med_mx)]}
 
     placement_inputs = None
-    if (args.mx or not args.no_extras) and dt == torch.bfloat16:
-        cases = [(T, args.alpha, bufs, stage["grouped_swiglu_ffn"])]
-        for Tb, a in (((min(shape.Ts), 0.0),) if not args.no_extras else ()):
-            if Tb != T:
-                xs, _, bs, _ = make_router(shape, Tb, a, seed=args.seed)
-                bb = make_bufs(Tb, up(xs))
-                bb["bias"] = up(bs, torch.float32)
-                _, st_b = run_timed(up(xs), bb, Tb, max(5, args.steps // 2), 3)
-                cases.append((Tb, a, bb, st_b["grouped_swiglu_ffn"]))
-        result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps,
-                                      key=lambda Tb, a: f"{args.config}-T{Tb}-a{a:g}-s{args.seed}-mx")
     if not args.no_extras:
         result["reference_peaks"] = reference_peaks(torch, np, w, T, H, I, dt)
         result["sclk"] = read_sclk()
@@ -314,16 +316,17 @@ def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps, key):
         counts = np.diff(offs.cpu().numpy())
         m = int(counts.sum())
         active = int((counts > 0).sum())
-        tx = moe.moe_mx_quantize(xp)
+        n_rows = offs[-1:]  # routed rows only, as the layer would
+        tx = moe.moe_mx_quantize(xp, row_count=n_rows)
         y, ws = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs)
         for _ in range(3):
-            moe.moe_mx_quantize(xp, out=tx)
+            moe.moe_mx_quantize(xp, out=tx, row_count=n_rows)
             moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs, ws=ws, y_perm=y)
         torch.cuda.synchronize()
         ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
         for e in ev:
             e[0].record()
-            moe.moe_mx_quantize(xp, out=tx)
+            moe.moe_mx_quantize(xp, out=tx, row_count=n_rows)
             e[1].record()
             moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, offs, ws=ws, y_perm=y)
             e[2].record()

@@ -201,13 +201,18 @@ moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const 
 /*
  * moe_mx_quantize - MXFP8 quantisation of `batch` matrices of `rows` x K.
  *
- * x      [batch, rows, K] dt (bf16 or fp32)
- * codes  [batch, rows, K] uint8, all written
- * scales [batch, K/128, rows] uint32, all written
+ * x         [batch, rows, K] dt (bf16 or fp32)
+ * row_count DEVICE int32 or NULL (batch 1 only): quantise rows
+ *           [0, min(rows, *row_count)) only, e.g. the routed rows of x_perm
+ *           with row_count = offsets + E_local, without a host sync; the
+ *           other rows' codes and scales are left untouched
+ * codes     [batch, rows, K] uint8
+ * scales    [batch, K/128, rows] uint32
  * Limits: K % 128 == 0; batch * rows * K <= 2^40.
  */
-moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, uint8_t* codes,
-                           uint32_t* scales, hipStream_t stream);
+moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K,
+                           const int32_t* row_count, uint8_t* codes, uint32_t* scales,
+                           hipStream_t stream);
 
 /*
  * moe_grouped_swiglu_mx - the gate/up half of the MXFP8 expert FFN.

@@ -80,7 +80,7 @@ def load_library(path: str = LIB_PATH):
     L.moe_drift_distance.restype = _I
     L.moe_drift_distance.argtypes = [_P, _P, _I, _I, _D, _P, _P, _P]
     L.moe_mx_quantize.restype = _I
-    L.moe_mx_quantize.argtypes = [_P, _I, _I, _I, _I, _P, _P, _P]
+    L.moe_mx_quantize.argtypes = [_P, _I, _I, _I, _I, _P, _P, _P, _P]
     L.moe_grouped_swiglu_mx.restype = _I
     L.moe_grouped_swiglu_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P]
     L.moe_grouped_gemm_mx.restype = _I
@@ -436,15 +436,22 @@ class MxTensor:
         return tuple(self.codes.shape)
 
 
-def moe_mx_quantize(x, out=None):
-    """MXFP8 quantisation of x [R, K] or [B, R, K] (bf16 or fp32) along K."""
+def moe_mx_quantize(x, out=None, row_count=None):
+    """MXFP8 quantisation of x [R, K] or [B, R, K] (bf16 or fp32) along K.
+    row_count: optional device int32 tensor of one element (R-row x only):
+    rows from it on are left as they are in `out`."""
     L = load_library()
     xb = x.unsqueeze(0) if x.dim() == 2 else x
     B, R, K = xb.shape
     if out is None:
         out = MxTensor(torch.empty(x.shape, dtype=torch.uint8, device=x.device),
                        torch.empty(tuple(x.shape[:-2]) + (K // 128, R), dtype=torch.int32, device=x.device))
-    st = L.moe_mx_quantize(_dev(x, "x"), _dtype_code(x), B, R, K, _dev(out.codes, "codes", torch.uint8),
+    rc = ctypes.c_void_p(None)
+    if row_count is not None:
+        if row_count.numel() != 1 or row_count.dtype != torch.int32 or not row_count.is_cuda:
+            raise ValueError("row_count must be one device int32")
+        rc = ctypes.c_void_p(row_count.data_ptr())
+    st = L.moe_mx_quantize(_dev(x, "x"), _dtype_code(x), B, R, K, rc, _dev(out.codes, "codes", torch.uint8),
                            _dev(out.scales, "scales", torch.int32), _stream())
     _check("moe_mx_quantize", st)
     return out

@@ -28,8 +28,8 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       void* ws, hipStream_t s);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
-hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, uint8_t* codes,
-                              uint32_t* scales, hipStream_t s);
+hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, const int32_t* row_count,
+                              uint8_t* codes, uint32_t* scales, hipStream_t s);
 hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
                             int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s);

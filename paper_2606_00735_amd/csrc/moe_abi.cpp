@@ -335,14 +335,15 @@ moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_
 // ---------------------------------------------------------------------------
 extern "C" {
 
-moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, uint8_t* codes,
-                           uint32_t* scales, hipStream_t stream) {
+moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, const int32_t* row_count,
+                           uint8_t* codes, uint32_t* scales, hipStream_t stream) {
   if (!valid_dtype(dt) || batch < 0 || rows < 0 || K < 1) return MOE_ERR_INVALID_ARG;
   if (K % 128 != 0) return MOE_ERR_UNSUPPORTED;
   if ((long long)batch * rows * K > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
+  if (row_count != nullptr && (batch > 1 || !aligned4(row_count))) return MOE_ERR_INVALID_ARG;
   if (batch == 0 || rows == 0) return MOE_OK;
   if (!x || !aligned16(x) || !mx_operand_ok(codes, scales)) return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_mx_quantize(x, dt == MOE_F32, batch, rows, K, codes, scales, stream));
+  return hip_status(moe::launch_mx_quantize(x, dt == MOE_F32, batch, rows, K, row_count, codes, scales, stream));
 }
 
 moe_status moe_grouped_swiglu_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,

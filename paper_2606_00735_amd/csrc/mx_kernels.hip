@@ -12,12 +12,16 @@ namespace moe {
 // largest magnitude with two shuffles; the first of them writes the scale
 // code. K % 128 == 0 keeps every group inside one row, and the element count
 // is a multiple of 32, so a group is either wholly in range or wholly out.
+// row_count (device, optional, batch 1 only): only rows [0, min(rows,
+// *row_count)) are quantised; the others are left as they are.
 template <bool F32IN>
 __global__ __launch_bounds__(256) void mx_quantize_kernel(const void* __restrict__ x, int batch, int rows, int K,
+                                                          const int32_t* __restrict__ row_count,
                                                           uint8_t* __restrict__ codes,
                                                           uint32_t* __restrict__ scales) {
   const int n8k = K / 8;
-  const size_t n8 = (size_t)batch * rows * n8k;
+  const int live = row_count != nullptr ? min(max(*row_count, 0), rows) : rows;
+  const size_t n8 = (size_t)batch * live * n8k;
   for (size_t t = (size_t)blockIdx.x * 256 + threadIdx.x; t < n8; t += (size_t)gridDim.x * 256) {
     float v[8];
     if (F32IN) {
@@ -55,8 +59,8 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const void* __restrict
   }
 }
 
-hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, uint8_t* codes,
-                              uint32_t* scales, hipStream_t s) {
+hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, const int32_t* row_count,
+                              uint8_t* codes, uint32_t* scales, hipStream_t s) {
   const size_t n8 = (size_t)batch * rows * (K / 8);
   if (n8 == 0) return hipSuccess;
   int dev = 0, cus = 256;
@@ -67,9 +71,9 @@ hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int 
   size_t grid = (n8 + 255) / 256;
   if (grid > (size_t)cus * 16) grid = (size_t)cus * 16;
   if (f32)
-    mx_quantize_kernel<true><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, codes, scales);
+    mx_quantize_kernel<true><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, row_count, codes, scales);
   else
-    mx_quantize_kernel<false><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, codes, scales);
+    mx_quantize_kernel<false><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, row_count, codes, scales);
   return hipGetLastError();
 }
 

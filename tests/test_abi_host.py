@@ -241,11 +241,12 @@ def test_mx_validation_and_query(L):
     assert L.moe_grouped_swiglu_ffn_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 64,
                                        FAKE, FAKE, ctypes.byref(n), None) == WORKSPACE
     # quantiser: K % 128, dtype, null and misaligned pointers
-    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 200, FAKE, FAKE, None) == UNSUPPORTED
-    assert L.moe_mx_quantize(FAKE, 7, 1, 4, 256, FAKE, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 256, None, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(MISALIGNED, 1, 1, 4, 256, FAKE, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(None, 1, 0, 4, 256, None, None, None) == 0     # empty: no-op
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 200, None, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.moe_mx_quantize(FAKE, 7, 1, 4, 256, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 256, None, None, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(MISALIGNED, 1, 1, 4, 256, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(FAKE, 1, 2, 4, 256, FAKE, FAKE, FAKE, None) == INVALID   # row count: batch 1 only
+    assert L.moe_mx_quantize(None, 1, 0, 4, 256, None, None, None, None) == 0     # empty: no-op
     # GEMMs
     assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 100, 256, 64, FAKE, None) == UNSUPPORTED
     assert L.moe_grouped_gemm_mx(FAKE, FAKE, None, FAKE, FAKE, 2, 128, 256, 64, FAKE, None) == INVALID

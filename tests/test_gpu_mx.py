@@ -203,6 +203,21 @@ def test_quantize_batched_weights_layout():
     check_quant(t, a, "batched")
 
 
+def test_quantize_device_row_count():
+    """With a device row count only the first rows are quantised; the rest of
+    the output keeps what it held."""
+    banner("mx quantize with a device row count")
+    a = (torch.from_numpy(np.random.default_rng(3).standard_normal((300, 256)).astype(np.float32))
+         .bfloat16().float().numpy())
+    out = moe.MxTensor(torch.full((300, 256), 0x5A, dtype=torch.uint8, device=DEV),
+                       torch.full((2, 300), 0x11111111, dtype=torch.int32, device=DEV))
+    n = torch.tensor([171], dtype=torch.int32, device=DEV)
+    moe.moe_mx_quantize(up(a), out=out, row_count=n)
+    torch.cuda.synchronize()
+    check_quant(_Sub(out, np.arange(171)), a[:171], "first rows")
+    assert torch.all(out.codes[171:] == 0x5A) and torch.all(out.scales[:, 171:] == 0x11111111)
+
+
 # ---------------------------------------------------------------- GEMMs
 def _shape(H, I, n):
     return dataclasses.replace(CONFIGS["qwen3"], name="mx", H=H, I=I, E=n, k=1, E_local=n)
@@ -390,12 +405,16 @@ def test_ffn_mx_rows_of_empty_experts_untouched():
 
 
 # ---------------------------------------------------------------- full size
-def test_ffn_mx_fullsize_mixtral_t4096():
-    """Mixtral-shaped layer at T = 4096, skew 1.0 (8 experts, 8192 routed rows):
-    routing from the oracle, the FFN in the bench's launch configuration,
-    sampled rows of the hottest and the coldest expert checked."""
-    banner("mx ffn fullsize mixtral T=4096 a=1.0 seed 0")
-    li = make_layer("mixtral", 4096, 1.0, seed=0)
+MX_FULL = [("mixtral", 4096, 1.0), ("qwen3", 8192, 1.0), ("dsv3_shard", 16384, 0.0), ("maverick_shard", 32768, 0.0)]
+
+
+@pytest.mark.parametrize("name,T,alpha", MX_FULL, ids=[f"{n}-T{t}-a{a}" for n, t, a in MX_FULL])
+def test_ffn_mx_fullsize(name, T, alpha):
+    """Every bf16 workload at full size: routing from the oracle, the MXFP8
+    FFN in the bench's launch configuration (x_perm of M_cap = T k rows),
+    sampled rows of the hottest and the coldest local expert checked."""
+    banner("mx ffn fullsize", name, T, alpha, "seed 0")
+    li = make_layer(name, T, alpha, seed=0)
     H, I = li.shape.H, li.shape.I
     z = O.router_logits(li.x, li.w_router, li.bias)
     ids = O.topk_select(z, li.shape.k)
@@ -403,7 +422,10 @@ def test_ffn_mx_fullsize_mixtral_t4096():
     offsets = O.local_offsets(counts, li.expert_map)
     x_perm, _, _ = O.permute(li.x, ids, li.expert_map, offsets)
     m = int(offsets[-1])
-    tx = moe.moe_mx_quantize(up(x_perm))
+    M_cap = T * li.shape.k
+    xp_full = np.zeros((M_cap, H), np.float32)
+    xp_full[:m] = x_perm
+    tx = moe.moe_mx_quantize(up(xp_full))
     tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (li.w_gate, li.w_up, li.w_down))
     y, _ = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, torch.from_numpy(offsets.astype(np.int32)).to(DEV))
     torch.cuda.synchronize()
