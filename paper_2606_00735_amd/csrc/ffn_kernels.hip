@@ -71,6 +71,9 @@ struct GemmArgs {
   const uint32_t* Bs0;
   const uint32_t* Bs1;
   uint32_t* Cs;
+  // Per-XCD work counters (8 ints, zero before the launch) or nullptr for
+  // the static tile order.
+  int32_t* queue;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -705,9 +708,8 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     }
   }
 
-  const int per_xcd = G >> 3;
-  const int slot = (G & 7) ? (int)blockIdx.x : ((int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3));
-  for (int item = slot; item < n_items; item += G) {
+  // One item: a split-K tile, a split of a tail tile, or a tile.
+  auto run_item = [&](int item) {
     if (S > 1) {
       // split tile: S consecutive tiles share a row tile and a column block
       int lo = 0, hi = E - 1;
@@ -729,7 +731,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
       const size_t ps = (size_t)S * R * a.N;
       run_split_tile<DUAL, MX, 128>(a, smem, tile_class(left), e, m0, m_end, nt * 128, kc0, kc1, pbase, ps, a.N,
                                     nt * 128);
-      continue;
+      return;
     }
     if (item >= full) {
       // a split of a tail tile
@@ -742,12 +744,12 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
         if (wide) {
           run_split_tile<DUAL, MX, 256>(a, smem, tile_class(t.left), t.e, t.m0, t.m_end, t.n0, kc0, kc1, pbase,
                                         St * tsz, cols, 0);
-          continue;
+          return;
         }
       }
       run_split_tile<DUAL, MX, 128>(a, smem, tile_class(t.left), t.e, t.m0, t.m_end, t.n0, kc0, kc1, pbase,
                                     St * tsz, cols, 0);
-      continue;
+      return;
     }
     const TileRef t = decode_tile(item, E, s_start, s_row0, s_rows, cols);
     const int cls = tile_class(t.left);
@@ -755,7 +757,33 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
       run_tile<DUAL, MX, !DUAL>(a, smem, cls, t.e, t.m0, t.m_end, t.n0);
     else
       run_tile<DUAL, MX, false>(a, smem, cls, t.e, t.m0, t.m_end, t.n0);
+  };
+
+  const int per_xcd = G >> 3;
+  if (a.queue != nullptr && (G & 7) == 0) {
+    // Per-XCD work queues: block b runs on XCD b % 8 and takes items of that
+    // XCD's share of every round (the same items the static order below
+    // gives it) in order from a counter, so blocks that drew cheap tiles
+    // take more. The counter for the next item is requested before a tile
+    // and read after it.
+    __shared__ int s_item;
+    const int xcd = (int)(blockIdx.x & 7);
+    auto item_of = [&](int j) { return (j / per_xcd) * G + xcd * per_xcd + j % per_xcd; };
+    if (tid == 0) s_item = item_of(atomicAdd(a.queue + xcd, 1));
+    __syncthreads();
+    int item = s_item;
+    while (item < n_items) {
+      int j_next = 0;
+      if (tid == 0) j_next = atomicAdd(a.queue + xcd, 1);
+      run_item(item);
+      if (tid == 0) s_item = item_of(j_next);
+      __syncthreads();
+      item = s_item;
+    }
+    return;
   }
+  const int slot = (G & 7) ? (int)blockIdx.x : ((int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3));
+  for (int item = slot; item < n_items; item += G) run_item(item);
 }
 
 template <bool DUAL>
@@ -974,6 +1002,12 @@ __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__
   y[(size_t)row * H + c] = s;
 }
 
+// Clears the per-XCD work counters of an FFN call (a kernel, not a memset,
+// so that the call can be captured in a graph).
+__global__ void clear_counters_kernel(int32_t* q, int n) {
+  if ((int)threadIdx.x < n) q[threadIdx.x] = 0;
+}
+
 __global__ void set_offsets_kernel(int32_t* offsets, int m) {
   if (threadIdx.x == 0) {
     offsets[0] = 0;
@@ -986,14 +1020,15 @@ __global__ void set_offsets_kernel(int32_t* offsets, int m) {
 // ---------------------------------------------------------------------------
 static size_t round256(size_t n) { return ((n + 255) / 256) * 256; }
 
-// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials. A split
+// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials | the two
+// GEMMs' per-XCD work counters (8 ints each). A split
 // launch has R <= M_cap partial rows for offsets that are a valid scan (and
 // R <= 64 E_local when every expert is small), and S <= 8. The kernel splits
 // only when R fits the plan's row map and its partials fit in part_cap.
 struct FfnWs {
-  size_t h, plan, part;  // byte offsets
-  long long part_cap;    // floats
-  int plan_rows;         // rows of the plan's row map
+  size_t h, plan, part, queue;  // byte offsets
+  long long part_cap;           // floats
+  int plan_rows;                // rows of the plan's row map
   size_t bytes;
 };
 
@@ -1010,7 +1045,8 @@ static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
   w.plan = h;
   w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
-  w.bytes = w.part + round256((size_t)w.part_cap * 4) + 256;
+  w.queue = w.part + round256((size_t)w.part_cap * 4);
+  w.bytes = w.queue + 256 + 256;
   return w;
 }
 
@@ -1068,11 +1104,16 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   // blocks per CU (a split launch has up to max(M_cap, 64 E_local) rows of
   // N columns to finish, a tail split up to G / 2 tiles of 256 x 256)
   auto reduce_grid = [&](int) { return (unsigned)(4 * cus); };
+  int32_t* queue = reinterpret_cast<int32_t*>(wsb + L.queue);
+  clear_counters_kernel<<<1, 64, 0, s>>>(queue, 16);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
               part, L.part_cap, plan, L.plan_rows};
+  g1.queue = queue;
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   // A GEMM can split only if its K range holds two splits of kMinSplitChunks.
   const bool split_gu = H / kBK >= 2 * kMinSplitChunks, split_dn = I / kBK >= 2 * kMinSplitChunks;
@@ -1083,6 +1124,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   }
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan, L.plan_rows};
+  g2.queue = queue + 8;
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1094,9 +1136,9 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
 // MXFP8 expert FFN: gate/up (MXFP8 in, MXFP8 h out), then down (bf16 out)
 // ---------------------------------------------------------------------------
 // MXFP8 FFN workspace: h codes [M_cap, I] | h scale dwords [I/128][M_cap] |
-// split-K plan | fp32 partials, sized as for the bf16 FFN.
+// split-K plan | fp32 partials, sized as for the bf16 FFN | work counters.
 struct FfnMxWs {
-  size_t hs, plan, part;  // byte offsets (h codes at 0)
+  size_t hs, plan, part, queue;  // byte offsets (h codes at 0)
   long long part_cap;
   int plan_rows;
   size_t bytes;
@@ -1110,7 +1152,8 @@ static FfnMxWs ffn_mx_ws_layout(int M_cap, int E_local, int H, int I) {
   w.part_cap = std::min(need, kPartCapFloats);
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
   w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
-  w.bytes = w.part + round256((size_t)w.part_cap * 4) + 256;
+  w.queue = w.part + round256((size_t)w.part_cap * 4);
+  w.bytes = w.queue + 256 + 256;
   return w;
 }
 
@@ -1137,6 +1180,7 @@ struct MxSplit {
   long long part_cap;
   int32_t* plan;
   int plan_rows;
+  int32_t* queue;  // per-XCD work counters or nullptr
 };
 
 static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
@@ -1156,6 +1200,7 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;
   g.plan_rows = sp.plan_rows;
+  g.queue = sp.queue;
   g.As = xs;
   g.Bs0 = wgs;
   g.Bs1 = wus;
@@ -1185,6 +1230,7 @@ static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;
   g.plan_rows = sp.plan_rows;
+  g.queue = sp.queue;
   g.As = as;
   g.Bs0 = bs;
   const bool split = sp.plan != nullptr && K / kMxChunk >= 2 * kMinSplitChunks;
@@ -1218,11 +1264,17 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   char* w = static_cast<char*>(ws);
   uint8_t* hq = reinterpret_cast<uint8_t*>(w);
   uint32_t* hs = reinterpret_cast<uint32_t*>(w + L.hs);
-  const MxSplit sp{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
-                   L.plan_rows};
-  hipError_t e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, sp, s);
+  int32_t* queue = reinterpret_cast<int32_t*>(w + L.queue);
+  clear_counters_kernel<<<1, 64, 0, s>>>(queue, 16);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, sp, s);
+  const MxSplit sp1{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
+                    L.plan_rows, queue};
+  e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, sp1, s);
+  if (e != hipSuccess) return e;
+  MxSplit sp2 = sp1;
+  sp2.queue = queue + 8;
+  return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, sp2, s);
 }
 
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {
