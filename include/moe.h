@@ -148,7 +148,9 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  * y_perm       [M_cap, H] dt, rows [0, offsets[E_local]) written
  * ws           holds h [M_cap, I] dt; for bf16 also the fp32 partial sums
  *              of split-K tiles (used when every expert has at most 64
- *              rows; summed in a fixed order, so results are deterministic)
+ *              rows, or for the tiles of a last, at most half-full round of
+ *              tiles; summed in a fixed order, so results are deterministic)
+ *              and the GEMMs' per-XCD tile counters (cleared by the call)
  * Limits: 0 <= E_local <= 256 (0 is a no-op); bf16: H % 128 == 0 and
  * I % 128 == 0; fp32: H % 4 == 0 and I % 4 == 0.
  */
@@ -251,9 +253,9 @@ moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint
  * [E_local, I/128, H]) into y_perm [M_cap, H] bf16.
  * ws holds h codes [M_cap, I] at offset 0 and their scales [I/128, M_cap]
  * at offset M_cap * I rounded up to 256 bytes, then the fp32 partial sums
- * of split-K tiles (used, as in moe_grouped_swiglu_ffn, when every expert has
- * at most 64 rows or a launch has fewer tiles than CUs; summed in a fixed
- * order, so results are deterministic).
+ * of split-K tiles (used as in moe_grouped_swiglu_ffn; summed in a fixed
+ * order, so results are deterministic) and the per-XCD tile counters.
+ * Calls that share a workspace must not overlap.
  */
 moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                                      const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
