@@ -281,9 +281,9 @@ FFN_CASES = [
 ]
 
 
-def _ffn_case(H, I, rows, seed):
-    """The MXFP8 FFN on one case under the rules of the module docstring.
-    Returns the FFN's workspace."""
+def _ffn_case(H, I, rows, seed, rerun=False):
+    """The MXFP8 FFN on one case under the rules of the module docstring
+    (rerun: a second call must be bitwise equal). Returns the FFN's workspace."""
     xp, wg, wu, wd, offsets, m = _inputs(H, I, rows, seed=seed)
     tx = moe.moe_mx_quantize(up(xp))
     tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (wg, wu, wd))
@@ -311,6 +311,10 @@ def _ffn_case(H, I, rows, seed):
             allow[r0:r1] = dev[r0:r1] @ Wd.T
     # the GPU's down GEMM sums |h_gpu| |W_down| <= mag + allow
     check_gemm(got, y_ref, mag + allow, f"ffn y H={H} I={I}", extra=allow)
+    if rerun:
+        y2, _ = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, doff)
+        torch.cuda.synchronize()
+        assert torch.equal(y2[:m], y[:m]), "a second call differs"
     # the gate/up entry point alone writes the same h
     h = moe.moe_grouped_swiglu_mx(tx, tg, tu, doff)
     torch.cuda.synchronize()
@@ -362,7 +366,7 @@ MX_TAIL_CASES = [
                          ids=[f"H{h}-I{i}-rows{r[0]}" for h, i, r, _ in MX_TAIL_CASES])
 def test_ffn_mx_tail_split(H, I, rows, plan):
     banner("mx ffn tail split", H, I, rows, "seed 4")
-    ws, M_cap, _ = _ffn_case(H, I, rows, seed=4)
+    ws, M_cap, _ = _ffn_case(H, I, rows, seed=4, rerun=True)
     hs_off = ((M_cap * I + 255) // 256) * 256
     plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
     got = ws[plan_off:plan_off + 20].view(torch.int32).cpu().numpy()

@@ -307,6 +307,11 @@ def test_ffn_tail_split(H, I, rows, plan):
     h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
     G.check_bf16(h, h_ref, "tail h")
     G.check_bf16(G.down(y)[:m], y_ref, "tail y", scale=G.down_scale(h_ref, wd, offsets))
+    # tiles taken from the work queues in whatever order: still bitwise equal
+    y2, _ = moe.moe_grouped_swiglu_ffn(G.up(xp, torch.bfloat16), G.up(wg, torch.bfloat16),
+                                       G.up(wu, torch.bfloat16), G.up(wd, torch.bfloat16), G.up_i32(offsets), ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y2[:m], y[:m])
 
 
 def test_combine_stage_on_oracle_inputs():
