@@ -159,12 +159,41 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[b][i][j] = f32x16_t{};
 
+  // Loop-invariant byte offsets of this lane's 16-byte pieces (dma16s; the
+  // chunk's column goes into the wave-uniform base): instruction t of wave w
+  // moves rows [8 (t kWaves + w), +8), lane l row l / 8, piece l % 8 of the
+  // swizzled row; A rows past the tile re-read its last row. Both weight
+  // matrices share offsets. A placeholder load (live == false) reads the
+  // first 16 bytes of the chunk in every lane.
+  constexpr int RPI = 8, LA = AR / (RPI * kWaves), LB = BN / (RPI * kWaves);
+  static_assert(AR % (RPI * kWaves) == 0 && BN % (RPI * kWaves) == 0, "rows per wave");
+  uint32_t offA[LA], offB[LB];
+#pragma unroll
+  for (int t = 0; t < LA; ++t) {
+    const int r = (t * kWaves + wave) * RPI + lane / 8;
+    const int rr = r < a_rows ? r : a_rows - 1;
+    offA[t] = (uint32_t)(rr * K * 2 + swz_chunk<kBK>(r, lane % 8) * 16);
+  }
+#pragma unroll
+  for (int t = 0; t < LB; ++t) {
+    const int r = (t * kWaves + wave) * RPI + lane / 8;
+    offB[t] = (uint32_t)(r * K * 2 + swz_chunk<kBK>(r, lane % 8) * 16);
+  }
   if (kc1 < 0) kc1 = K / kBK;
   auto issue = [&](int kc, bool live, bf16_t* st) {
-    const int col = (kc0 + kc) * kBK;
-    dma_rows<AR, kWaves, kBK>(A, K, col, a_rows, live, st, wave, lane);
-    dma_rows<BN, kWaves, kBK>(B0, K, col, BN, live, st + AR * kBK, wave, lane);
-    if (DUAL) dma_rows<BN, kWaves, kBK>(B1, K, col, BN, live, st + (AR + BN) * kBK, wave, lane);
+    const size_t col = (size_t)(live ? kc0 + kc : kc0) * kBK;
+    const void* pa = uniform_ptr(A + col);
+#pragma unroll
+    for (int t = 0; t < LA; ++t) dma16s(pa, live ? offA[t] : 0u, st + (t * kWaves + wave) * RPI * kBK);
+    const void* pb0 = uniform_ptr(B0 + col);
+#pragma unroll
+    for (int t = 0; t < LB; ++t) dma16s(pb0, live ? offB[t] : 0u, st + (AR + (t * kWaves + wave) * RPI) * kBK);
+    if (DUAL) {
+      const void* pb1 = uniform_ptr(B1 + col);
+#pragma unroll
+      for (int t = 0; t < LB; ++t)
+        dma16s(pb1, live ? offB[t] : 0u, st + (AR + BN + (t * kWaves + wave) * RPI) * kBK);
+    }
   };
   // Operands of k-step s+1 are read from LDS while the MFMAs of k-step s
   // run (register double buffering), across chunks too (pipeline_xk).
@@ -290,10 +319,8 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
   const char* B0 = reinterpret_cast<const char*>(a.B0) + ((size_t)e * N + n0) * K;
   const char* B1 = DUAL ? reinterpret_cast<const char*>(a.B1) + ((size_t)e * N + n0) * K : nullptr;
 
-  // Loop-invariant byte offsets of this lane's 16-byte pieces (dma16s): one
-  // instruction moves 8 rows of 128 bytes, instruction t of wave w rows
-  // [8 (t kWaves + w), +8); A rows past the tile re-read its last row, as
-  // in dma_rows. Both weight matrices share offsets.
+  // Loop-invariant byte offsets of this lane's 16-byte pieces, as in
+  // gemm_tile (the rows of a chunk are 128 codes here).
   constexpr int RPI = 8, LA = AR / (RPI * kWaves), LB = BN / (RPI * kWaves);
   uint32_t offA[LA], offB[LB];
 #pragma unroll

@@ -314,6 +314,46 @@ def test_ffn_tail_split(H, I, rows, plan):
     assert torch.equal(y2[:m], y[:m])
 
 
+RAGGED_CASES = [
+    # (H, I, rows per local expert, (S, cols) of the down GEMM): experts of
+    # 256 q + t rows end in a 64-, 128- or 256-row tile (t = 1, 44, 64, 65, 4).
+    # Case 1: the gate/up GEMM runs 320 tiles unsplit and splits its last 64
+    # (among them 64-row remainders and one-row experts) along K over the idle
+    # CUs; the down GEMM runs split-K. Case 2: the down GEMM in 256-column
+    # tiles over 29 ragged experts.
+    (1024, 4096, [257, 300, 321, 576, 1], (3, 128)),
+    (4096, 512, [300] * 28 + [64, 260, 576, 1], (1, 256)),
+]
+
+
+@pytest.mark.parametrize("H,I,rows,plan", RAGGED_CASES, ids=["tail-split", "wide-down"])
+def test_ffn_ragged_tails(H, I, rows, plan):
+    """Experts with short row remainders after full 256-row tiles."""
+    banner("stage ffn ragged tails", H, I, len(rows), "experts seed 7")
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="ragged", H=H, I=I, E=len(rows), k=1, E_local=len(rows))
+    wg, wu, wd = make_experts(shape, list(range(len(rows))), seed=7)
+    m = sum(rows)
+    x, *_ = make_router(shape, m, 0.0, seed=7)
+    offsets = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    M_cap = m + 2
+    xp = np.zeros((M_cap, H), np.float32)
+    xp[:m] = x
+    h_ref, y_ref = O.grouped_swiglu_ffn(x, wg, wu, wd, offsets, bf16=True)
+    dg, du, dd = (G.up(w, torch.bfloat16) for w in (wg, wu, wd))
+    dx, doff = G.up(xp, torch.bfloat16), G.up_i32(offsets)
+    y, ws = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff)
+    torch.cuda.synchronize()
+    off = ((M_cap * I * 2 + 255) // 256) * 256
+    got = ws[off:off + 20].view(torch.int32).cpu().numpy()
+    assert (got[0], got[4]) == plan, got[:5]
+    h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
+    G.check_bf16(h, h_ref, "ragged h")
+    G.check_bf16(G.down(y)[:m], y_ref, "ragged y", scale=G.down_scale(h_ref, wd, offsets))
+    y2, _ = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y2[:m], y[:m])
+
+
 def test_combine_stage_on_oracle_inputs():
     banner("stage combine qwen3")
     li = make_layer("qwen3", 64, 1.0, seed=4)
