@@ -421,7 +421,7 @@ __global__ __launch_bounds__(256) void gate_topk_f32_kernel(
 // Activation profile: per-block expert counts (LDS atomics on integers, so
 // the result does not depend on their order).
 // ---------------------------------------------------------------------------
-constexpr int kTokPerBlk = 1024;  // tokens per block of the count table
+constexpr int kTokPerBlk = 256;  // tokens per block of the count table (T / 256 blocks)
 
 __global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ ids, int T, int k, int E,
                                                    int32_t* __restrict__ table) {
@@ -450,6 +450,7 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
   const int E = map.n_experts, L = map.n_local;
   for (int e = tid; e < E; e += 256) {
     int c = 0;
+#pragma unroll 8
     for (int b = 0; b < n_blk; ++b) c += table[(size_t)b * E + e];
     counts[e] = c;
     s_cnt[e] = c;
@@ -462,6 +463,7 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
   if (tid < L) {
     offsets[tid + 1] = excl + v;
     int run = excl;
+#pragma unroll 8
     for (int b = 0; b < n_blk; ++b) {
       bases[(size_t)b * L + tid] = run;
       run += table[(size_t)b * E + my_e];
@@ -475,7 +477,7 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
 
 // ---------------------------------------------------------------------------
 // Dispatch permutation, step 1: positions. Block b re-reads the ids of its
-// 1024 tokens in four rounds of 256 (one token per thread). The rank of an
+// kTokPerBlk tokens in rounds of 256 (one token per thread). The rank of an
 // assignment within its slot comes from 64-bit lane masks per (round, wave)
 // -- lane order is token order -- never from atomic return order, so the
 // permutation is the stable counting sort and is identical run to run.
@@ -536,8 +538,8 @@ __global__ __launch_bounds__(256) void permute_index_kernel(const int32_t* __res
 }
 
 // Dispatch permutation, step 2: x_perm[pos] = x[perm_src[pos] / k] for
-// pos < offsets[E_local]. One wave per row, 16-byte vectors, up to eight
-// loads in flight per lane before the stores.
+// pos < offsets[E_local]. One wave per row, 16-byte vectors, eight (then
+// four) loads in flight per lane before the stores.
 __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restrict__ x, int row_vecs, int T, int k,
                                                           const int32_t* __restrict__ perm_src,
                                                           const int32_t* __restrict__ m_loc, int M_cap,
@@ -558,6 +560,14 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restric
       for (int u = 0; u < U; ++u) buf[u] = src[v0 + u * kWave + lane];
 #pragma unroll
       for (int u = 0; u < U; ++u) dst[v0 + u * kWave + lane] = buf[u];
+    }
+    if (v0 + (U / 2) * kWave <= row_vecs) {  // half a batch (rows of 2048 bf16, row tails)
+      uint4 buf[U / 2];
+#pragma unroll
+      for (int u = 0; u < U / 2; ++u) buf[u] = src[v0 + u * kWave + lane];
+#pragma unroll
+      for (int u = 0; u < U / 2; ++u) dst[v0 + u * kWave + lane] = buf[u];
+      v0 += (U / 2) * kWave;
     }
     for (int v = v0 + lane; v < row_vecs; v += kWave) dst[v] = src[v];
   }
