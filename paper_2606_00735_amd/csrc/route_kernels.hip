@@ -118,6 +118,7 @@ __device__ __forceinline__ void write_topk(const float (&sel_v)[kMaxTopk], const
 // (see pipeline).
 // ---------------------------------------------------------------------------
 constexpr int kGateBK = 64;
+constexpr int kSmallRouterT = 8192;  // largest batch for gate_topk_bf16_small_kernel
 
 template <int NCB>
 __global__ __launch_bounds__(256) void gate_topk_bf16_kernel(
@@ -260,6 +261,102 @@ __global__ __launch_bounds__(256) void gate_topk_bf16_ksplit_kernel(
       float z = 0.0f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) z += red[((w * NCB + c) * 16 + v) * kWave + lane];
+      const int col = c * 32 + r;
+      val[c] = (col < E) ? z + bias_r[c] : -__builtin_huge_valf();
+    }
+    if (logits != nullptr && row < T) {
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) {
+        const int col = c * 32 + r;
+        if (col < E) logits[(size_t)row * E + col] = val[c];
+      }
+    }
+    float sel_v[kMaxTopk];
+    int sel_i[kMaxTopk];
+    topk_group<32, NCB>(val, r, E, k, sel_v, sel_i);
+    if (row < T) write_topk(sel_v, sel_i, r, k, row, ids, wts);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Router, bf16, for batches of a few hundred tokens (decode) and E <= 128:
+// 32 tokens per block and NW waves, each taking an equal, contiguous share of
+// the K range straight from global memory into registers (no LDS stages, so
+// no barriers in the K loop: one block's K range is streamed by all its
+// waves at once instead of chunk by chunk). A wave loads GK k-steps of
+// operands per group, the next group while the MFMAs of the current one run;
+// the four k-steps of a 64-wide chunk cover whole 128-byte lines of each row.
+// Partial logits are summed through LDS in wave order; on inputs whose
+// partial sums are exact in fp32 that equals any other order.
+// ---------------------------------------------------------------------------
+template <int NCB, int NW, int GK>
+__global__ __launch_bounds__(NW * 64) void gate_topk_bf16_small_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
+    int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
+    float* __restrict__ wts) {
+  __shared__ float red[NW * NCB * 16 * kWave];  // partial logits of every wave
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 31, half = lane >> 5;
+  const int row0 = blockIdx.x * 32;
+  // lane (r, half) holds elements 16 s + 8 half .. + 8 of k-step s of token
+  // row r (A operand) and of router row 32 c + r (B operand, block c);
+  // rows past the batch or past E re-read the last one and are masked below
+  const bf16x8_t* xp =
+      reinterpret_cast<const bf16x8_t*>(x + (size_t)min(row0 + r, T - 1) * H) + half;
+  const bf16x8_t* wp[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c)
+    wp[c] = reinterpret_cast<const bf16x8_t*>(wr + (size_t)min(c * 32 + r, E - 1) * H) + half;
+  const int nks = H / 16, per = nks / NW;  // the launcher checks per % (2 GK) == 0
+  const int s0 = wave * per;
+
+  f32x16_t acc[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) acc[c] = f32x16_t{};
+  bf16x8_t a0[GK], b0[GK][NCB], a1[GK], b1[GK][NCB];
+  auto load = [&](int s, bf16x8_t(&a)[GK], bf16x8_t(&b)[GK][NCB]) {
+#pragma unroll
+    for (int g = 0; g < GK; ++g) {
+      a[g] = xp[2 * (s + g)];
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) b[g][c] = wp[c][2 * (s + g)];
+    }
+  };
+  auto mma = [&](const bf16x8_t(&a)[GK], const bf16x8_t(&b)[GK][NCB]) {
+#pragma unroll
+    for (int g = 0; g < GK; ++g)
+#pragma unroll
+      for (int c = 0; c < NCB; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[g], b[g][c], acc[c], 0, 0, 0);
+  };
+  load(s0, a0, b0);
+  for (int s = s0; s < s0 + per; s += 2 * GK) {
+    load(s + GK, a1, b1);
+    mma(a0, b0);
+    if (s + 2 * GK < s0 + per) load(s + 2 * GK, a0, b0);
+    mma(a1, b1);
+  }
+
+#pragma unroll
+  for (int c = 0; c < NCB; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[((wave * NCB + c) * 16 + v) * kWave + lane] = acc[c][v];
+  __syncthreads();
+
+  float bias_r[NCB];
+#pragma unroll
+  for (int c = 0; c < NCB; ++c) {
+    const int col = c * 32 + r;
+    bias_r[c] = (bias != nullptr && col < E) ? bias[col] : 0.0f;
+  }
+  // wave w finishes accumulator registers v = w, w + NW, ... (2 rows each)
+  for (int v = wave; v < 16; v += NW) {
+    const int row = row0 + 8 * (v >> 2) + 4 * half + (v & 3);
+    float val[NCB];
+#pragma unroll
+    for (int c = 0; c < NCB; ++c) {
+      float z = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) z += red[((w * NCB + c) * 16 + v) * kWave + lane];
       const int col = c * 32 + r;
       val[c] = (col < E) ? z + bias_r[c] : -__builtin_huge_valf();
     }
@@ -665,6 +762,27 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
   const int ncb = (E + 31) / 32;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   const bf16_t* wb = static_cast<const bf16_t*>(wr);
+  // Small batches of few experts: 32-token blocks whose waves stream
+  // contiguous shares of the K range (NW waves, GK k-steps per load group).
+  if (ncb <= 4 && T <= kSmallRouterT) {
+    const dim3 g32((T + 31) / 32);
+    const int nks = H / 16;
+#define MOE_GATE_SMALL(N, NW, GK)                                                                     \
+  case N:                                                                                           \
+    if (nks % (NW * 2 * GK) != 0) break;                                                            \
+    gate_topk_bf16_small_kernel<N, NW, GK><<<g32, NW * 64, 0, s>>>(xb, wb, bias, T, H, E, k, logits, \
+                                                                    ids, wts);                       \
+    return hipGetLastError();
+    switch (ncb) {
+      MOE_GATE_SMALL(1, 16, 4)
+      MOE_GATE_SMALL(2, 8, 4)
+      MOE_GATE_SMALL(3, 8, 2)
+      MOE_GATE_SMALL(4, 8, 2)
+      default:
+        break;
+    }
+#undef MOE_GATE_SMALL
+  }
   // Few experts and fewer than 256 blocks of 128 tokens: 32-token blocks with
   // the K range split over the waves, so more CUs stream x.
   if (ncb <= 4 && (T + 127) / 128 < 256) {

@@ -163,7 +163,13 @@ ROUTER_WIDE = [
     (256, 256, 8, 20000),     # 4-wave router, 128-token blocks, E_pad 256
     (256, 100, 6, 33000),     # 4-wave router, E_pad 128
     (256, 40, 4, 33000),      # 4-wave router, E = 40 of 64
-    (2048, 128, 8, 4096),     # K-split router
+    (2048, 128, 8, 9000),     # K-split router
+    (1088, 8, 2, 40),         # K-split router: H/16 = 68 k-steps do not split evenly over 16 waves
+    (4096, 8, 2, 1),          # small-batch router (16 waves, E_pad 32): one token
+    (4096, 8, 2, 33),         # small-batch router, ragged second block
+    (2048, 64, 4, 100),       # small-batch router, E_pad 64
+    (2048, 96, 6, 65),        # small-batch router, E = 96 of 96
+    (2048, 128, 8, 4096),     # small-batch router (8 waves, E_pad 128)
 ]
 
 
