@@ -134,11 +134,15 @@ def main():
         moe.moe_layer(xb, wr, bias, k, emap, wg, wu, wd, bufs=b)
         return b
 
+    # bf16: the FFN reads the routed rows of x itself (moe_grouped_swiglu_ffn_gather),
+    # so the permute stage only computes positions
+    fuse = dt == torch.bfloat16
+
     def run_timed(xb, bb, Tb, steps, warmup):
         """Warmup, then `steps` timed layer passes with per-stage HIP events."""
         names = ["gate_topk", "histogram_scan", "permute", "grouped_swiglu_ffn", "combine"]
         for _ in range(warmup):
-            moe.moe_layer(xb, wr, bb["bias"], k, emap, wg, wu, wd, bufs=bb)
+            moe.moe_layer(xb, wr, bb["bias"], k, emap, wg, wu, wd, bufs=bb, fuse_gather=fuse)
         torch.cuda.synchronize()
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
         torch.cuda.synchronize()
@@ -152,9 +156,13 @@ def main():
                                                                  counts=bb["counts"], offsets=bb["offsets"])
             ev[2].record()
             xp, ps, dest = moe.moe_permute(xb, ids, emap, hws, x_perm=bb["x_perm"], perm_src=bb["perm_src"],
-                                           dest=bb["dest"])
+                                           dest=bb["dest"], gather=not fuse)
             ev[3].record()
-            yp, _ = moe.moe_grouped_swiglu_ffn(xp, wg, wu, wd, offsets, ws=bb["ffn_ws"], y_perm=bb["y_perm"])
+            if fuse:
+                yp, _ = moe.moe_grouped_swiglu_ffn_gather(xb, ps, k, wg, wu, wd, offsets, ws=bb["ffn_ws"],
+                                                          y_perm=bb["y_perm"])
+            else:
+                yp, _ = moe.moe_grouped_swiglu_ffn(xp, wg, wu, wd, offsets, ws=bb["ffn_ws"], y_perm=bb["y_perm"])
             ev[4].record()
             moe.moe_unpermute_combine(yp, wts, dest, Tb, out=bb["out"])
             ev[5].record()
@@ -189,7 +197,8 @@ def main():
     mfma_bound = w["ffn_flops"] / (peak_f * 1e12) >= w["ffn_bytes"] / (PEAK_HBM_GBPS * 1e9)
     wkey = f"{args.config}-T{T}-a{args.alpha:g}-s{args.seed}"
     roofline = {
-        "kernel": "moe_grouped_swiglu_ffn (gate/up and down GEMMs + split-K reductions)",
+        "kernel": ("moe_grouped_swiglu_ffn_gather (gate/up GEMM reading the routed rows of x, down GEMM, "
+                   "split-K reductions)" if fuse else "moe_grouped_swiglu_ffn (gate/up and down GEMMs + split-K reductions)"),
         "bound": "mfma" if mfma_bound else "hbm",
         "achieved": round(ffn_tflops if mfma_bound else ffn_gbps, 3),
         "peak": peak_f if mfma_bound else PEAK_HBM_GBPS,

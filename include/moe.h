@@ -122,7 +122,9 @@ moe_status moe_expert_histogram_scan(const int32_t* topk_ids, int T, int k, int 
  *
  * ws, ws_bytes  the workspace filled by moe_expert_histogram_scan (same T, k,
  *               E, E_local); expert_map is the same HOST array.
- * x_perm   [M_cap, H] dt   rows [0, offsets[E_local]) written
+ * x_perm   [M_cap, H] dt   rows [0, offsets[E_local]) written; may be NULL,
+ *          then only perm_src and dest are written (for
+ *          moe_grouped_swiglu_ffn_gather, which reads the rows from x)
  * perm_src [M_cap]    int32 entries [0, offsets[E_local]) written
  * dest     [T*k]      int32 all written
  * Requires M_cap >= T*k (the worst case, so no host sync is needed).
@@ -158,6 +160,30 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
                                   const void* w_down, const int32_t* offsets, int E_local,
                                   int H, int I, int M_cap, moe_dtype dt, void* y_perm,
                                   void* ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
+ * moe_grouped_swiglu_ffn_gather - moe_grouped_swiglu_ffn with the dispatch
+ * gather folded into the gate/up GEMM's operand loads.
+ *
+ * Computes exactly what moe_permute followed by moe_grouped_swiglu_ffn
+ * computes (bitwise the same y_perm and h), but row r of the expert input is
+ * read as x[perm_src[r] / k] (the token of flat assignment perm_src[r],
+ * Section 2's dispatch) instead of from a permuted copy, so the x_perm write
+ * and re-read are skipped: call moe_permute with x_perm = NULL for perm_src.
+ *
+ * x        [T, H] bf16 (the layer's input tokens); T >= 1, T*H*2 < 2^32
+ * perm_src [M_cap] int32 from moe_permute; entries of rows outside
+ *          [offsets[0], offsets[E_local]) are not read, the others are
+ *          clamped to a token of x
+ * k        the top-k of the routing (1..MOE_MAX_TOPK)
+ * other arguments, workspace and limits: as moe_grouped_swiglu_ffn (bf16
+ * only; fp32 returns MOE_ERR_UNSUPPORTED).
+ */
+moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src, int T, int k,
+                                         const void* w_gate, const void* w_up, const void* w_down,
+                                         const int32_t* offsets, int E_local, int H, int I, int M_cap,
+                                         moe_dtype dt, void* y_perm, void* ws, size_t* ws_bytes,
+                                         hipStream_t stream);
 
 /*
  * moe_unpermute_combine - gather and weighted sum back to token order.

@@ -26,6 +26,7 @@ from ._lib import (  # noqa: F401
     moe_gate_topk,
     moe_grouped_gemm_mx,
     moe_grouped_swiglu_ffn,
+    moe_grouped_swiglu_ffn_gather,
     moe_grouped_swiglu_ffn_mx,
     moe_grouped_swiglu_mx,
     moe_layer,

@@ -25,7 +25,8 @@ EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert
             "moe_permute", "moe_grouped_swiglu_ffn", "moe_unpermute_combine", "moe_load_sweep",
             "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_placement_cost",
             "moe_window_push", "moe_drift_distance", "moe_mx_quantize", "moe_grouped_swiglu_mx",
-            "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx", "moe_load_sweep_mx")
+            "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx", "moe_load_sweep_mx",
+            "moe_grouped_swiglu_ffn_gather")
 
 
 class MoeError(RuntimeError):
@@ -62,6 +63,9 @@ def load_library(path: str = LIB_PATH):
     L.moe_permute.argtypes = [_P, _P, _P, _P, _SZ, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]
     L.moe_grouped_swiglu_ffn.restype = _I
     L.moe_grouped_swiglu_ffn.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _PSZ, _P]
+    L.moe_grouped_swiglu_ffn_gather.restype = _I
+    L.moe_grouped_swiglu_ffn_gather.argtypes = [_P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _PSZ,
+                                                _P]
     L.moe_unpermute_combine.restype = _I
     L.moe_unpermute_combine.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P]
     L.moe_load_sweep.restype = _I
@@ -189,8 +193,10 @@ def moe_expert_histogram_scan(ids, E, expert_map, ws=None, counts=None, offsets=
     return counts, offsets, ws
 
 
-def moe_permute(x, ids, expert_map, ws, M_cap=None, x_perm=None, perm_src=None, dest=None):
-    """Dispatch. Returns (x_perm [M_cap,H], perm_src [M_cap], dest [T*k])."""
+def moe_permute(x, ids, expert_map, ws, M_cap=None, x_perm=None, perm_src=None, dest=None, gather=True):
+    """Dispatch. Returns (x_perm [M_cap,H], perm_src [M_cap], dest [T*k]); with
+    gather=False only the positions (x_perm is None), for
+    moe_grouped_swiglu_ffn_gather."""
     L = load_library()
     T, H = x.shape
     k = ids.shape[1]
@@ -199,12 +205,15 @@ def moe_permute(x, ids, expert_map, ws, M_cap=None, x_perm=None, perm_src=None, 
     E_local = int((emap >= 0).sum())
     M_cap = T * k if M_cap is None else M_cap
     dev = x.device
-    x_perm = torch.empty((M_cap, H), dtype=x.dtype, device=dev) if x_perm is None else x_perm
+    if not gather:
+        x_perm = None
+    elif x_perm is None:
+        x_perm = torch.empty((M_cap, H), dtype=x.dtype, device=dev)
     perm_src = torch.empty(M_cap, dtype=torch.int32, device=dev) if perm_src is None else perm_src
     dest = torch.empty(T * k, dtype=torch.int32, device=dev) if dest is None else dest
     st = L.moe_permute(_dev(x, "x"), _dev(ids, "ids", torch.int32), emap_p, _dev(ws, "ws"),
                        ws.numel() * ws.element_size(), T, H, k, E, E_local, M_cap, _dtype_code(x),
-                       _dev(x_perm, "x_perm", x.dtype), _dev(perm_src, "perm_src", torch.int32),
+                       _ptr_or_null(x_perm, "x_perm", x.dtype), _dev(perm_src, "perm_src", torch.int32),
                        _dev(dest, "dest", torch.int32), _stream())
     _check("moe_permute", st)
     return x_perm, perm_src, dest
@@ -241,6 +250,33 @@ def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_per
                                   _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ctypes.byref(n),
                                   _stream())
     _check("moe_grouped_swiglu_ffn", st)
+    return y_perm, ws
+
+
+def moe_grouped_swiglu_ffn_gather(x, perm_src, k, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):
+    """The grouped SwiGLU FFN reading row r of its input as x[perm_src[r] // k]
+    (bf16). Same results as moe_permute + moe_grouped_swiglu_ffn. Returns
+    (y_perm [M_cap,H], ws)."""
+    L = load_library()
+    T, H = x.shape
+    M_cap = perm_src.numel()
+    E_local, I, H2 = w_gate.shape
+    if H2 != H or tuple(w_up.shape) != (E_local, I, H) or tuple(w_down.shape) != (E_local, H, I):
+        raise ValueError("expert weights must be w_gate/w_up [E_local, I, H] and w_down [E_local, H, I]")
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    dt = _dtype_code(x)
+    need = ffn_ws_bytes(E_local, H, I, M_cap, x.dtype)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+    y_perm = torch.empty((M_cap, H), dtype=x.dtype, device=x.device) if y_perm is None else y_perm
+    n = ctypes.c_size_t(ws.numel() * ws.element_size())
+    st = L.moe_grouped_swiglu_ffn_gather(_dev(x, "x"), _dev(perm_src, "perm_src", torch.int32), T, k,
+                                         _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
+                                         _dev(w_down, "w_down", x.dtype), _dev(offsets, "offsets", torch.int32),
+                                         E_local, H, I, M_cap, dt, _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"),
+                                         ctypes.byref(n), _stream())
+    _check("moe_grouped_swiglu_ffn_gather", st)
     return y_perm, ws
 
 
@@ -291,11 +327,14 @@ def moe_load_sweep(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=No
 # ---------------------------------------------------------------------------
 # Whole layer: the five stream-ordered calls, no host synchronisation.
 # ---------------------------------------------------------------------------
-def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=False, bufs=None):
+def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=False, bufs=None,
+              fuse_gather=False):
     """One GPU's share of the MoE layer; returns a dict of every output.
 
     ``bufs`` (optional dict) supplies preallocated outputs and workspaces so
-    that repeated calls allocate nothing.
+    that repeated calls allocate nothing. ``fuse_gather`` (bf16): the FFN
+    reads the routed rows of x itself (moe_grouped_swiglu_ffn_gather) and
+    x_perm is not built (None in the result); every other output is the same.
     """
     b = {} if bufs is None else bufs
     T = x.shape[0]
@@ -305,13 +344,19 @@ def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=Fal
     counts, offsets, hws = moe_expert_histogram_scan(ids, E, expert_map, ws=b.get("hist_ws"),
                                                      counts=b.get("counts"), offsets=b.get("offsets"))
     x_perm, perm_src, dest = moe_permute(x, ids, expert_map, hws, x_perm=b.get("x_perm"),
-                                         perm_src=b.get("perm_src"), dest=b.get("dest"))
-    y_perm, fws = moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=b.get("ffn_ws"),
-                                         y_perm=b.get("y_perm"))
+                                         perm_src=b.get("perm_src"), dest=b.get("dest"), gather=not fuse_gather)
+    if fuse_gather:
+        y_perm, fws = moe_grouped_swiglu_ffn_gather(x, perm_src, k, w_gate, w_up, w_down, offsets,
+                                                    ws=b.get("ffn_ws"), y_perm=b.get("y_perm"))
+    else:
+        y_perm, fws = moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=b.get("ffn_ws"),
+                                             y_perm=b.get("y_perm"))
     out = moe_unpermute_combine(y_perm, wts, dest, T, out=b.get("out"))
     if bufs is not None:
-        bufs.update(ids=ids, weights=wts, hist_ws=hws, counts=counts, offsets=offsets, x_perm=x_perm,
-                    perm_src=perm_src, dest=dest, ffn_ws=fws, y_perm=y_perm, out=out)
+        bufs.update(ids=ids, weights=wts, hist_ws=hws, counts=counts, offsets=offsets, perm_src=perm_src,
+                    dest=dest, ffn_ws=fws, y_perm=y_perm, out=out)
+        if x_perm is not None:
+            bufs["x_perm"] = x_perm
     return dict(ids=ids, weights=wts, logits=lg, counts=counts, offsets=offsets, x_perm=x_perm,
                 perm_src=perm_src, dest=dest, y_perm=y_perm, h=fws, out=out)
 

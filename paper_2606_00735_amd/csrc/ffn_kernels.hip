@@ -74,6 +74,12 @@ struct GemmArgs {
   // Per-XCD work counters (8 ints, zero before the launch) or nullptr for
   // the static tile order.
   int32_t* queue;
+  // Row gather (bf16 GEMMs): when a_src != nullptr, row m of the A operand
+  // is row clamp(a_src[m] / a_div, 0, a_T - 1) of A (A holds a_T rows and
+  // a_T * K * 2 < 2^32), so the gate/up GEMM reads the routed tokens of x
+  // directly instead of a permuted copy.
+  const int32_t* a_src;
+  int a_div, a_T;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -146,7 +152,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
   const int K = a.K, N = a.N;
-  const bf16_t* A = a.A + (size_t)m0 * K;
+  const bool gather = a.a_src != nullptr;
+  const bf16_t* A = gather ? a.A : a.A + (size_t)m0 * K;
   const int a_rows = m_end - m0;
   const bf16_t* B0 = a.B0 + ((size_t)e * N + n0) * K;
   const bf16_t* B1 = DUAL ? a.B1 + ((size_t)e * N + n0) * K : nullptr;
@@ -171,8 +178,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
 #pragma unroll
   for (int t = 0; t < LA; ++t) {
     const int r = (t * kWaves + wave) * RPI + lane / 8;
-    const int rr = r < a_rows ? r : a_rows - 1;
-    offA[t] = (uint32_t)(rr * K * 2 + swz_chunk<kBK>(r, lane % 8) * 16);
+    int rr = r < a_rows ? r : a_rows - 1;
+    if (gather) rr = min(max(a.a_src[m0 + rr] / a.a_div, 0), a.a_T - 1);
+    offA[t] = (uint32_t)rr * (uint32_t)(K * 2) + (uint32_t)(swz_chunk<kBK>(r, lane % 8) * 16);
   }
 #pragma unroll
   for (int t = 0; t < LB; ++t) {
@@ -1095,7 +1103,7 @@ static int device_cu_count() {
 
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
                       const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
-                      void* ws, hipStream_t s) {
+                      void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
   const FfnWs L = ffn_ws_layout(M_cap, E_local, H, I, bf16);
   char* wsb = static_cast<char*>(ws);
@@ -1139,6 +1147,9 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
               part, L.part_cap, plan, L.plan_rows};
   g1.queue = queue;
+  g1.a_src = a_src;
+  g1.a_div = a_div;
+  g1.a_T = a_T;
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

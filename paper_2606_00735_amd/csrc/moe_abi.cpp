@@ -211,7 +211,7 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
   if (ws == nullptr) return MOE_ERR_INVALID_ARG;
   if (ws_bytes < moe::hist_ws_bytes(T, E, E_local)) return MOE_ERR_WORKSPACE;
   if (T == 0) return MOE_OK;
-  if (!x || !topk_ids || !dest || (M_cap > 0 && (!x_perm || !perm_src))) return MOE_ERR_INVALID_ARG;
+  if (!x || !topk_ids || !dest || (M_cap > 0 && !perm_src)) return MOE_ERR_INVALID_ARG;
   if (!aligned16(x) || !aligned16(ws) || (x_perm && !aligned16(x_perm)) || !aligned4(topk_ids) ||
       !aligned4(dest) || (perm_src && !aligned4(perm_src)))
     return MOE_ERR_INVALID_ARG;
@@ -238,6 +238,31 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
     return MOE_ERR_INVALID_ARG;
   return hip_status(moe::launch_ffn(x_perm, w_gate, w_up, w_down, offsets, E_local, H, I, M_cap,
                                     dt == MOE_BF16, y_perm, ws, stream));
+}
+
+moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src, int T, int k, const void* w_gate,
+                                         const void* w_up, const void* w_down, const int32_t* offsets, int E_local,
+                                         int H, int I, int M_cap, moe_dtype dt, void* y_perm, void* ws,
+                                         size_t* ws_bytes, hipStream_t stream) {
+  moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
+  if (st != MOE_OK) return st;
+  if (ws_bytes == nullptr || T < 1 || k < 1 || k > MOE_MAX_TOPK) return MOE_ERR_INVALID_ARG;
+  if (dt != MOE_BF16) return MOE_ERR_UNSUPPORTED;
+  // row offsets into x are 32-bit byte offsets
+  if ((unsigned long long)T * (unsigned long long)H * 2ull > 0xFFFFFFFFull) return MOE_ERR_UNSUPPORTED;
+  const size_t need = moe::ffn_ws_bytes(M_cap, E_local, H, I, true);
+  if (ws == nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (*ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!x || !perm_src || !w_gate || !w_up || !w_down || !offsets || !y_perm) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_perm) ||
+      !aligned16(ws) || !aligned4(offsets) || !aligned4(perm_src))
+    return MOE_ERR_INVALID_ARG;
+  return hip_status(moe::launch_ffn(x, w_gate, w_up, w_down, offsets, E_local, H, I, M_cap, true, y_perm, ws,
+                                    stream, perm_src, k, T));
 }
 
 moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const int32_t* dest, int T, int k,

@@ -886,7 +886,8 @@ hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map,
   hist_ws_split(const_cast<void*>(ws), T, map.n_experts, map.n_local, &table, &bases, &m_loc);
   permute_index_kernel<<<n_blk, 256, 0, s>>>(ids, T, k, map, bases, M_cap, perm_src, dest);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || map.n_local == 0 || M_cap == 0) return e;
+  // x_perm == nullptr: positions only (the FFN gathers the rows itself)
+  if (e != hipSuccess || map.n_local == 0 || M_cap == 0 || x_perm == nullptr) return e;
   const int row_vecs = (H * (bf16 ? 2 : 4)) / 16;
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) != hipSuccess ||

@@ -139,6 +139,34 @@ def test_ffn_validation_and_query(L):
                                     ctypes.byref(n), None) == WORKSPACE
 
 
+def test_ffn_gather_validation_and_query(L):
+    n, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    args = (8, 4096, 14336, 8192)
+    assert L.moe_grouped_swiglu_ffn_gather(None, None, 4096, 2, None, None, None, None, *args, 1, None, None,
+                                           ctypes.byref(n), None) == 0
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, *args, 1, None, None, ctypes.byref(m), None) == 0
+    assert n.value == m.value  # the same workspace
+    # fp32 has no gathering variant
+    assert L.moe_grouped_swiglu_ffn_gather(None, None, 64, 2, None, None, None, None, 8, 128, 128, 128, 0, None,
+                                           None, ctypes.byref(n), None) == UNSUPPORTED
+    for T, k in ((0, 2), (64, 0), (64, 17)):
+        assert L.moe_grouped_swiglu_ffn_gather(None, None, T, k, None, None, None, None, 8, 128, 128, 128, 1,
+                                               None, None, ctypes.byref(n), None) == INVALID
+    # row offsets into x must fit 32 bits
+    assert L.moe_grouped_swiglu_ffn_gather(None, None, 1 << 20, 1, None, None, None, None, 8, 4096, 128, 1 << 20,
+                                           1, None, None, ctypes.byref(n), None) == UNSUPPORTED
+    n = ctypes.c_size_t(10)
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1, FAKE,
+                                           FAKE, ctypes.byref(n), None) == WORKSPACE
+    n = ctypes.c_size_t(1 << 30)
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, None, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1, FAKE,
+                                           FAKE, ctypes.byref(n), None) == INVALID
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, ctypes.c_void_p(0x10002), 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128,
+                                           256, 128, 1, FAKE, FAKE, ctypes.byref(n), None) == INVALID
+    assert L.moe_grouped_swiglu_ffn_gather(MISALIGNED, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1,
+                                           FAKE, FAKE, ctypes.byref(n), None) == INVALID
+
+
 def test_combine_validation(L):
     assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, 4, 0, 128, 8, 1, FAKE, None) == INVALID
     assert L.moe_unpermute_combine(FAKE, FAKE, FAKE, 4, 2, 100, 8, 1, FAKE, None) == INVALID

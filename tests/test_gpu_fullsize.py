@@ -72,3 +72,13 @@ def test_fullsize(name, T, alpha):
     else:
         G.check_f32(got, ref["out"], f"{name} out rows")
     assert np.all(np.isfinite(G.down(g["out"]))), "unwritten out rows"
+    if bf16:
+        # the FFN reading the routed rows of x itself gives the same bits
+        fb = G.poison_bufs(T, k, li.shape.H, E, len(li.local), d["dtype"])
+        fb.pop("x_perm")
+        f = moe.moe_layer(d["x"], d["w_router"], d["bias"], k, li.expert_map, d["w_gate"], d["w_up"],
+                          d["w_down"], bufs=fb, fuse_gather=True)
+        torch.cuda.synchronize()
+        assert f["x_perm"] is None
+        assert torch.equal(f["y_perm"][:m], g["y_perm"][:m]), "fused gather: y_perm"
+        assert torch.equal(f["out"], g["out"]), "fused gather: out"
