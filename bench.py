@@ -124,7 +124,9 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(dtype).contiguous()
 
     x, wr, bias = up(li.x), up(li.w_router), up(li.bias, torch.float32)
-    wg, wu, wd = up(li.w_gate), up(li.w_up), up(li.w_down)
+    # expert weights in HBM with rows padded off multiples of 4 KiB
+    # (moe.weight_row_stride), the layout the FFN streams fastest
+    wg, wu, wd = (moe.pad_weight_rows(up(a)) for a in (li.w_gate, li.w_up, li.w_down))
     t_gen = time.time() - t_gen
     emap = li.expert_map
     E_local = len(li.local)
@@ -226,7 +228,8 @@ def main():
         "config": {"workload": f"{args.config}-shaped MoE layer, {E_local}/{E} experts local, top-{k}, "
                                f"T={T}, alpha={args.alpha:g}",
                    "T": T, "H": H, "I": I, "E": E, "k": k, "E_local": E_local, "alpha": args.alpha,
-                   "seed": args.seed, "M_loc": w["m_loc"], "active_local_experts": w["active"]},
+                   "seed": args.seed, "M_loc": w["m_loc"], "active_local_experts": w["active"],
+                   "weight_row_stride": {"gate_up": wg.stride(1), "down": wd.stride(1)}},
         "us_per_layer": round(us, 2),
         "layer_gbps": round(w["layer_bytes"] / (us * 1e-6) / 1e9, 1),
         "stages_us": {n: round(v, 2) for n, v in stage.items()},
@@ -272,7 +275,7 @@ def main():
         e_bytes = 3 * H * I * (2 if dt == torch.bfloat16 else 4)
         n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
         g1, u1, d1 = make_experts(shape, [int(li.local[0])], seed=args.seed)
-        rep = lambda a: up(a).repeat(n_rot, 1, 1).contiguous()
+        rep = lambda a: moe.pad_weight_rows(up(a).repeat(n_rot, 1, 1))
         xs = up(make_router(shape, max(SWEEP_MS), 0.0, seed=args.seed)[0])
         med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), SWEEP_MS, warmup=3, iters=args.sweep_iters)
         med = [float(v) for v in med]
@@ -317,7 +320,7 @@ def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps, key):
     of the bf16 layer): weights quantised once, outside the timing; x_perm
     quantisation and the FFN timed with HIP events on the current stream."""
     H, I = shape.H, shape.I
-    tg, tu, td = (moe.moe_mx_quantize(t) for t in (wg, wu, wd))
+    tg, tu, td = (moe.moe_mx_quantize(t.contiguous()) for t in (wg, wu, wd))
     torch.cuda.synchronize()
     out = []
     for Tb, a, bb, bf16_us in cases:
@@ -430,7 +433,7 @@ def placement_section(moe, seed):
     g1, u1, d1 = make_experts(shape, [0], seed=seed)
     e_bytes = 3 * shape.H * shape.I * 2
     n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
-    rep = lambda a: up(a).repeat(n_rot, 1, 1).contiguous()
+    rep = lambda a: moe.pad_weight_rows(up(a).repeat(n_rot, 1, 1))
     xs = up(make_router(shape, max(PLACE_SWEEP_MS), 0.0, seed=seed)[0])
     med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), PLACE_SWEEP_MS, warmup=3, iters=10)
     kn, kt = moe.moe_fit_latency_model(PLACE_SWEEP_MS, med)

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 1
+#define MOE_ABI_VERSION 2
 #define MOE_MAX_EXPERTS 256 /* E and E_local limit */
 #define MOE_MAX_TOPK 16
 
@@ -144,7 +144,14 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  * This is the expert computation whose latency per token load is f_g(n)
  * (Section 4.2.1). Experts with no rows cost nothing and are not read.
  *
- * w_gate, w_up [E_local, I, H] dt; w_down [E_local, H, I] dt
+ * w_gate, w_up [E_local, I, H] dt with row stride ldw_gu elements (expert
+ *              l's matrix starts at row l * I); w_down [E_local, H, I] dt with
+ *              row stride ldw_dn (expert l at row l * H). A stride of 0 means
+ *              dense (H, resp. I); otherwise it must be >= that, a multiple
+ *              of 16 bytes and <= 2^20 (else MOE_ERR_INVALID_ARG). Padding
+ *              the rows off a power of two (e.g. H + 64 for H = 4096) spreads
+ *              a weight tile's rows over more HBM channels; padding elements
+ *              are never read.
  * offsets      [E_local+1] int32 (device, from moe_expert_histogram_scan);
  *              clamped to [0, M_cap] inside the kernels
  * y_perm       [M_cap, H] dt, rows [0, offsets[E_local]) written
@@ -158,8 +165,8 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  */
 moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const void* w_up,
                                   const void* w_down, const int32_t* offsets, int E_local,
-                                  int H, int I, int M_cap, moe_dtype dt, void* y_perm,
-                                  void* ws, size_t* ws_bytes, hipStream_t stream);
+                                  int H, int I, int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt,
+                                  void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
  * moe_grouped_swiglu_ffn_gather - moe_grouped_swiglu_ffn with the dispatch
@@ -181,9 +188,9 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
  */
 moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src, int T, int k,
                                          const void* w_gate, const void* w_up, const void* w_down,
-                                         const int32_t* offsets, int E_local, int H, int I, int M_cap,
-                                         moe_dtype dt, void* y_perm, void* ws, size_t* ws_bytes,
-                                         hipStream_t stream);
+                                         const int32_t* offsets, int E_local, int H, int I,
+                                         int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt,
+                                         void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
  * moe_unpermute_combine - gather and weighted sum back to token order.
@@ -300,7 +307,8 @@ moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, cons
  * that the 256 MB last-level cache does not hold them between runs.
  *
  * x        [maxM, H] dt        input rows (maxM = max of Ms)
- * w_gate, w_up [n_rot, I, H]; w_down [n_rot, H, I]   dt
+ * w_gate, w_up [n_rot, I, H]; w_down [n_rot, H, I]   dt, rows strided by
+ *          ldw_gu and ldw_dn as in moe_grouped_swiglu_ffn (0: dense)
  * y_scratch [maxM, H] dt       output rows (contents unspecified afterwards)
  * ws       workspace for maxM (query with ws == NULL)
  * us_out   HOST [nM]: median microseconds per run
@@ -309,7 +317,8 @@ moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, cons
  * 1 <= Ms[i] <= 1 << 20, 0 <= warmup, 1 <= iters <= 10000, n_rot >= 1.
  */
 moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up,
-                          const void* w_down, int n_rot, int H, int I, moe_dtype dt,
+                          const void* w_down, int n_rot, int H, int I, int ldw_gu,
+                          int ldw_dn, moe_dtype dt,
                           const int32_t* Ms, int nM, int warmup, int iters,
                           void* y_scratch, void* ws, size_t* ws_bytes,
                           float* us_out, float* us_all, hipStream_t stream);

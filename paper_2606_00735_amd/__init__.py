@@ -39,4 +39,6 @@ from ._lib import (  # noqa: F401
     moe_placement_cost,
     moe_unpermute_combine,
     moe_window_push,
+    pad_weight_rows,
+    weight_row_stride,
 )

@@ -62,14 +62,14 @@ def load_library(path: str = LIB_PATH):
     L.moe_permute.restype = _I
     L.moe_permute.argtypes = [_P, _P, _P, _P, _SZ, _I, _I, _I, _I, _I, _I, _I, _P, _P, _P, _P]
     L.moe_grouped_swiglu_ffn.restype = _I
-    L.moe_grouped_swiglu_ffn.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _PSZ, _P]
+    L.moe_grouped_swiglu_ffn.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P, _PSZ, _P]
     L.moe_grouped_swiglu_ffn_gather.restype = _I
-    L.moe_grouped_swiglu_ffn_gather.argtypes = [_P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _PSZ,
-                                                _P]
+    L.moe_grouped_swiglu_ffn_gather.argtypes = [_P, _P, _I, _I, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P,
+                                                _PSZ, _P]
     L.moe_unpermute_combine.restype = _I
     L.moe_unpermute_combine.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P]
     L.moe_load_sweep.restype = _I
-    L.moe_load_sweep.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P, _P]
+    L.moe_load_sweep.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P, _P]
     _D = ctypes.c_double
     L.moe_fit_latency_model.restype = _I
     L.moe_fit_latency_model.argtypes = [_P, _P, _I, _P, _P]
@@ -94,7 +94,7 @@ def load_library(path: str = LIB_PATH):
                                     _P]
     L.moe_grouped_swiglu_ffn_mx.restype = _I
     L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _PSZ, _P]
-    if L.moe_abi_version() != 1:
+    if L.moe_abi_version() != 2:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
     return L
@@ -120,6 +120,23 @@ def _dev(t, name, dtype=None):
     if dtype is not None and t.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _wrows(t, name, dtype):
+    """A batch of weight matrices [B, R, K] whose rows may be padded: a view
+    with unit element stride, row stride ld >= K and matrix stride R * ld (as
+    the columns [:, :, :K] of a [B, R, ld] tensor). Returns (pointer, ld)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU (libmoe has no CPU path)")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    B, R, K = t.shape
+    ld = t.stride(1) if R > 1 else K
+    if t.stride(2) != 1 or ld < K or (B > 1 and t.stride(0) != R * ld):
+        raise ValueError(f"{name} must be [B, R, K] with unit element stride and rows {ld} apart")
+    return ctypes.c_void_p(t.data_ptr()), ld
 
 
 def _dtype_code(t):
@@ -223,10 +240,43 @@ def ffn_ws_bytes(E_local, H, I, M_cap, dtype):
     L = load_library()
     n = ctypes.c_size_t(0)
     dt = MOE_BF16 if dtype == torch.bfloat16 else MOE_F32
-    st = L.moe_grouped_swiglu_ffn(None, None, None, None, None, E_local, H, I, M_cap, dt, None, None,
+    st = L.moe_grouped_swiglu_ffn(None, None, None, None, None, E_local, H, I, 0, 0, M_cap, dt, None, None,
                                   ctypes.byref(n), None)
     _check("moe_grouped_swiglu_ffn", st)
     return n.value
+
+
+def weight_row_stride(K, elem_bytes=2):
+    """Row stride (elements) for expert weight rows of K elements: rows whose
+    byte length is a multiple of 4 KiB (H = 4096 or 2048 in bf16) put the
+    rows of a weight tile on the same few HBM channels, so they get 64
+    elements (128 bytes) of padding; other rows stay dense."""
+    return K + 64 if (K * elem_bytes) % 4096 == 0 else K
+
+
+def pad_weight_rows(w, ld=None):
+    """Copy of weights [B, R, K] whose rows are ``ld`` elements apart
+    (default ``weight_row_stride``), returned as the view [:, :, :K] of a
+    [B, R, ld] tensor; the FFN entry points take such views as they are.
+    The padding is zero-filled and never read."""
+    B, R, K = w.shape
+    ld = weight_row_stride(K, w.element_size()) if ld is None else ld
+    if ld == K:
+        return w.contiguous()
+    buf = torch.zeros((B, R, ld), dtype=w.dtype, device=w.device)
+    buf[:, :, :K] = w
+    return buf[:, :, :K]
+
+
+def _ffn_weights(w_gate, w_up, w_down, dtype):
+    """Pointers and row strides of the expert weights (w_gate and w_up must
+    share their row stride)."""
+    pg, ld_gu = _wrows(w_gate, "w_gate", dtype)
+    pu, ld_u = _wrows(w_up, "w_up", dtype)
+    pd, ld_dn = _wrows(w_down, "w_down", dtype)
+    if ld_u != ld_gu:
+        raise ValueError("w_gate and w_up must have the same row stride")
+    return pg, pu, pd, ld_gu, ld_dn
 
 
 def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):
@@ -244,9 +294,9 @@ def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_per
         ws = torch.empty(need, dtype=torch.uint8, device=x_perm.device)
     y_perm = torch.empty((M_cap, H), dtype=x_perm.dtype, device=x_perm.device) if y_perm is None else y_perm
     n = ctypes.c_size_t(ws.numel() * ws.element_size())
-    st = L.moe_grouped_swiglu_ffn(_dev(x_perm, "x_perm"), _dev(w_gate, "w_gate", x_perm.dtype),
-                                  _dev(w_up, "w_up", x_perm.dtype), _dev(w_down, "w_down", x_perm.dtype),
-                                  _dev(offsets, "offsets", torch.int32), E_local, H, I, M_cap, dt,
+    pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x_perm.dtype)
+    st = L.moe_grouped_swiglu_ffn(_dev(x_perm, "x_perm"), pg, pu, pd,
+                                  _dev(offsets, "offsets", torch.int32), E_local, H, I, ld_gu, ld_dn, M_cap, dt,
                                   _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ctypes.byref(n),
                                   _stream())
     _check("moe_grouped_swiglu_ffn", st)
@@ -271,11 +321,11 @@ def moe_grouped_swiglu_ffn_gather(x, perm_src, k, w_gate, w_up, w_down, offsets,
         ws = torch.empty(need, dtype=torch.uint8, device=x.device)
     y_perm = torch.empty((M_cap, H), dtype=x.dtype, device=x.device) if y_perm is None else y_perm
     n = ctypes.c_size_t(ws.numel() * ws.element_size())
+    pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x.dtype)
     st = L.moe_grouped_swiglu_ffn_gather(_dev(x, "x"), _dev(perm_src, "perm_src", torch.int32), T, k,
-                                         _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
-                                         _dev(w_down, "w_down", x.dtype), _dev(offsets, "offsets", torch.int32),
-                                         E_local, H, I, M_cap, dt, _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"),
-                                         ctypes.byref(n), _stream())
+                                         pg, pu, pd, _dev(offsets, "offsets", torch.int32),
+                                         E_local, H, I, ld_gu, ld_dn, M_cap, dt, _dev(y_perm, "y_perm", x.dtype),
+                                         _dev(ws, "ws"), ctypes.byref(n), _stream())
     _check("moe_grouped_swiglu_ffn_gather", st)
     return y_perm, ws
 
@@ -305,7 +355,7 @@ def moe_load_sweep(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=No
         raise ValueError("x must be [max(Ms), H]")
     dt = _dtype_code(x)
     n = ctypes.c_size_t(0)
-    st = L.moe_load_sweep(None, None, None, None, n_rot, H, I, dt, Ms.ctypes.data_as(ctypes.c_void_p), nM,
+    st = L.moe_load_sweep(None, None, None, None, n_rot, H, I, 0, 0, dt, Ms.ctypes.data_as(ctypes.c_void_p), nM,
                           warmup, iters, None, None, ctypes.byref(n), None, None, None)
     _check("moe_load_sweep", st)
     if ws is None:
@@ -315,9 +365,9 @@ def moe_load_sweep(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=No
     us = np.zeros(nM, np.float32)
     us_all = np.zeros((nM, iters), np.float32) if keep_all else None
     n = ctypes.c_size_t(ws.numel())
-    st = L.moe_load_sweep(_dev(x, "x"), _dev(w_gate, "w_gate", x.dtype), _dev(w_up, "w_up", x.dtype),
-                          _dev(w_down, "w_down", x.dtype), n_rot, H, I, dt, Ms.ctypes.data_as(ctypes.c_void_p),
-                          nM, warmup, iters, _dev(y_scratch, "y_scratch", x.dtype), _dev(ws, "ws"),
+    pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x.dtype)
+    st = L.moe_load_sweep(_dev(x, "x"), pg, pu, pd, n_rot, H, I, ld_gu, ld_dn, dt,
+                          Ms.ctypes.data_as(ctypes.c_void_p), nM, warmup, iters, _dev(y_scratch, "y_scratch", x.dtype), _dev(ws, "ws"),
                           ctypes.byref(n), us.ctypes.data_as(ctypes.c_void_p),
                           us_all.ctypes.data_as(ctypes.c_void_p) if keep_all else None, _stream())
     _check("moe_load_sweep", st)

@@ -80,6 +80,10 @@ struct GemmArgs {
   // directly instead of a permuted copy.
   const int32_t* a_src;
   int a_div, a_T;
+  // Row stride of B0/B1 in the units of K (elements for bf16, bytes for
+  // MXFP8 codes), >= K; expert e's matrix starts at row e * N. A stride off
+  // a power of two spreads a tile's rows over more HBM channels.
+  int ldb;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -155,8 +159,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   const bool gather = a.a_src != nullptr;
   const bf16_t* A = gather ? a.A : a.A + (size_t)m0 * K;
   const int a_rows = m_end - m0;
-  const bf16_t* B0 = a.B0 + ((size_t)e * N + n0) * K;
-  const bf16_t* B1 = DUAL ? a.B1 + ((size_t)e * N + n0) * K : nullptr;
+  const int LDB = a.ldb;
+  const bf16_t* B0 = a.B0 + ((size_t)e * N + n0) * LDB;
+  const bf16_t* B1 = DUAL ? a.B1 + ((size_t)e * N + n0) * LDB : nullptr;
 
   f32x16_t acc[NB][MI][NI];
 #pragma unroll
@@ -185,7 +190,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
 #pragma unroll
   for (int t = 0; t < LB; ++t) {
     const int r = (t * kWaves + wave) * RPI + lane / 8;
-    offB[t] = (uint32_t)(r * K * 2 + swz_chunk<kBK>(r, lane % 8) * 16);
+    offB[t] = (uint32_t)(r * LDB * 2 + swz_chunk<kBK>(r, lane % 8) * 16);
   }
   if (kc1 < 0) kc1 = K / kBK;
   auto issue = [&](int kc, bool live, bf16_t* st) {
@@ -324,8 +329,9 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
   const int K = a.K, N = a.N, nK = K / kMxChunk;  // K: bytes of an operand row
   const int a_rows = m_end - m0;
   const char* A = reinterpret_cast<const char*>(a.A) + (size_t)m0 * K;
-  const char* B0 = reinterpret_cast<const char*>(a.B0) + ((size_t)e * N + n0) * K;
-  const char* B1 = DUAL ? reinterpret_cast<const char*>(a.B1) + ((size_t)e * N + n0) * K : nullptr;
+  const int LDB = a.ldb;  // bytes
+  const char* B0 = reinterpret_cast<const char*>(a.B0) + ((size_t)e * N + n0) * LDB;
+  const char* B1 = DUAL ? reinterpret_cast<const char*>(a.B1) + ((size_t)e * N + n0) * LDB : nullptr;
 
   // Loop-invariant byte offsets of this lane's 16-byte pieces, as in
   // gemm_tile (the rows of a chunk are 128 codes here).
@@ -340,7 +346,7 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
 #pragma unroll
   for (int t = 0; t < LB; ++t) {
     const int r = (t * kWaves + wave) * RPI + lane / 8;
-    offB[t] = (uint32_t)(r * K + swz_chunk<kBK>(r, lane % 8) * 16);
+    offB[t] = (uint32_t)(r * LDB + swz_chunk<kBK>(r, lane % 8) * 16);
   }
   // Scale rows: wave w loads scale rows [64 w, 64 w + 64) of the stage, all
   // in one operand (AR and BN are multiples of 64): A rows (clamped), the
@@ -1005,15 +1011,15 @@ __device__ __forceinline__ int find_slot(const int32_t* offsets, int E, int M_ca
 __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict__ X, const float* __restrict__ Wg,
                                                          const float* __restrict__ Wu,
                                                          const int32_t* __restrict__ offsets, int E, int M_cap,
-                                                         int H, int I, float* __restrict__ h) {
+                                                         int H, int I, int ldw, float* __restrict__ h) {
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (size_t)M_cap * I) return;
   const int row = (int)(idx / I), i = (int)(idx % I);
   const int e = find_slot(offsets, E, M_cap, row);
   if (e < 0) return;
   const float* x = X + (size_t)row * H;
-  const float* wg = Wg + ((size_t)e * I + i) * H;
-  const float* wu = Wu + ((size_t)e * I + i) * H;
+  const float* wg = Wg + ((size_t)e * I + i) * ldw;
+  const float* wu = Wu + ((size_t)e * I + i) * ldw;
   float g = 0.0f, u = 0.0f;
   for (int c = 0; c < H; ++c) {
     g = __builtin_fmaf(x[c], wg[c], g);
@@ -1024,14 +1030,14 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(const float* __restrict
 
 __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__ h, const float* __restrict__ Wd,
                                                        const int32_t* __restrict__ offsets, int E, int M_cap, int H,
-                                                       int I, float* __restrict__ y) {
+                                                       int I, int ldw, float* __restrict__ y) {
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (size_t)M_cap * H) return;
   const int row = (int)(idx / H), c = (int)(idx % H);
   const int e = find_slot(offsets, E, M_cap, row);
   if (e < 0) return;
   const float* hr = h + (size_t)row * I;
-  const float* wd = Wd + ((size_t)e * H + c) * I;
+  const float* wd = Wd + ((size_t)e * H + c) * ldw;
   float s = 0.0f;
   for (int i = 0; i < I; ++i) s = __builtin_fmaf(hr[i], wd[i], s);
   y[(size_t)row * H + c] = s;
@@ -1102,8 +1108,8 @@ static int device_cu_count() {
 }
 
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
-                      const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
-                      void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T) {
+                      const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
+                      void* y_perm, void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
   const FfnWs L = ffn_ws_layout(M_cap, E_local, H, I, bf16);
   char* wsb = static_cast<char*>(ws);
@@ -1112,12 +1118,12 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
     const size_t n1 = (size_t)M_cap * I, n2 = (size_t)M_cap * H;
     gateup_f32_kernel<<<(unsigned)((n1 + 255) / 256), 256, 0, s>>>(
         static_cast<const float*>(x_perm), static_cast<const float*>(w_gate), static_cast<const float*>(w_up),
-        offsets, E_local, M_cap, H, I, static_cast<float*>(h));
+        offsets, E_local, M_cap, H, I, ld_gu, static_cast<float*>(h));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     down_f32_kernel<<<(unsigned)((n2 + 255) / 256), 256, 0, s>>>(static_cast<const float*>(h),
                                                                   static_cast<const float*>(w_down), offsets,
-                                                                  E_local, M_cap, H, I,
+                                                                  E_local, M_cap, H, I, ld_dn,
                                                                   static_cast<float*>(y_perm));
     return hipGetLastError();
   }
@@ -1150,6 +1156,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   g1.a_src = a_src;
   g1.a_div = a_div;
   g1.a_T = a_T;
+  g1.ldb = ld_gu;
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1163,6 +1170,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan, L.plan_rows};
   g2.queue = queue + 8;
+  g2.ldb = ld_dn;
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1234,6 +1242,7 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   g.M_cap = M_cap;
   g.N = I;
   g.K = H;
+  g.ldb = H;
   g.part = sp.part;
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;
@@ -1264,6 +1273,7 @@ static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
   g.M_cap = M_cap;
   g.N = N;
   g.K = K;
+  g.ldb = K;
   g.part = sp.part;
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;

@@ -26,8 +26,9 @@ size_t ffn_ws_bytes(int M_cap, int E_local, int H, int I, bool bf16);
 // a_src != nullptr (bf16 only): the gate/up GEMM's row m is row
 // a_src[m] / a_div of x_perm, which then holds a_T rows (see GemmArgs).
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
-                      const int32_t* offsets, int E_local, int H, int I, int M_cap, bool bf16, void* y_perm,
-                      void* ws, hipStream_t s, const int32_t* a_src = nullptr, int a_div = 1, int a_T = 0);
+                      const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
+                      void* y_perm, void* ws, hipStream_t s, const int32_t* a_src = nullptr, int a_div = 1,
+                      int a_T = 0);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
 hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, const int32_t* row_count,

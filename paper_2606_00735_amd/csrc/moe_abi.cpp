@@ -66,6 +66,17 @@ moe_status ffn_shape_ok(int E_local, int H, int I, int M_cap, moe_dtype dt) {
   return MOE_OK;
 }
 
+// Row stride of an expert weight matrix whose rows hold K elements: 0 means
+// K (dense); otherwise at least K, a whole number of 16-byte pieces and small
+// enough that 256 rows span less than 2^31 bytes (32-bit lane offsets).
+moe_status resolve_ld(int ld, int K, moe_dtype dt, int* out) {
+  if (ld == 0) ld = K;
+  const int per16 = dt == MOE_BF16 ? 8 : 4;
+  if (ld < K || ld % per16 != 0 || ld > (1 << 20)) return MOE_ERR_INVALID_ARG;
+  *out = ld;
+  return MOE_OK;
+}
+
 // The timing loop shared by the load sweeps: for each M of Ms, sets
 // offsets = [0, M], then runs `run(rot, M)` warmup + iters times rotating
 // through n_rot weight copies, each timed run bracketed by HIP events.
@@ -220,10 +231,14 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
 }
 
 moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
-                                  const int32_t* offsets, int E_local, int H, int I, int M_cap, moe_dtype dt,
-                                  void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream) {
+                                  const int32_t* offsets, int E_local, int H, int I, int ldw_gu, int ldw_dn,
+                                  int M_cap, moe_dtype dt, void* y_perm, void* ws, size_t* ws_bytes,
+                                  hipStream_t stream) {
   moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
   if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld(ldw_gu, H, dt, &ld_gu)) != MOE_OK || (st = resolve_ld(ldw_dn, I, dt, &ld_dn)) != MOE_OK)
+    return st;
   if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
   const size_t need = moe::ffn_ws_bytes(M_cap, E_local, H, I, dt == MOE_BF16);
   if (ws == nullptr) {
@@ -236,16 +251,19 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
   if (!aligned16(x_perm) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_perm) ||
       !aligned16(ws) || !aligned4(offsets))
     return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_ffn(x_perm, w_gate, w_up, w_down, offsets, E_local, H, I, M_cap,
+  return hip_status(moe::launch_ffn(x_perm, w_gate, w_up, w_down, offsets, E_local, H, I, ld_gu, ld_dn, M_cap,
                                     dt == MOE_BF16, y_perm, ws, stream));
 }
 
 moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src, int T, int k, const void* w_gate,
                                          const void* w_up, const void* w_down, const int32_t* offsets, int E_local,
-                                         int H, int I, int M_cap, moe_dtype dt, void* y_perm, void* ws,
-                                         size_t* ws_bytes, hipStream_t stream) {
+                                         int H, int I, int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt,
+                                         void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream) {
   moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
   if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld(ldw_gu, H, dt, &ld_gu)) != MOE_OK || (st = resolve_ld(ldw_dn, I, dt, &ld_dn)) != MOE_OK)
+    return st;
   if (ws_bytes == nullptr || T < 1 || k < 1 || k > MOE_MAX_TOPK) return MOE_ERR_INVALID_ARG;
   if (dt != MOE_BF16) return MOE_ERR_UNSUPPORTED;
   // row offsets into x are 32-bit byte offsets
@@ -261,8 +279,8 @@ moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src,
   if (!aligned16(x) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_perm) ||
       !aligned16(ws) || !aligned4(offsets) || !aligned4(perm_src))
     return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_ffn(x, w_gate, w_up, w_down, offsets, E_local, H, I, M_cap, true, y_perm, ws,
-                                    stream, perm_src, k, T));
+  return hip_status(moe::launch_ffn(x, w_gate, w_up, w_down, offsets, E_local, H, I, ld_gu, ld_dn, M_cap, true,
+                                    y_perm, ws, stream, perm_src, k, T));
 }
 
 moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const int32_t* dest, int T, int k,
@@ -278,7 +296,8 @@ moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const 
 }
 
 moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, const void* w_down, int n_rot,
-                          int H, int I, moe_dtype dt, const int32_t* Ms, int nM, int warmup, int iters,
+                          int H, int I, int ldw_gu, int ldw_dn, moe_dtype dt, const int32_t* Ms, int nM,
+                          int warmup, int iters,
                           void* y_scratch, void* ws, size_t* ws_bytes, float* us_out, float* us_all,
                           hipStream_t stream) {
   if (Ms == nullptr || nM < 1 || nM > 64 || warmup < 0 || iters < 1 || iters > 10000 || n_rot < 1 ||
@@ -291,6 +310,9 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
   }
   moe_status st = ffn_shape_ok(1, H, I, max_m, dt);
   if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld(ldw_gu, H, dt, &ld_gu)) != MOE_OK || (st = resolve_ld(ldw_dn, I, dt, &ld_dn)) != MOE_OK)
+    return st;
   const bool bf16 = dt == MOE_BF16;
   const size_t ffn_ws = moe::ffn_ws_bytes(max_m, 1, H, I, bf16);
   const size_t need = ffn_ws + 256;
@@ -305,13 +327,13 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
     return MOE_ERR_INVALID_ARG;
 
   const size_t es = bf16 ? 2 : 4;
-  const size_t wmat = (size_t)H * I * es;  // bytes of one expert matrix
+  const size_t wgu = (size_t)I * ld_gu * es, wdn = (size_t)H * ld_dn * es;  // bytes of one copy
   int32_t* offsets = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + ffn_ws);
   return sweep_loop(Ms, nM, warmup, iters, n_rot, offsets, us_out, us_all, stream, [&](int rot, int m) {
-    const char* g = static_cast<const char*>(w_gate) + (size_t)rot * wmat;
-    const char* u = static_cast<const char*>(w_up) + (size_t)rot * wmat;
-    const char* d = static_cast<const char*>(w_down) + (size_t)rot * wmat;
-    return moe::launch_ffn(x, g, u, d, offsets, 1, H, I, m, bf16, y_scratch, ws, stream);
+    const char* g = static_cast<const char*>(w_gate) + (size_t)rot * wgu;
+    const char* u = static_cast<const char*>(w_up) + (size_t)rot * wgu;
+    const char* d = static_cast<const char*>(w_down) + (size_t)rot * wdn;
+    return moe::launch_ffn(x, g, u, d, offsets, 1, H, I, ld_gu, ld_dn, m, bf16, y_scratch, ws, stream);
   });
 }
 

@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.moe_abi_version() == 1
+    assert L.moe_abi_version() == 2
     assert L.moe_status_string(0) == b"ok"
     assert L.moe_status_string(3) == b"workspace too small"
     assert L.moe_status_string(99) == b"unknown status"
@@ -126,45 +126,70 @@ def test_permute_validation(L):
 
 def test_ffn_validation_and_query(L):
     n = ctypes.c_size_t(0)
-    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 4096, 14336, 8192, 1, None, None,
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 4096, 14336, 0, 0, 8192, 1, None, None,
                                     ctypes.byref(n), None) == 0
     assert n.value >= 8192 * 14336 * 2
     for H, I in ((4096, 14300), (4000, 14336)):
-        assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, H, I, 64, 1, None, None,
+        assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, H, I, 0, 0, 64, 1, None, None,
                                         ctypes.byref(n), None) == UNSUPPORTED
-    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 300, 128, 128, 64, 1, None, None,
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 300, 128, 128, 0, 0, 64, 1, None, None,
                                     ctypes.byref(n), None) == UNSUPPORTED
     n = ctypes.c_size_t(10)
-    assert L.moe_grouped_swiglu_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 64, 1, FAKE, FAKE,
+    assert L.moe_grouped_swiglu_ffn(FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 0, 0, 64, 1, FAKE, FAKE,
                                     ctypes.byref(n), None) == WORKSPACE
+
+
+def test_ffn_weight_row_strides(L):
+    # padded rows: accepted (and the workspace does not depend on them)
+    n, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 4096, 14336, 0, 0, 64, 1, None, None,
+                                    ctypes.byref(n), None) == 0
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 4096, 14336, 4160, 14344, 64, 1, None, None,
+                                    ctypes.byref(m), None) == 0
+    assert n.value == m.value
+    # fp32: a multiple of 4 elements; bf16: of 8 (16-byte rows)
+    assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, 128, 256, 132, 260, 64, 0, None, None,
+                                    ctypes.byref(m), None) == 0
+    for gu, dn, dt in ((4095, 0, 1), (4100, 0, 1), (0, 14337, 1), (0, 14340, 1), (130, 0, 0), (4097, 0, 1),
+                       (1 << 21, 0, 1), (-8, 0, 1)):
+        H, I = (4096, 14336) if dt == 1 else (128, 256)
+        assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, 8, H, I, gu, dn, 64, dt, None, None,
+                                        ctypes.byref(m), None) == INVALID, (gu, dn, dt)
+        assert L.moe_grouped_swiglu_ffn_gather(None, None, 64, 2, None, None, None, None, 8, H, I, gu, dn, 64, 1,
+                                               None, None, ctypes.byref(m), None) in (INVALID, UNSUPPORTED)
+    Ms = np.array([1, 2], np.int32)
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 2056, 776, 1, Ms.ctypes.data_as(ctypes.c_void_p),
+                            2, 1, 5, None, None, ctypes.byref(m), None, None, None) == 0
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 2047, 0, 1, Ms.ctypes.data_as(ctypes.c_void_p),
+                            2, 1, 5, None, None, ctypes.byref(m), None, None, None) == INVALID
 
 
 def test_ffn_gather_validation_and_query(L):
     n, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
-    args = (8, 4096, 14336, 8192)
+    args = (8, 4096, 14336, 0, 0, 8192)
     assert L.moe_grouped_swiglu_ffn_gather(None, None, 4096, 2, None, None, None, None, *args, 1, None, None,
                                            ctypes.byref(n), None) == 0
     assert L.moe_grouped_swiglu_ffn(None, None, None, None, None, *args, 1, None, None, ctypes.byref(m), None) == 0
     assert n.value == m.value  # the same workspace
     # fp32 has no gathering variant
-    assert L.moe_grouped_swiglu_ffn_gather(None, None, 64, 2, None, None, None, None, 8, 128, 128, 128, 0, None,
-                                           None, ctypes.byref(n), None) == UNSUPPORTED
+    assert L.moe_grouped_swiglu_ffn_gather(None, None, 64, 2, None, None, None, None, 8, 128, 128, 0, 0, 128, 0,
+                                           None, None, ctypes.byref(n), None) == UNSUPPORTED
     for T, k in ((0, 2), (64, 0), (64, 17)):
-        assert L.moe_grouped_swiglu_ffn_gather(None, None, T, k, None, None, None, None, 8, 128, 128, 128, 1,
-                                               None, None, ctypes.byref(n), None) == INVALID
+        assert L.moe_grouped_swiglu_ffn_gather(None, None, T, k, None, None, None, None, 8, 128, 128, 0, 0, 128,
+                                               1, None, None, ctypes.byref(n), None) == INVALID
     # row offsets into x must fit 32 bits
-    assert L.moe_grouped_swiglu_ffn_gather(None, None, 1 << 20, 1, None, None, None, None, 8, 4096, 128, 1 << 20,
-                                           1, None, None, ctypes.byref(n), None) == UNSUPPORTED
+    assert L.moe_grouped_swiglu_ffn_gather(None, None, 1 << 20, 1, None, None, None, None, 8, 4096, 128, 0, 0,
+                                           1 << 20, 1, None, None, ctypes.byref(n), None) == UNSUPPORTED
     n = ctypes.c_size_t(10)
-    assert L.moe_grouped_swiglu_ffn_gather(FAKE, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1, FAKE,
-                                           FAKE, ctypes.byref(n), None) == WORKSPACE
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 0, 0, 128, 1,
+                                           FAKE, FAKE, ctypes.byref(n), None) == WORKSPACE
     n = ctypes.c_size_t(1 << 30)
-    assert L.moe_grouped_swiglu_ffn_gather(FAKE, None, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1, FAKE,
-                                           FAKE, ctypes.byref(n), None) == INVALID
-    assert L.moe_grouped_swiglu_ffn_gather(FAKE, ctypes.c_void_p(0x10002), 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128,
-                                           256, 128, 1, FAKE, FAKE, ctypes.byref(n), None) == INVALID
-    assert L.moe_grouped_swiglu_ffn_gather(MISALIGNED, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 128, 1,
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, None, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 0, 0, 128, 1,
                                            FAKE, FAKE, ctypes.byref(n), None) == INVALID
+    assert L.moe_grouped_swiglu_ffn_gather(FAKE, ctypes.c_void_p(0x10002), 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128,
+                                           256, 0, 0, 128, 1, FAKE, FAKE, ctypes.byref(n), None) == INVALID
+    assert L.moe_grouped_swiglu_ffn_gather(MISALIGNED, FAKE, 64, 2, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 0, 0, 128,
+                                           1, FAKE, FAKE, ctypes.byref(n), None) == INVALID
 
 
 def test_combine_validation(L):
@@ -178,13 +203,13 @@ def test_sweep_validation(L):
     Ms = np.array([1, 2, 4], np.int32)
     p = Ms.ctypes.data_as(ctypes.c_void_p)
     n = ctypes.c_size_t(0)
-    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 1, p, 3, 1, 5, None, None,
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 0, 0, 1, p, 3, 1, 5, None, None,
                             ctypes.byref(n), None, None, None) == 0
     assert n.value >= 4 * 768 * 2
     bad = np.array([1, 0], np.int32)
-    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 1, bad.ctypes.data_as(ctypes.c_void_p), 2,
-                            1, 5, None, None, ctypes.byref(n), None, None, None) == INVALID
-    assert L.moe_load_sweep(None, None, None, None, 0, 2048, 768, 1, p, 3, 1, 5, None, None,
+    assert L.moe_load_sweep(None, None, None, None, 1, 2048, 768, 0, 0, 1, bad.ctypes.data_as(ctypes.c_void_p),
+                            2, 1, 5, None, None, ctypes.byref(n), None, None, None) == INVALID
+    assert L.moe_load_sweep(None, None, None, None, 0, 2048, 768, 0, 0, 1, p, 3, 1, 5, None, None,
                             ctypes.byref(n), None, None, None) == INVALID
 
 

@@ -451,3 +451,83 @@ def test_load_sweep_output_and_timing():
     assert np.all(us > 0) and allus.shape == (5, 5)
     _, yref = O.swiglu_rows(x, wg[0], wu[0], wd[0], bf16=True)
     G.check_bf16(G.down(y), yref, "sweep y")
+
+
+def _padded(w, pad, dtype):
+    """Device copy of weights [B, R, K] as the columns [:, :, :K] of a
+    [B, R, K + pad] buffer whose padding holds NaN (read, it would poison
+    the outputs)."""
+    B, R, K = w.shape
+    buf = torch.full((B, R, K + pad), float("nan"), dtype=dtype, device="cuda")
+    buf[:, :, :K] = G.up(w, dtype)
+    return buf[:, :, :K]
+
+
+PAD_CASES = [
+    # (H, I, rows per expert, pad of W_gate/W_up rows, pad of W_down rows, dtype)
+    (1024, 2048, [1, 64, 0, 30], 64, 8, "bf16"),              # split-K in both GEMMs
+    (1024, 1024, [257, 300, 321, 576, 1], 64, 64, "bf16"),    # every tile class, ragged tails
+    (2048, 2048, [4608], 128, 8, "bf16"),                     # unsplit gate/up with a tail split
+    (128, 256, [3, 40, 0, 77], 4, 12, "f32"),
+]
+
+
+@pytest.mark.parametrize("H,I,rows,pg,pd,dt", PAD_CASES, ids=["split", "ragged", "tail", "f32"])
+def test_ffn_padded_weight_rows(H, I, rows, pg, pd, dt):
+    """Weights whose rows are padded (row stride H + pg, I + pd) give the
+    dense call's results bit for bit, through the permuted and the gathering
+    FFN, and never read the padding."""
+    banner("stage ffn padded rows", H, I, rows, pg, pd, dt, "seed 9")
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    k = 2
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="pad", H=H, I=I, E=len(rows), k=k, E_local=len(rows))
+    wg, wu, wd = make_experts(shape, list(range(len(rows))), seed=9)
+    m = sum(rows)
+    T = m
+    x, *_ = make_router(shape, T, 0.0, seed=9)
+    M_cap = m + 3
+    rng = np.random.default_rng(9)
+    perm_src = np.full(M_cap, -1, np.int32)
+    perm_src[:m] = rng.choice(T * k, size=m, replace=False)
+    offsets = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+    xr = x[perm_src[:m] // k]
+    xp = np.zeros((M_cap, H), np.float32)
+    xp[:m] = xr
+    dxp, doff = G.up(xp, tdt), G.up_i32(offsets)
+    dense = [G.up(w, tdt) for w in (wg, wu, wd)]
+    padded = [_padded(wg, pg, tdt), _padded(wu, pg, tdt), _padded(wd, pd, tdt)]
+    assert padded[0].stride(1) == H + pg and padded[2].stride(1) == I + pd
+    y1, _ = moe.moe_grouped_swiglu_ffn(dxp, *dense, doff)
+    y2, ws2 = moe.moe_grouped_swiglu_ffn(dxp, *padded, doff)
+    torch.cuda.synchronize()
+    assert torch.equal(y2[:m], y1[:m])
+    h_ref, y_ref = O.grouped_swiglu_ffn(xr, wg, wu, wd, offsets, bf16=dt == "bf16")
+    if dt == "bf16":
+        G.check_bf16(G.down(y2)[:m], y_ref, "padded y", scale=G.down_scale(h_ref, wd, offsets))
+        dx, dps = G.up(x, tdt), G.up_i32(perm_src)
+        y3, _ = moe.moe_grouped_swiglu_ffn_gather(dx, dps, k, *padded, doff)
+        torch.cuda.synchronize()
+        assert torch.equal(y3[:m], y1[:m])
+    else:
+        G.check_f32(G.down(y2)[:m], y_ref, "padded y")
+
+
+def test_load_sweep_padded_weight_rows():
+    """The sweep over weight copies with padded rows leaves the same y as
+    over dense copies."""
+    banner("sweep qwen3 expert padded rows")
+    shape = CONFIGS["qwen3"]
+    wg, wu, wd = make_experts(shape, [5], seed=0)
+    x, *_ = make_router(shape, 96, 0.0, seed=0)
+    rot = 3
+    dx = G.up(x, torch.bfloat16)
+    ys = []
+    for pad in (0, 64):
+        w = [_padded(np.repeat(a, rot, 0), pad, torch.bfloat16) for a in (wg, wu, wd)]
+        y = torch.full((96, shape.H), float("nan"), dtype=torch.bfloat16, device="cuda")
+        moe.moe_load_sweep(dx, *w, [1, 96], warmup=1, iters=2, y_scratch=y)
+        ys.append(y)
+    torch.cuda.synchronize()
+    assert torch.equal(ys[0], ys[1])
+    _, yref = O.swiglu_rows(x, wg[0], wu[0], wd[0], bf16=True)
+    G.check_bf16(G.down(ys[1]), yref, "padded sweep y")
