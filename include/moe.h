@@ -230,7 +230,11 @@ moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const 
  *                        row r for elements [128 k, 128 k + 128), byte b
  *                        (little-endian) for elements [128 k + 32 b, +32)
  * A batch of B such matrices (expert weights) is codes [B, R, K] and scales
- * [B, K/128, R].
+ * [B, K/128, R]. Weight codes may have padded rows: row r of matrix b at
+ * byte (b * R + r) * ld, with ld >= K a multiple of 16 and <= 2^20 (0 means
+ * ld = K); padding bytes are never read. Rows a multiple of 4 KiB long
+ * (K = 4096) stream faster from HBM with 128 bytes of padding.
+ * Activation codes (x, h, a) are always dense.
  */
 
 /*
@@ -241,13 +245,14 @@ moe_status moe_unpermute_combine(const void* y_perm, const float* topk_w, const 
  *           [0, min(rows, *row_count)) only, e.g. the routed rows of x_perm
  *           with row_count = offsets + E_local, without a host sync; the
  *           other rows' codes and scales are left untouched
- * codes     [batch, rows, K] uint8
+ * codes     [batch, rows, K] uint8, rows ld_codes bytes apart (0: dense;
+ *           otherwise as padded weight rows above, else MOE_ERR_INVALID_ARG)
  * scales    [batch, K/128, rows] uint32
  * Limits: K % 128 == 0; batch * rows * K <= 2^40.
  */
 moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K,
-                           const int32_t* row_count, uint8_t* codes, uint32_t* scales,
-                           hipStream_t stream);
+                           int ld_codes, const int32_t* row_count, uint8_t* codes,
+                           uint32_t* scales, hipStream_t stream);
 
 /*
  * moe_grouped_swiglu_mx - the gate/up half of the MXFP8 expert FFN.
@@ -258,32 +263,35 @@ moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int
  *                                        fp32 accumulation)
  *   h = silu(G) * U                      (fp32)
  *   (hq, hs)[R] = MXFP8 quantisation of h along I (rules above)
- * xq [M_cap, H], xs [H/128, M_cap]; wgq, wuq [E_local, I, H],
- * wgs, wus [E_local, H/128, I]; hq [M_cap, I], hs [I/128, M_cap]: rows R of
- * every local expert written, the rest untouched.
+ * xq [M_cap, H], xs [H/128, M_cap]; wgq, wuq [E_local, I, H] (code rows ldw
+ * bytes apart, 0: dense), wgs, wus [E_local, H/128, I]; hq [M_cap, I],
+ * hs [I/128, M_cap]: rows R of every local expert written, the rest
+ * untouched.
  * Limits: 0 <= E_local <= 256; H % 128 == 0, I % 128 == 0; H, I <= 2^20.
  */
 moe_status moe_grouped_swiglu_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                                  const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
-                                 const int32_t* offsets, int E_local, int H, int I, int M_cap,
-                                 uint8_t* hq, uint32_t* hs, hipStream_t stream);
+                                 const int32_t* offsets, int E_local, int H, int I, int ldw,
+                                 int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t stream);
 
 /*
  * moe_grouped_gemm_mx - grouped MXFP8 GEMM with bf16 output: for local slot l,
  * c[R] = bf16( A[R] B[l]^T ) (fp32 accumulation), R as above.
- * aq [M_cap, K], as [K/128, M_cap]; bq [E_local, N, K], bs [E_local, K/128, N];
- * c [M_cap, N] bf16, rows R written. The down projection of the MXFP8 FFN.
+ * aq [M_cap, K], as [K/128, M_cap]; bq [E_local, N, K] (code rows ldb bytes
+ * apart, 0: dense), bs [E_local, K/128, N]; c [M_cap, N] bf16, rows R
+ * written. The down projection of the MXFP8 FFN.
  * Limits: 0 <= E_local <= 256; N % 128 == 0, K % 128 == 0; N, K <= 2^20.
  */
 moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq,
                                const uint32_t* bs, const int32_t* offsets, int E_local, int N,
-                               int K, int M_cap, void* c, hipStream_t stream);
+                               int K, int ldb, int M_cap, void* c, hipStream_t stream);
 
 /*
  * moe_grouped_swiglu_ffn_mx - the MXFP8 expert FFN (the FP8 counterpart of
  * moe_grouped_swiglu_ffn): moe_grouped_swiglu_mx into the workspace, then
  * moe_grouped_gemm_mx with W_down (wdq [E_local, H, I], wds
- * [E_local, I/128, H]) into y_perm [M_cap, H] bf16.
+ * [E_local, I/128, H]) into y_perm [M_cap, H] bf16. Weight code rows are
+ * ldw_gu (W_gate, W_up) and ldw_dn (W_down) bytes apart (0: dense).
  * ws holds h codes [M_cap, I] at offset 0 and their scales [I/128, M_cap]
  * at offset M_cap * I rounded up to 256 bytes, then the fp32 partial sums
  * of split-K tiles (used as in moe_grouped_swiglu_ffn; summed in a fixed
@@ -293,8 +301,9 @@ moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint
 moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                                      const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
                                      const uint8_t* wdq, const uint32_t* wds,
-                                     const int32_t* offsets, int E_local, int H, int I, int M_cap,
-                                     void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream);
+                                     const int32_t* offsets, int E_local, int H, int I,
+                                     int ldw_gu, int ldw_dn, int M_cap, void* y_perm, void* ws,
+                                     size_t* ws_bytes, hipStream_t stream);
 
 /*
  * moe_load_sweep - per-expert latency versus token load.
@@ -330,14 +339,15 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up,
  *
  * xq [maxM, H], xs [H/128, maxM]   MXFP8 input rows (maxM = max of Ms)
  * wgq, wuq [n_rot, I, H], wgs, wus [n_rot, H/128, I];
- * wdq [n_rot, H, I], wds [n_rot, I/128, H]   MXFP8 weight copies
+ * wdq [n_rot, H, I], wds [n_rot, I/128, H]   MXFP8 weight copies, code rows
+ *          ldw_gu / ldw_dn bytes apart (0: dense)
  * y_scratch [maxM, H] bf16; ws, us_out, us_all and limits as moe_load_sweep;
  * H % 128 == 0, I % 128 == 0.
  */
 moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                              const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,
                              const uint8_t* wdq, const uint32_t* wds, int n_rot, int H, int I,
-                             const int32_t* Ms, int nM, int warmup, int iters, void* y_scratch,
+                             int ldw_gu, int ldw_dn, const int32_t* Ms, int nM, int warmup, int iters, void* y_scratch,
                              void* ws, size_t* ws_bytes, float* us_out, float* us_all,
                              hipStream_t stream);
 

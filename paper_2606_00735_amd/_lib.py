@@ -84,16 +84,17 @@ def load_library(path: str = LIB_PATH):
     L.moe_drift_distance.restype = _I
     L.moe_drift_distance.argtypes = [_P, _P, _I, _I, _D, _P, _P, _P]
     L.moe_mx_quantize.restype = _I
-    L.moe_mx_quantize.argtypes = [_P, _I, _I, _I, _I, _P, _P, _P, _P]
+    L.moe_mx_quantize.argtypes = [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P]
     L.moe_grouped_swiglu_mx.restype = _I
-    L.moe_grouped_swiglu_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _P]
+    L.moe_grouped_swiglu_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P]
     L.moe_grouped_gemm_mx.restype = _I
-    L.moe_grouped_gemm_mx.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P]
+    L.moe_grouped_gemm_mx.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _P]
     L.moe_load_sweep_mx.restype = _I
-    L.moe_load_sweep_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ, _P, _P,
-                                    _P]
+    L.moe_load_sweep_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _P, _I, _I, _I, _P, _P, _PSZ,
+                                    _P, _P, _P]
     L.moe_grouped_swiglu_ffn_mx.restype = _I
-    L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _P, _P, _PSZ, _P]
+    L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _PSZ,
+                                            _P]
     if L.moe_abi_version() != 2:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
@@ -133,6 +134,8 @@ def _wrows(t, name, dtype):
     if t.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
     B, R, K = t.shape
+    if t.numel() == 0:  # no experts (or empty matrices): nothing is read
+        return ctypes.c_void_p(t.data_ptr()), K
     ld = t.stride(1) if R > 1 else K
     if t.stride(2) != 1 or ld < K or (B > 1 and t.stride(0) != R * ld):
         raise ValueError(f"{name} must be [B, R, K] with unit element stride and rows {ld} apart")
@@ -247,11 +250,13 @@ def ffn_ws_bytes(E_local, H, I, M_cap, dtype):
 
 
 def weight_row_stride(K, elem_bytes=2):
-    """Row stride (elements) for expert weight rows of K elements: rows whose
-    byte length is a multiple of 4 KiB (H = 4096 or 2048 in bf16) put the
-    rows of a weight tile on the same few HBM channels, so they get 64
-    elements (128 bytes) of padding; other rows stay dense."""
-    return K + 64 if (K * elem_bytes) % 4096 == 0 else K
+    """Row stride (elements) for expert weight rows of K elements of
+    `elem_bytes` bytes: rows whose byte length is a multiple of 4 KiB put the
+    rows of a weight tile on few HBM channels, so they get 128 bytes of
+    padding (whole cache lines); other rows stay dense. Measured for bf16
+    weights (H = 4096 or 2048: the decode FFN 6-10 % faster); MXFP8 code
+    rows of 4 KiB streamed no faster padded."""
+    return K + 128 // elem_bytes if (K * elem_bytes) % 4096 == 0 else K
 
 
 def pad_weight_rows(w, ld=None):
@@ -516,7 +521,9 @@ def moe_drift_distance(w_cur, w_ref, delta=0.05, d=None, trigger=None):
 class MxTensor:
     """An MXFP8 operand: E4M3 codes [.., R, K] uint8 and scale dwords
     [.., K/128, R] int32 (byte b of dword (k, r): the E8M0 code of elements
-    [128 k + 32 b, +32) of row r)."""
+    [128 k + 32 b, +32) of row r). The codes may be a view with padded rows
+    (row stride ld >= K bytes, matrices R * ld apart), which weight operands
+    accept."""
 
     def __init__(self, codes, scales):
         if codes.dtype != torch.uint8 or scales.dtype != torch.int32:
@@ -524,40 +531,57 @@ class MxTensor:
         R, K = codes.shape[-2:]
         if tuple(scales.shape[-2:]) != (K // 128, R) or codes.shape[:-2] != scales.shape[:-2]:
             raise ValueError("scales must be [.., K/128, R] for codes [.., R, K]")
-        self.codes, self.scales = codes, scales
+        ld = codes.stride(-2) if R > 1 and codes.numel() > 0 else K
+        if codes.numel() > 0 and (codes.stride(-1) != 1 or ld < K or (codes.dim() == 3 and codes.shape[0] > 1
+                                                                       and codes.stride(0) != R * ld)):
+            raise ValueError("MXFP8 codes must be dense or rows padded to a common stride")
+        self.codes, self.scales, self.ld = codes, scales, ld
 
     @property
     def shape(self):
         return tuple(self.codes.shape)
 
 
-def moe_mx_quantize(x, out=None, row_count=None):
+def moe_mx_quantize(x, out=None, row_count=None, ld=None):
     """MXFP8 quantisation of x [R, K] or [B, R, K] (bf16 or fp32) along K.
     row_count: optional device int32 tensor of one element (R-row x only):
-    rows from it on are left as they are in `out`."""
+    rows from it on are left as they are in `out`. ld: row stride in bytes
+    of newly allocated codes (weights: ``weight_row_stride(K, 1)``)."""
     L = load_library()
     xb = x.unsqueeze(0) if x.dim() == 2 else x
     B, R, K = xb.shape
     if out is None:
-        out = MxTensor(torch.empty(x.shape, dtype=torch.uint8, device=x.device),
-                       torch.empty(tuple(x.shape[:-2]) + (K // 128, R), dtype=torch.int32, device=x.device))
+        ld = K if ld is None else ld
+        codes = torch.empty(tuple(x.shape[:-1]) + (ld,), dtype=torch.uint8, device=x.device)[..., :K]
+        out = MxTensor(codes, torch.empty(tuple(x.shape[:-2]) + (K // 128, R), dtype=torch.int32,
+                                          device=x.device))
     rc = ctypes.c_void_p(None)
     if row_count is not None:
         if row_count.numel() != 1 or row_count.dtype != torch.int32 or not row_count.is_cuda:
             raise ValueError("row_count must be one device int32")
         rc = ctypes.c_void_p(row_count.data_ptr())
-    st = L.moe_mx_quantize(_dev(x, "x"), _dtype_code(x), B, R, K, rc, _dev(out.codes, "codes", torch.uint8),
+    st = L.moe_mx_quantize(_dev(x, "x"), _dtype_code(x), B, R, K, out.ld, rc, _mx_codes(out.codes, "codes"),
                            _dev(out.scales, "scales", torch.int32), _stream())
     _check("moe_mx_quantize", st)
     return out
 
 
-def _mx_dev(t, name, shape):
+def _mx_codes(c, name):
+    if not c.is_cuda:
+        raise ValueError(f"{name} must be on the GPU (libmoe has no CPU path)")
+    return ctypes.c_void_p(c.data_ptr())
+
+
+def _mx_dev(t, name, shape, padded=False):
+    """Pointers of an MXFP8 operand; only weight operands (padded=True) may
+    have padded code rows."""
     if not isinstance(t, MxTensor):
         raise TypeError(f"{name} must be an MxTensor")
     if t.shape != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)}, got {t.shape}")
-    return _dev(t.codes, name + ".codes", torch.uint8), _dev(t.scales, name + ".scales", torch.int32)
+    if not padded and t.ld != t.shape[-1]:
+        raise ValueError(f"{name} must have dense code rows")
+    return _mx_codes(t.codes, name + ".codes"), _dev(t.scales, name + ".scales", torch.int32)
 
 
 def moe_grouped_swiglu_mx(x, w_gate, w_up, offsets, h=None):
@@ -571,9 +595,12 @@ def moe_grouped_swiglu_mx(x, w_gate, w_up, offsets, h=None):
     if h is None:
         h = MxTensor(torch.empty((M_cap, I), dtype=torch.uint8, device=dev),
                      torch.empty((I // 128, M_cap), dtype=torch.int32, device=dev))
-    st = L.moe_grouped_swiglu_mx(*_mx_dev(x, "x", (M_cap, H)), *_mx_dev(w_gate, "w_gate", (E_local, I, H)),
-                                 *_mx_dev(w_up, "w_up", (E_local, I, H)), _dev(offsets, "offsets", torch.int32),
-                                 E_local, H, I, M_cap, *_mx_dev(h, "h", (M_cap, I)), _stream())
+    if w_up.ld != w_gate.ld:
+        raise ValueError("w_gate and w_up must have the same row stride")
+    st = L.moe_grouped_swiglu_mx(*_mx_dev(x, "x", (M_cap, H)), *_mx_dev(w_gate, "w_gate", (E_local, I, H), True),
+                                 *_mx_dev(w_up, "w_up", (E_local, I, H), True),
+                                 _dev(offsets, "offsets", torch.int32), E_local, H, I, w_gate.ld, M_cap,
+                                 *_mx_dev(h, "h", (M_cap, I)), _stream())
     _check("moe_grouped_swiglu_mx", st)
     return h
 
@@ -587,8 +614,8 @@ def moe_grouped_gemm_mx(a, b, offsets, c=None):
         raise ValueError("offsets must have E_local + 1 entries")
     if c is None:
         c = torch.empty((M_cap, N), dtype=torch.bfloat16, device=a.codes.device)
-    st = L.moe_grouped_gemm_mx(*_mx_dev(a, "a", (M_cap, K)), *_mx_dev(b, "b", (E_local, N, K)),
-                               _dev(offsets, "offsets", torch.int32), E_local, N, K, M_cap,
+    st = L.moe_grouped_gemm_mx(*_mx_dev(a, "a", (M_cap, K)), *_mx_dev(b, "b", (E_local, N, K), True),
+                               _dev(offsets, "offsets", torch.int32), E_local, N, K, b.ld, M_cap,
                                _dev(c, "c", torch.bfloat16), _stream())
     _check("moe_grouped_gemm_mx", st)
     return c
@@ -597,8 +624,8 @@ def moe_grouped_gemm_mx(a, b, offsets, c=None):
 def ffn_mx_ws_bytes(E_local, H, I, M_cap):
     L = load_library()
     n = ctypes.c_size_t(0)
-    st = L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, E_local, H, I, M_cap,
-                                     None, None, ctypes.byref(n), None)
+    st = L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, E_local, H, I, 0, 0,
+                                     M_cap, None, None, ctypes.byref(n), None)
     _check("moe_grouped_swiglu_ffn_mx", st)
     return n.value
 
@@ -617,10 +644,14 @@ def moe_grouped_swiglu_ffn_mx(x, w_gate, w_up, w_down, offsets, ws=None, y_perm=
     if y_perm is None:
         y_perm = torch.empty((M_cap, H), dtype=torch.bfloat16, device=dev)
     n = ctypes.c_size_t(ws.numel())
-    st = L.moe_grouped_swiglu_ffn_mx(*_mx_dev(x, "x", (M_cap, H)), *_mx_dev(w_gate, "w_gate", (E_local, I, H)),
-                                     *_mx_dev(w_up, "w_up", (E_local, I, H)),
-                                     *_mx_dev(w_down, "w_down", (E_local, H, I)),
-                                     _dev(offsets, "offsets", torch.int32), E_local, H, I, M_cap,
+    if w_up.ld != w_gate.ld:
+        raise ValueError("w_gate and w_up must have the same row stride")
+    st = L.moe_grouped_swiglu_ffn_mx(*_mx_dev(x, "x", (M_cap, H)),
+                                     *_mx_dev(w_gate, "w_gate", (E_local, I, H), True),
+                                     *_mx_dev(w_up, "w_up", (E_local, I, H), True),
+                                     *_mx_dev(w_down, "w_down", (E_local, H, I), True),
+                                     _dev(offsets, "offsets", torch.int32), E_local, H, I, w_gate.ld, w_down.ld,
+                                     M_cap,
                                      _dev(y_perm, "y_perm", torch.bfloat16), _dev(ws, "ws", torch.uint8),
                                      ctypes.byref(n), _stream())
     _check("moe_grouped_swiglu_ffn_mx", st)
@@ -639,9 +670,11 @@ def moe_load_sweep_mx(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch
         raise ValueError(f"x must be [{max_m}, {H}] (rows for the largest M)")
     dev = x.codes.device
     n = ctypes.c_size_t(0)
-    args = (*_mx_dev(x, "x", (max_m, H)), *_mx_dev(w_gate, "w_gate", (n_rot, I, H)),
-            *_mx_dev(w_up, "w_up", (n_rot, I, H)), *_mx_dev(w_down, "w_down", (n_rot, H, I)), n_rot, H, I,
-            Ms.ctypes.data_as(ctypes.c_void_p), nM, warmup, iters)
+    if w_up.ld != w_gate.ld:
+        raise ValueError("w_gate and w_up must have the same row stride")
+    args = (*_mx_dev(x, "x", (max_m, H)), *_mx_dev(w_gate, "w_gate", (n_rot, I, H), True),
+            *_mx_dev(w_up, "w_up", (n_rot, I, H), True), *_mx_dev(w_down, "w_down", (n_rot, H, I), True), n_rot,
+            H, I, w_gate.ld, w_down.ld, Ms.ctypes.data_as(ctypes.c_void_p), nM, warmup, iters)
     st = L.moe_load_sweep_mx(*args, None, None, ctypes.byref(n), None, None, _stream())
     _check("moe_load_sweep_mx", st)
     ws = torch.empty(n.value, dtype=torch.uint8, device=dev)

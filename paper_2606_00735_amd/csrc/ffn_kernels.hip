@@ -1231,7 +1231,8 @@ struct MxSplit {
 
 static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
-                            int I, int M_cap, uint8_t* hq, uint32_t* hs, const MxSplit& sp, hipStream_t s) {
+                            int I, int ldw, int M_cap, uint8_t* hq, uint32_t* hs, const MxSplit& sp,
+                            hipStream_t s) {
   GemmArgs g{};
   g.A = reinterpret_cast<const bf16_t*>(xq);
   g.B0 = reinterpret_cast<const bf16_t*>(wgq);
@@ -1242,7 +1243,7 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   g.M_cap = M_cap;
   g.N = I;
   g.K = H;
-  g.ldb = H;
+  g.ldb = ldw;
   g.part = sp.part;
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;
@@ -1262,8 +1263,8 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
 }
 
 static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
-                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, const MxSplit& sp,
-                          hipStream_t s) {
+                          const int32_t* offsets, int E_local, int N, int K, int ldb, int M_cap, void* c,
+                          const MxSplit& sp, hipStream_t s) {
   GemmArgs g{};
   g.A = reinterpret_cast<const bf16_t*>(aq);
   g.B0 = reinterpret_cast<const bf16_t*>(bq);
@@ -1273,7 +1274,7 @@ static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
   g.M_cap = M_cap;
   g.N = N;
   g.K = K;
-  g.ldb = K;
+  g.ldb = ldb;
   g.part = sp.part;
   g.part_cap = sp.part_cap;
   g.plan = sp.plan;
@@ -1292,21 +1293,22 @@ static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
 
 hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
-                            int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s) {
+                            int I, int ldw, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
-  return gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, MxSplit{}, s);
+  return gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ldw, M_cap, hq, hs, MxSplit{}, s);
 }
 
 hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
-                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s) {
+                          const int32_t* offsets, int E_local, int N, int K, int ldb, int M_cap, void* c,
+                          hipStream_t s) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
-  return gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, M_cap, c, MxSplit{}, s);
+  return gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, ldb, M_cap, c, MxSplit{}, s);
 }
 
 hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                          const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
-                         const int32_t* offsets, int E_local, int H, int I, int M_cap, void* y_perm, void* ws,
-                         hipStream_t s) {
+                         const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap,
+                         void* y_perm, void* ws, hipStream_t s) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
   const FfnMxWs L = ffn_mx_ws_layout(M_cap, E_local, H, I);
   char* w = static_cast<char*>(ws);
@@ -1318,11 +1320,11 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   if (e != hipSuccess) return e;
   const MxSplit sp1{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
                     L.plan_rows, queue};
-  e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, sp1, s);
+  e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld_gu, M_cap, hq, hs, sp1, s);
   if (e != hipSuccess) return e;
   MxSplit sp2 = sp1;
   sp2.queue = queue + 8;
-  return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, M_cap, y_perm, sp2, s);
+  return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, ld_dn, M_cap, y_perm, sp2, s);
 }
 
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {

@@ -31,18 +31,21 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       int a_T = 0);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
-hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, const int32_t* row_count,
-                              uint8_t* codes, uint32_t* scales, hipStream_t s);
+// MXFP8: code rows of weight operands (and of quantiser outputs) are
+// ldw / ldb / ldc bytes apart; activation codes are dense.
+hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, int ldc,
+                              const int32_t* row_count, uint8_t* codes, uint32_t* scales, hipStream_t s);
 hipError_t launch_gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
-                            int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s);
+                            int I, int ldw, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t s);
 hipError_t launch_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
-                          const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c, hipStream_t s);
+                          const int32_t* offsets, int E_local, int N, int K, int ldb, int M_cap, void* c,
+                          hipStream_t s);
 size_t ffn_mx_ws_bytes(int M_cap, int E_local, int H, int I);
 hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                          const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
-                         const int32_t* offsets, int E_local, int H, int I, int M_cap, void* y_perm, void* ws,
-                         hipStream_t s);
+                         const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap,
+                         void* y_perm, void* ws, hipStream_t s);
 
 hipError_t launch_place_greedy(const double* W, int L, int E, const double* kn, const double* kt, int G, int nk,
                                int cap, int32_t* assign, double* loads, double* targets, hipStream_t s);

@@ -77,6 +77,15 @@ moe_status resolve_ld(int ld, int K, moe_dtype dt, int* out) {
   return MOE_OK;
 }
 
+// Row stride in bytes of MXFP8 weight codes with K codes a row: 0 means K;
+// otherwise at least K, a multiple of 16 and at most 2^20.
+moe_status resolve_ld_mx(int ld, int K, int* out) {
+  if (ld == 0) ld = K;
+  if (ld < K || ld % 16 != 0 || ld > (1 << 20)) return MOE_ERR_INVALID_ARG;
+  *out = ld;
+  return MOE_OK;
+}
+
 // The timing loop shared by the load sweeps: for each M of Ms, sets
 // offsets = [0, M], then runs `run(rot, M)` warmup + iters times rotating
 // through n_rot weight copies, each timed run bracketed by HIP events.
@@ -339,7 +348,8 @@ moe_status moe_load_sweep(const void* x, const void* w_gate, const void* w_up, c
 
 moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                              const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq, const uint32_t* wds,
-                             int n_rot, int H, int I, const int32_t* Ms, int nM, int warmup, int iters,
+                             int n_rot, int H, int I, int ldw_gu, int ldw_dn, const int32_t* Ms, int nM, int warmup,
+                             int iters,
                              void* y_scratch, void* ws, size_t* ws_bytes, float* us_out, float* us_all,
                              hipStream_t stream) {
   if (Ms == nullptr || nM < 1 || nM > 64 || warmup < 0 || iters < 1 || iters > 10000 || n_rot < 1 ||
@@ -352,6 +362,9 @@ moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_
   }
   moe_status st = mx_gemm_shape_ok(1, I, H, max_m);
   if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld_mx(ldw_gu, H, &ld_gu)) != MOE_OK || (st = resolve_ld_mx(ldw_dn, I, &ld_dn)) != MOE_OK)
+    return st;
   // x and its scales are laid out for max_m rows, so every run uses
   // M_cap = max_m with offsets [0, M]
   const size_t ffn_ws = moe::ffn_mx_ws_bytes(max_m, 1, H, I);
@@ -364,14 +377,14 @@ moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_
   if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) ||
       !mx_operand_ok(wdq, wds) || !y_scratch || !aligned16(y_scratch) || !aligned16(ws) || !us_out)
     return MOE_ERR_INVALID_ARG;
-  const size_t wmat = (size_t)H * I;                   // code bytes of one expert matrix
+  const size_t wgu = (size_t)I * ld_gu, wdn = (size_t)H * ld_dn;  // code bytes of one copy
   const size_t smat = (size_t)(H / 128) * I;           // scale dwords of W_gate / W_up
   const size_t sdown = (size_t)(I / 128) * H;          // scale dwords of W_down
   int32_t* offsets = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + ffn_ws);
   return sweep_loop(Ms, nM, warmup, iters, n_rot, offsets, us_out, us_all, stream, [&](int rot, int m) {
-    return moe::launch_ffn_mx(xq, xs, wgq + rot * wmat, wgs + rot * smat, wuq + rot * wmat, wus + rot * smat,
-                              wdq + rot * wmat, wds + rot * sdown, offsets, 1, H, I, max_m, y_scratch, ws,
-                              stream);
+    return moe::launch_ffn_mx(xq, xs, wgq + rot * wgu, wgs + rot * smat, wuq + rot * wgu, wus + rot * smat,
+                              wdq + rot * wdn, wds + rot * sdown, offsets, 1, H, I, ld_gu, ld_dn, max_m, y_scratch,
+                              ws, stream);
   });
 }
 
@@ -382,46 +395,58 @@ moe_status moe_load_sweep_mx(const uint8_t* xq, const uint32_t* xs, const uint8_
 // ---------------------------------------------------------------------------
 extern "C" {
 
-moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, const int32_t* row_count,
-                           uint8_t* codes, uint32_t* scales, hipStream_t stream) {
+moe_status moe_mx_quantize(const void* x, moe_dtype dt, int batch, int rows, int K, int ld_codes,
+                           const int32_t* row_count, uint8_t* codes, uint32_t* scales, hipStream_t stream) {
   if (!valid_dtype(dt) || batch < 0 || rows < 0 || K < 1) return MOE_ERR_INVALID_ARG;
   if (K % 128 != 0) return MOE_ERR_UNSUPPORTED;
+  int ldc = 0;
+  if (resolve_ld_mx(ld_codes, K, &ldc) != MOE_OK) return MOE_ERR_INVALID_ARG;
   if ((long long)batch * rows * K > (1LL << 40)) return MOE_ERR_UNSUPPORTED;
   if (row_count != nullptr && (batch > 1 || !aligned4(row_count))) return MOE_ERR_INVALID_ARG;
   if (batch == 0 || rows == 0) return MOE_OK;
   if (!x || !aligned16(x) || !mx_operand_ok(codes, scales)) return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_mx_quantize(x, dt == MOE_F32, batch, rows, K, row_count, codes, scales, stream));
+  return hip_status(
+      moe::launch_mx_quantize(x, dt == MOE_F32, batch, rows, K, ldc, row_count, codes, scales, stream));
 }
 
 moe_status moe_grouped_swiglu_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                                  const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local,
-                                 int H, int I, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t stream) {
+                                 int H, int I, int ldw, int M_cap, uint8_t* hq, uint32_t* hs, hipStream_t stream) {
   moe_status st = mx_gemm_shape_ok(E_local, I, H, M_cap);
   if (st != MOE_OK) return st;
+  int ld = 0;
+  if ((st = resolve_ld_mx(ldw, H, &ld)) != MOE_OK) return st;
   if (E_local == 0 || M_cap == 0) return MOE_OK;
   if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) || !mx_operand_ok(hq, hs) ||
       !offsets || !aligned4(offsets))
     return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, M_cap, hq, hs, stream));
+  return hip_status(
+      moe::launch_gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld, M_cap, hq, hs, stream));
 }
 
 moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* bq, const uint32_t* bs,
-                               const int32_t* offsets, int E_local, int N, int K, int M_cap, void* c,
+                               const int32_t* offsets, int E_local, int N, int K, int ldb, int M_cap, void* c,
                                hipStream_t stream) {
   moe_status st = mx_gemm_shape_ok(E_local, N, K, M_cap);
   if (st != MOE_OK) return st;
+  int ld = 0;
+  if ((st = resolve_ld_mx(ldb, K, &ld)) != MOE_OK) return st;
   if (E_local == 0 || M_cap == 0) return MOE_OK;
   if (!mx_operand_ok(aq, as) || !mx_operand_ok(bq, bs) || !c || !aligned16(c) || !offsets || !aligned4(offsets))
     return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, M_cap, c, stream));
+  return hip_status(moe::launch_gemm_mx(aq, as, bq, bs, offsets, E_local, N, K, ld, M_cap, c, stream));
 }
 
 moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                                      const uint8_t* wuq, const uint32_t* wus, const uint8_t* wdq,
                                      const uint32_t* wds, const int32_t* offsets, int E_local, int H, int I,
-                                     int M_cap, void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream) {
+                                     int ldw_gu, int ldw_dn, int M_cap, void* y_perm, void* ws, size_t* ws_bytes,
+                                     hipStream_t stream) {
   moe_status st = mx_gemm_shape_ok(E_local, I, H, M_cap);
   if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld_mx(ldw_gu, H, &ld_gu)) != MOE_OK || (st = resolve_ld_mx(ldw_dn, I, &ld_dn)) != MOE_OK)
+    return st;
   if (ws_bytes == nullptr) return MOE_ERR_INVALID_ARG;
   const size_t need = moe::ffn_mx_ws_bytes(M_cap, E_local, H, I);
   if (ws == nullptr) {
@@ -433,8 +458,8 @@ moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, cons
   if (!mx_operand_ok(xq, xs) || !mx_operand_ok(wgq, wgs) || !mx_operand_ok(wuq, wus) ||
       !mx_operand_ok(wdq, wds) || !y_perm || !aligned16(y_perm) || !aligned16(ws) || !offsets || !aligned4(offsets))
     return MOE_ERR_INVALID_ARG;
-  return hip_status(moe::launch_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets, E_local, H, I, M_cap, y_perm,
-                                       ws, stream));
+  return hip_status(moe::launch_ffn_mx(xq, xs, wgq, wgs, wuq, wus, wdq, wds, offsets, E_local, H, I, ld_gu, ld_dn,
+                                       M_cap, y_perm, ws, stream));
 }
 
 }  // extern "C"

@@ -6,8 +6,8 @@
 
 namespace moe {
 
-// x [batch][rows][K] (bf16 or fp32) -> codes [batch][rows][K] E4M3 and scale
-// dwords [batch][K/128][rows]. Each lane takes 8 consecutive elements, so the
+// x [batch][rows][K] (bf16 or fp32) -> codes [batch][rows][K] E4M3 (rows ldc
+// bytes apart, ldc >= K a multiple of 16) and scale dwords [batch][K/128][rows]. Each lane takes 8 consecutive elements, so the
 // 4 lanes of a 32-element block (a lane group aligned to 4) find the block's
 // largest magnitude with two shuffles; the first of them writes the scale
 // code. K % 128 == 0 keeps every group inside one row, and the element count
@@ -16,7 +16,7 @@ namespace moe {
 // *row_count)) are quantised; the others are left as they are.
 template <bool F32IN>
 __global__ __launch_bounds__(256) void mx_quantize_kernel(const void* __restrict__ x, int batch, int rows, int K,
-                                                          const int32_t* __restrict__ row_count,
+                                                          int ldc, const int32_t* __restrict__ row_count,
                                                           uint8_t* __restrict__ codes,
                                                           uint32_t* __restrict__ scales) {
   const int n8k = K / 8;
@@ -47,10 +47,10 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const void* __restrict
     uint2 out;
     out.x = e4m3x4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
     out.y = e4m3x4(v[4] * inv, v[5] * inv, v[6] * inv, v[7] * inv);
-    reinterpret_cast<uint2*>(codes)[t] = out;
     const int k8 = (int)(t % n8k);
+    const size_t row = t / n8k;  // batch * rows + r
+    *reinterpret_cast<uint2*>(codes + row * ldc + (size_t)k8 * 8) = out;
     if ((k8 & 3) == 0) {
-      const size_t row = t / n8k;  // batch * rows + r
       const size_t b = row / rows, r = row % rows;
       const int kb = k8 / 4;  // 32-element block within the row
       reinterpret_cast<uint8_t*>(scales + (b * (K / kMxChunk) + kb / 4) * rows + r)[kb & 3] =
@@ -59,8 +59,8 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const void* __restrict
   }
 }
 
-hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, const int32_t* row_count,
-                              uint8_t* codes, uint32_t* scales, hipStream_t s) {
+hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int K, int ldc,
+                              const int32_t* row_count, uint8_t* codes, uint32_t* scales, hipStream_t s) {
   const size_t n8 = (size_t)batch * rows * (K / 8);
   if (n8 == 0) return hipSuccess;
   int dev = 0, cus = 256;
@@ -71,9 +71,9 @@ hipError_t launch_mx_quantize(const void* x, bool f32, int batch, int rows, int 
   size_t grid = (n8 + 255) / 256;
   if (grid > (size_t)cus * 16) grid = (size_t)cus * 16;
   if (f32)
-    mx_quantize_kernel<true><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, row_count, codes, scales);
+    mx_quantize_kernel<true><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, ldc, row_count, codes, scales);
   else
-    mx_quantize_kernel<false><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, row_count, codes, scales);
+    mx_quantize_kernel<false><<<(unsigned)grid, 256, 0, s>>>(x, batch, rows, K, ldc, row_count, codes, scales);
   return hipGetLastError();
 }
 

@@ -282,31 +282,31 @@ def test_mx_validation_and_query(L):
     misaligned operands invalid, the workspace query sized for h codes and
     their scale dwords."""
     n = ctypes.c_size_t(0)
-    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, 4096, 14336, 8192,
-                                       None, None, ctypes.byref(n), None) == 0
+    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, 4096, 14336, 0, 0,
+                                       8192, None, None, ctypes.byref(n), None) == 0
     assert n.value >= 8192 * 14336 + (14336 // 128) * 8192 * 4
     for H, I in ((4096, 14300), (4000, 14336)):
-        assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, H, I, 64,
+        assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 8, H, I, 0, 0, 64,
                                            None, None, ctypes.byref(n), None) == UNSUPPORTED
-    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 300, 128, 128, 64,
+    assert L.moe_grouped_swiglu_ffn_mx(None, None, None, None, None, None, None, None, None, 300, 128, 128, 0, 0, 64,
                                        None, None, ctypes.byref(n), None) == UNSUPPORTED
     n = ctypes.c_size_t(10)
-    assert L.moe_grouped_swiglu_ffn_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 64,
+    assert L.moe_grouped_swiglu_ffn_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 8, 128, 256, 0, 0, 64,
                                        FAKE, FAKE, ctypes.byref(n), None) == WORKSPACE
     # quantiser: K % 128, dtype, null and misaligned pointers
-    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 200, None, FAKE, FAKE, None) == UNSUPPORTED
-    assert L.moe_mx_quantize(FAKE, 7, 1, 4, 256, None, FAKE, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 256, None, None, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(MISALIGNED, 1, 1, 4, 256, None, FAKE, FAKE, None) == INVALID
-    assert L.moe_mx_quantize(FAKE, 1, 2, 4, 256, FAKE, FAKE, FAKE, None) == INVALID   # row count: batch 1 only
-    assert L.moe_mx_quantize(None, 1, 0, 4, 256, None, None, None, None) == 0     # empty: no-op
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 200, 0, None, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.moe_mx_quantize(FAKE, 7, 1, 4, 256, 0, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(FAKE, 1, 1, 4, 256, 0, None, None, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(MISALIGNED, 1, 1, 4, 256, 0, None, FAKE, FAKE, None) == INVALID
+    assert L.moe_mx_quantize(FAKE, 1, 2, 4, 256, 0, FAKE, FAKE, FAKE, None) == INVALID   # row count: batch 1 only
+    assert L.moe_mx_quantize(None, 1, 0, 4, 256, 0, None, None, None, None) == 0     # empty: no-op
     # GEMMs
-    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 100, 256, 64, FAKE, None) == UNSUPPORTED
-    assert L.moe_grouped_gemm_mx(FAKE, FAKE, None, FAKE, FAKE, 2, 128, 256, 64, FAKE, None) == INVALID
-    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, -1, 128, 256, 64, FAKE, None) == INVALID
-    assert L.moe_grouped_swiglu_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 128, 384, 64, FAKE, None,
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, 2, 100, 256, 0, 64, FAKE, None) == UNSUPPORTED
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, None, FAKE, FAKE, 2, 128, 256, 0, 64, FAKE, None) == INVALID
+    assert L.moe_grouped_gemm_mx(FAKE, FAKE, FAKE, FAKE, FAKE, -1, 128, 256, 0, 64, FAKE, None) == INVALID
+    assert L.moe_grouped_swiglu_mx(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 128, 384, 0, 64, FAKE, None,
                                    None) == INVALID
-    assert L.moe_grouped_swiglu_mx(None, None, None, None, None, None, None, 0, 128, 384, 64, None, None,
+    assert L.moe_grouped_swiglu_mx(None, None, None, None, None, None, None, 0, 128, 384, 0, 64, None, None,
                                    None) == 0
 
 
@@ -315,15 +315,41 @@ def test_mx_sweep_validation(L):
     pM = Ms.ctypes.data_as(ctypes.c_void_p)
     n = ctypes.c_size_t(0)
     args = [FAKE] * 8
-    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, 0, 0, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
                                None) == 0
     assert n.value >= 8 * 14336
-    assert L.moe_load_sweep_mx(*args, 1, 4096, 14300, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14300, 0, 0, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
                                None) == UNSUPPORTED
-    assert L.moe_load_sweep_mx(*args, 0, 4096, 14336, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
+    assert L.moe_load_sweep_mx(*args, 0, 4096, 14336, 0, 0, pM, 2, 1, 3, None, None, ctypes.byref(n), None, None,
                                None) == INVALID
-    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 0, None, None, ctypes.byref(n), None, None,
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, 0, 0, pM, 2, 1, 0, None, None, ctypes.byref(n), None, None,
                                None) == INVALID
     n = ctypes.c_size_t(16)
-    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, pM, 2, 1, 3, FAKE, FAKE, ctypes.byref(n), FAKE, None,
+    assert L.moe_load_sweep_mx(*args, 1, 4096, 14336, 0, 0, pM, 2, 1, 3, FAKE, FAKE, ctypes.byref(n), FAKE, None,
                                None) == WORKSPACE
+
+
+def test_mx_weight_row_strides(L):
+    """Padded MXFP8 code rows: a multiple of 16 bytes, at least K, checked
+    before anything else is looked at."""
+    n, m = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    nul = [None] * 9
+    assert L.moe_grouped_swiglu_ffn_mx(*nul, 8, 4096, 14336, 0, 0, 64, None, None, ctypes.byref(n), None) == 0
+    assert L.moe_grouped_swiglu_ffn_mx(*nul, 8, 4096, 14336, 4224, 14464, 64, None, None, ctypes.byref(m),
+                                       None) == 0
+    assert n.value == m.value
+    for gu, dn in ((4100, 0), (4095, 0), (0, 14344), (0, 14335), (1 << 21, 0)):
+        assert L.moe_grouped_swiglu_ffn_mx(*nul, 8, 4096, 14336, gu, dn, 64, None, None, ctypes.byref(m),
+                                           None) == INVALID, (gu, dn)
+    assert L.moe_mx_quantize(None, 1, 0, 4, 256, 384, None, None, None, None) == 0
+    for ld in (264, 255, -16):
+        assert L.moe_mx_quantize(None, 1, 0, 4, 256, ld, None, None, None, None) == INVALID
+    assert L.moe_grouped_gemm_mx(None, None, None, None, None, 0, 128, 256, 272, 64, None, None) == 0
+    assert L.moe_grouped_gemm_mx(None, None, None, None, None, 0, 128, 256, 200, 64, None, None) == INVALID
+    assert L.moe_grouped_swiglu_mx(None, None, None, None, None, None, None, 0, 128, 384, 136, 64, None, None,
+                                   None) == INVALID
+    Ms = np.array([1, 8], np.int32)
+    assert L.moe_load_sweep_mx(*([FAKE] * 8), 1, 4096, 14336, 4224, 0, Ms.ctypes.data_as(ctypes.c_void_p), 2, 1, 3,
+                               None, None, ctypes.byref(n), None, None, None) == 0
+    assert L.moe_load_sweep_mx(*([FAKE] * 8), 1, 4096, 14336, 4104, 0, Ms.ctypes.data_as(ctypes.c_void_p), 2, 1, 3,
+                               None, None, ctypes.byref(n), None, None, None) == INVALID

@@ -430,7 +430,9 @@ def test_ffn_mx_fullsize(name, T, alpha):
     xp_full = np.zeros((M_cap, H), np.float32)
     xp_full[:m] = x_perm
     tx = moe.moe_mx_quantize(up(xp_full))
-    tg, tu, td = (moe.moe_mx_quantize(up(w)) for w in (li.w_gate, li.w_up, li.w_down))
+    # weight code rows padded to weight_row_stride: the padded path at full size
+    tg, tu, td = (moe.moe_mx_quantize(up(w), ld=moe.weight_row_stride(w.shape[-1], 1))
+                  for w in (li.w_gate, li.w_up, li.w_down))
     y, _ = moe.moe_grouped_swiglu_ffn_mx(tx, tg, tu, td, torch.from_numpy(offsets.astype(np.int32)).to(DEV))
     torch.cuda.synchronize()
     got = y.float().cpu().numpy()
@@ -465,3 +467,70 @@ class _Sub:
             idx = torch.from_numpy(np.asarray(sel, np.int64)).to(DEV)
             self.codes = t.codes[idx]
             self.scales = t.scales[:, idx]
+
+
+def _quant_padded(w, pad):
+    """MXFP8 codes of weights [B, R, K] written into rows padded by `pad`
+    bytes, the padding pre-filled with 0x7F (an E4M3 NaN: read, it would
+    poison the output)."""
+    B, R, K = w.shape
+    codes = torch.full((B, R, K + pad), 0x7F, dtype=torch.uint8, device=DEV)[:, :, :K]
+    scales = torch.empty((B, K // 128, R), dtype=torch.int32, device=DEV)
+    return moe.moe_mx_quantize(up(w), out=moe.MxTensor(codes, scales))
+
+
+MX_PAD_CASES = [
+    # (H, I, rows per expert, pad of gate/up code rows, pad of down code rows)
+    (4096, 1024, [1, 64, 0, 30], 128, 16),        # split-K in both GEMMs
+    (1024, 1024, [257, 300, 321, 576, 1], 128, 128),
+    (2048, 2048, [4608], 16, 128),                # tail split
+]
+
+
+@pytest.mark.parametrize("H,I,rows,pg,pd", MX_PAD_CASES, ids=["split", "ragged", "tail"])
+def test_ffn_mx_padded_weight_rows(H, I, rows, pg, pd):
+    """MXFP8 weights quantised into padded code rows: the same codes and
+    scales as dense ones, the padding untouched, and the FFN, its gate/up
+    half and the down GEMM give the dense operands' results bit for bit."""
+    banner("mx ffn padded rows", H, I, rows, pg, pd, "seed 13")
+    xp, wg, wu, wd, offsets, m = _inputs(H, I, rows, seed=13)
+    doff = torch.from_numpy(offsets).to(DEV)
+    tx = moe.moe_mx_quantize(up(xp))
+    dense = [moe.moe_mx_quantize(up(w)) for w in (wg, wu, wd)]
+    padded = [_quant_padded(wg, pg), _quant_padded(wu, pg), _quant_padded(wd, pd)]
+    torch.cuda.synchronize()
+    for d, p, pad in zip(dense, padded, (pg, pg, pd)):
+        assert p.ld == d.ld + pad
+        assert torch.equal(p.codes, d.codes) and torch.equal(p.scales, d.scales)
+        assert bool((p.codes.as_strided((p.codes.shape[0], p.codes.shape[1], pad),
+                                        p.codes.stride(), p.codes.shape[2]) == 0x7F).all()), "padding written"
+    y1, _ = moe.moe_grouped_swiglu_ffn_mx(tx, *dense, doff)
+    y2, _ = moe.moe_grouped_swiglu_ffn_mx(tx, *padded, doff)
+    h1 = moe.moe_grouped_swiglu_mx(tx, dense[0], dense[1], doff)
+    h2 = moe.moe_grouped_swiglu_mx(tx, padded[0], padded[1], doff)
+    c1 = moe.moe_grouped_gemm_mx(h1, dense[2], doff)
+    c2 = moe.moe_grouped_gemm_mx(h1, padded[2], doff)
+    torch.cuda.synchronize()
+    assert torch.equal(y2[:m], y1[:m]), "FFN output"
+    assert torch.equal(h2.codes[:m], h1.codes[:m]) and torch.equal(h2.scales[:, :m], h1.scales[:, :m]), "h"
+    assert torch.equal(c2[:m], c1[:m]), "down GEMM"
+    assert bool(torch.isfinite(y2[:m].float()).all())
+
+
+def test_load_sweep_mx_padded_weight_rows():
+    """The MXFP8 sweep over weight copies with padded code rows leaves the
+    same y as over dense copies."""
+    banner("mx sweep padded rows")
+    H, I = 2048, 768
+    _, wg, wu, wd, _, _ = _inputs(H, I, [1], seed=12)
+    x, *_ = make_router(_shape(H, I, 1), 96, 0.0, seed=12)
+    tx = moe.moe_mx_quantize(up(x))
+    rot = 3
+    ys = []
+    for pad in (0, 128):
+        w = [_quant_padded(np.repeat(a, rot, 0), pad) for a in (wg, wu, wd)]
+        y = torch.full((96, H), float("nan"), dtype=torch.bfloat16, device=DEV)
+        moe.moe_load_sweep_mx(tx, *w, [1, 96], warmup=1, iters=2, y_scratch=y)
+        ys.append(y)
+    torch.cuda.synchronize()
+    assert torch.equal(ys[0], ys[1])
