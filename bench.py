@@ -152,7 +152,8 @@ def main():
         for s in range(steps):
             ev = evs[s]
             ev[0].record()
-            ids, wts, _ = moe.moe_gate_topk(xb, wr, bb["bias"], k, ids=bb["ids"], weights=bb["weights"])
+            ids, wts, _ = moe.moe_gate_topk(xb, wr, bb["bias"], k, ids=bb["ids"], weights=bb["weights"],
+                                            ws=bb["gate_ws"])
             ev[1].record()
             counts, offsets, hws = moe.moe_expert_histogram_scan(ids, E, emap, ws=bb["hist_ws"],
                                                                  counts=bb["counts"], offsets=bb["offsets"])

@@ -81,13 +81,25 @@ int moe_abi_version(void);
  * topk_ids   [T, k]  int32       selected expert ids
  * topk_w     [T, k]  fp32        gate weights
  * Limits: 1 <= E <= 256, 1 <= k <= min(E, 16), H % 8 == 0 (bf16: H % 64 == 0).
+ * ws         optional workspace: with ws == NULL and ws_bytes != NULL the
+ *            call stores the byte count in *ws_bytes and launches nothing
+ *            (the count is 0 where no workspace is used: fp32, E other than
+ *            128 or 256, E = 128 with more than 4096 tokens); with ws and
+ *            ws_bytes both
+ *            NULL the router runs without it. Given one (16-byte aligned,
+ *            *ws_bytes at least the count, else MOE_ERR_WORKSPACE), bf16
+ *            routers over 128 or 256 experts sum the logits over K ranges of
+ *            256-token tiles into fp32 partials there and add them in a fixed
+ *            order, so a CU loads 256 tokens' rows and a K range of the router
+ *            rows instead of every router row for each 64 tokens.
  * T == 0 is a no-op. The kernel accumulates in fp32; inputs whose products
- * and partial sums are exact in fp32 give order-independent logits.
+ * and partial sums are exact in fp32 give order-independent logits (and the
+ * same logits with or without the workspace).
  */
 moe_status moe_gate_topk(const void* x, const void* w_router, const float* bias,
                          int T, int H, int E, int k, moe_dtype dt,
                          float* logits_out, int32_t* topk_ids, float* topk_w,
-                         hipStream_t stream);
+                         void* ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
  * moe_expert_histogram_scan - the activation profile and local offsets.

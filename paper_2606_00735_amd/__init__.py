@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     ffn_hidden,
     ffn_mx_ws_bytes,
     ffn_ws_bytes,
+    gate_ws_bytes,
     hist_ws_bytes,
     load_library,
     moe_drift_distance,

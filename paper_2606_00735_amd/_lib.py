@@ -56,7 +56,7 @@ def load_library(path: str = LIB_PATH):
     L.moe_abi_version.restype = _I
     L.moe_abi_version.argtypes = []
     L.moe_gate_topk.restype = _I
-    L.moe_gate_topk.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P]
+    L.moe_gate_topk.argtypes = [_P, _P, _P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _PSZ, _P]
     L.moe_expert_histogram_scan.restype = _I
     L.moe_expert_histogram_scan.argtypes = [_P, _I, _I, _I, _P, _I, _P, _P, _P, _PSZ, _P]
     L.moe_permute.restype = _I
@@ -162,8 +162,20 @@ def _ptr_or_null(t, name, dtype=None):
 # ---------------------------------------------------------------------------
 # The six entry points
 # ---------------------------------------------------------------------------
-def moe_gate_topk(x, w_router, bias, k, logits=False, ids=None, weights=None):
-    """Top-k gating. Returns (ids [T,k] int32, weights [T,k] fp32, logits [T,E] or None)."""
+def gate_ws_bytes(T, H, E, dtype):
+    """Bytes of the router's optional workspace (0 where it is not used)."""
+    L = load_library()
+    n = ctypes.c_size_t(0)
+    dt = MOE_BF16 if dtype == torch.bfloat16 else MOE_F32
+    st = L.moe_gate_topk(None, None, None, T, H, E, 1, dt, None, None, None, None, ctypes.byref(n), None)
+    _check("moe_gate_topk", st)
+    return n.value
+
+
+def moe_gate_topk(x, w_router, bias, k, logits=False, ids=None, weights=None, ws=None, use_ws=True):
+    """Top-k gating. Returns (ids [T,k] int32, weights [T,k] fp32, logits [T,E] or None).
+    ws: the router's workspace (allocated here when needed and not given);
+    use_ws=False runs the router without one."""
     L = load_library()
     T, H = x.shape
     E = w_router.shape[0]
@@ -175,9 +187,17 @@ def moe_gate_topk(x, w_router, bias, k, logits=False, ids=None, weights=None):
     weights = torch.empty((T, k), dtype=torch.float32, device=dev) if weights is None else weights
     lg = torch.empty((T, E), dtype=torch.float32, device=dev) if logits is True else (
         logits if isinstance(logits, torch.Tensor) else None)
+    pws, n = ctypes.c_void_p(None), None
+    if use_ws:
+        need = gate_ws_bytes(T, H, E, x.dtype)
+        if need > 0:
+            if ws is None or ws.numel() * ws.element_size() < need:
+                ws = torch.empty(need, dtype=torch.uint8, device=dev)
+            pws, n = _dev(ws, "ws"), ctypes.c_size_t(ws.numel() * ws.element_size())
     st = L.moe_gate_topk(_dev(x, "x"), _dev(w_router, "w_router"), _ptr_or_null(bias, "bias", torch.float32),
                          T, H, E, k, dt, _ptr_or_null(lg, "logits", torch.float32),
-                         _dev(ids, "ids", torch.int32), _dev(weights, "weights", torch.float32), _stream())
+                         _dev(ids, "ids", torch.int32), _dev(weights, "weights", torch.float32), pws,
+                         ctypes.byref(n) if n is not None else None, _stream())
     _check("moe_gate_topk", st)
     return ids, weights, lg
 
@@ -394,8 +414,12 @@ def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=Fal
     b = {} if bufs is None else bufs
     T = x.shape[0]
     E = w_router.shape[0]
+    gws = b.get("gate_ws")
+    if gws is None:
+        need = gate_ws_bytes(T, x.shape[1], E, x.dtype)
+        gws = torch.empty(need, dtype=torch.uint8, device=x.device) if need > 0 else None
     ids, wts, lg = moe_gate_topk(x, w_router, bias, k, logits=logits, ids=b.get("ids"),
-                                 weights=b.get("weights"))
+                                 weights=b.get("weights"), ws=gws)
     counts, offsets, hws = moe_expert_histogram_scan(ids, E, expert_map, ws=b.get("hist_ws"),
                                                      counts=b.get("counts"), offsets=b.get("offsets"))
     x_perm, perm_src, dest = moe_permute(x, ids, expert_map, hws, x_perm=b.get("x_perm"),
@@ -408,7 +432,7 @@ def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=Fal
                                              y_perm=b.get("y_perm"))
     out = moe_unpermute_combine(y_perm, wts, dest, T, out=b.get("out"))
     if bufs is not None:
-        bufs.update(ids=ids, weights=wts, hist_ws=hws, counts=counts, offsets=offsets, perm_src=perm_src,
+        bufs.update(ids=ids, weights=wts, gate_ws=gws, hist_ws=hws, counts=counts, offsets=offsets, perm_src=perm_src,
                     dest=dest, ffn_ws=fws, y_perm=y_perm, out=out)
         if x_perm is not None:
             bufs["x_perm"] = x_perm

@@ -1327,6 +1327,48 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, ld_dn, M_cap, y_perm, sp2, s);
 }
 
+// ---------------------------------------------------------------------------
+// Router logits by K ranges (the router GEMM z = x W_r^T for many tokens and
+// E = 128 or 256 experts): block (t, s) sums x[256 t, +256) W_r^T over the K
+// chunks [s nK / S, (s + 1) nK / S) with the expert FFN's 256-row tile and
+// writes the fp32 sums to part[s][row][0, E); gate_topk_reduce_kernel adds the
+// S slices in split order. A CU then loads 256 token rows and the E router
+// rows of one K range, where a router block that finishes its tokens' top-k
+// itself loads all E router rows for every 64 tokens.
+// ---------------------------------------------------------------------------
+template <int BN>
+__global__ __launch_bounds__(kThreads) void router_logits_split_kernel(GemmArgs a, int S, float* __restrict__ part) {
+  __shared__ __align__(16) bf16_t smem[Stages<256, BN, false>::BYTES / 2];
+  const int T = a.M_cap;
+  const int m0 = (int)blockIdx.x * 256;
+  const int m_end = min(m0 + 256, T);
+  const int nK = a.K / kBK, sp = (int)blockIdx.y;
+  const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
+  float* pbase = part + ((size_t)sp * T + m0) * BN;
+  gemm_tile<256, BN, 4, false, true>(a, smem, 0, m0, m_end, 0, kc0, kc1, pbase, 0, BN, 0);
+}
+
+hipError_t launch_router_logits_split(const void* x, const void* wr, int T, int H, int E, int S, float* part,
+                                      hipStream_t s) {
+  if (T < 1 || S < 1 || S > 8 || H % kBK != 0 || H / kBK < S) return hipErrorInvalidValue;
+  GemmArgs g{};
+  g.A = static_cast<const bf16_t*>(x);
+  g.B0 = static_cast<const bf16_t*>(wr);
+  g.E_local = 1;
+  g.M_cap = T;
+  g.N = E;
+  g.K = H;
+  g.ldb = H;
+  const dim3 grid((unsigned)((T + 255) / 256), (unsigned)S);
+  if (E == 256)
+    router_logits_split_kernel<256><<<grid, kThreads, 0, s>>>(g, S, part);
+  else if (E == 128)
+    router_logits_split_kernel<128><<<grid, kThreads, 0, s>>>(g, S, part);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {
   set_offsets_kernel<<<1, 64, 0, s>>>(offsets, m);
   return hipGetLastError();

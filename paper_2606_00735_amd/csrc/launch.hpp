@@ -10,8 +10,12 @@
 
 namespace moe {
 
+// ws (optional, gate_ws_bytes): fp32 partial logits of the K-split router.
+size_t gate_ws_bytes(int T, int H, int E, bool bf16);
 hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, int T, int H, int E, int k,
-                            bool bf16, float* logits, int32_t* ids, float* wts, hipStream_t s);
+                            bool bf16, float* logits, int32_t* ids, float* wts, void* ws, hipStream_t s);
+hipError_t launch_router_logits_split(const void* x, const void* wr, int T, int H, int E, int S, float* part,
+                                      hipStream_t s);
 
 size_t hist_ws_bytes(int T, int E, int E_local);
 hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map, int32_t* counts,

@@ -182,19 +182,26 @@ const char* moe_status_string(moe_status s) {
 int moe_abi_version(void) { return MOE_ABI_VERSION; }
 
 moe_status moe_gate_topk(const void* x, const void* w_router, const float* bias, int T, int H, int E, int k,
-                         moe_dtype dt, float* logits_out, int32_t* topk_ids, float* topk_w,
-                         hipStream_t stream) {
+                         moe_dtype dt, float* logits_out, int32_t* topk_ids, float* topk_w, void* ws,
+                         size_t* ws_bytes, hipStream_t stream) {
   moe_status st = check_tk(T, k, E);
   if (st != MOE_OK) return st;
   if (!valid_dtype(dt) || H < 1 || H % 8 != 0) return MOE_ERR_INVALID_ARG;
   if (dt == MOE_BF16 && H % 64 != 0) return MOE_ERR_UNSUPPORTED;
+  const size_t need = moe::gate_ws_bytes(T, H, E, dt == MOE_BF16);
+  if (ws == nullptr && ws_bytes != nullptr) {
+    *ws_bytes = need;
+    return MOE_OK;
+  }
+  if (ws != nullptr && (ws_bytes == nullptr || !aligned16(ws))) return MOE_ERR_INVALID_ARG;
+  if (ws != nullptr && *ws_bytes < need) return MOE_ERR_WORKSPACE;
   if (T == 0) return MOE_OK;
   if (!x || !w_router || !topk_ids || !topk_w) return MOE_ERR_INVALID_ARG;
   if (!aligned16(x) || !aligned16(w_router) || !aligned4(topk_ids) || !aligned4(topk_w) ||
       (bias && !aligned4(bias)) || (logits_out && !aligned4(logits_out)))
     return MOE_ERR_INVALID_ARG;
   return hip_status(moe::launch_gate_topk(x, w_router, bias, T, H, E, k, dt == MOE_BF16, logits_out, topk_ids,
-                                          topk_w, stream));
+                                          topk_w, need > 0 ? ws : nullptr, stream));
 }
 
 moe_status moe_expert_histogram_scan(const int32_t* topk_ids, int T, int k, int E, const int32_t* expert_map,

@@ -750,8 +750,75 @@ __global__ __launch_bounds__(256) void combine_f32_kernel(const float4* __restri
 // ---------------------------------------------------------------------------
 // Host-side launchers (called from the C ABI after validation).
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Router top-k over K-split logits (router_logits_split_kernel): one wave per
+// token; lane g sums its columns q * 64 + g over the S slices in split order,
+// adds the bias and the wave selects as the other router kernels do.
+// ---------------------------------------------------------------------------
+template <int NV>  // E = 64 * NV
+__global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __restrict__ part, int S, int T, int k,
+                                                               const float* __restrict__ bias,
+                                                               float* __restrict__ logits, int32_t* __restrict__ ids,
+                                                               float* __restrict__ wts) {
+  constexpr int E = 64 * NV;
+  const int lane = threadIdx.x & 63;
+  const int row = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (row >= T) return;  // wave-uniform
+  float val[NV];
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    const int col = q * 64 + lane;
+    float v = part[(size_t)row * E + col];
+    for (int sp = 1; sp < S; ++sp) v = v + part[((size_t)sp * T + row) * E + col];
+    val[q] = v + (bias != nullptr ? bias[col] : 0.0f);
+  }
+  if (logits != nullptr) {
+#pragma unroll
+    for (int q = 0; q < NV; ++q) logits[(size_t)row * E + q * 64 + lane] = val[q];
+  }
+  float sel_v[kMaxTopk];
+  int sel_i[kMaxTopk];
+  topk_group<64, NV>(val, lane, E, k, sel_v, sel_i);
+  write_topk(sel_v, sel_i, lane, k, row, ids, wts);
+}
+
+static int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+  return n;
+}
+
+// Largest batch the split router takes for E = 128: beyond it the one-pass
+// kernels fill the CUs with 128-token blocks and were measured as fast (at
+// E = 256 the one-pass kernel re-reads all 256 router rows per 64 tokens, so
+// the split router takes every batch).
+constexpr int kRouterSplitMaxT128 = 4096;
+constexpr size_t kRouterSplitMaxBytes = 256ull << 20;  // partial logits at most
+
+// K ranges of the split router for T tokens (0: not used). E = 128 or 256
+// (bf16); S fills the CUs with 256-token tiles, each range >= 4 K chunks,
+// the partials within kRouterSplitMaxBytes.
+static int router_split_factor(int T, int H, int E) {
+  if ((E != 128 && E != 256) || T < 1 || H % kGateBK != 0) return 0;
+  if (E == 128 && T > kRouterSplitMaxT128) return 0;
+  const long long tiles = (T + 255) / 256;
+  const int nK = H / kGateBK;
+  long long S = device_cus() / tiles;
+  S = S < 1 ? 1 : (S > 8 ? 8 : S);
+  while (S > 1 && (nK / S < 4 || (size_t)S * T * E * 4 > kRouterSplitMaxBytes)) --S;
+  if ((size_t)S * T * E * 4 > kRouterSplitMaxBytes || nK < (int)S) return 0;
+  return (int)S;
+}
+
+size_t gate_ws_bytes(int T, int H, int E, bool bf16) {
+  if (!bf16 || T < 1) return 0;
+  const int S = router_split_factor(T, H, E);
+  return S > 0 ? (((size_t)S * T * E * 4 + 255) / 256) * 256 : 0;
+}
+
 hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, int T, int H, int E, int k,
-                            bool bf16, float* logits, int32_t* ids, float* wts, hipStream_t s) {
+                            bool bf16, float* logits, int32_t* ids, float* wts, void* ws, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (!bf16) {
     gate_topk_f32_kernel<<<(T + 3) / 4, 256, 0, s>>>(static_cast<const float*>(x),
@@ -762,6 +829,22 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
   const int ncb = (E + 31) / 32;
   const bf16_t* xb = static_cast<const bf16_t*>(x);
   const bf16_t* wb = static_cast<const bf16_t*>(wr);
+  // Many tokens over 128 or 256 experts, with a workspace: logits by K
+  // ranges, then the top-k pass.
+  if (ws != nullptr) {
+    const int S = router_split_factor(T, H, E);
+    if (S > 0) {
+      float* part = static_cast<float*>(ws);
+      hipError_t e = launch_router_logits_split(xb, wb, T, H, E, S, part, s);
+      if (e != hipSuccess) return e;
+      const dim3 g4((unsigned)((T + 3) / 4));
+      if (E == 256)
+        gate_topk_reduce_kernel<4><<<g4, 256, 0, s>>>(part, S, T, k, bias, logits, ids, wts);
+      else
+        gate_topk_reduce_kernel<2><<<g4, 256, 0, s>>>(part, S, T, k, bias, logits, ids, wts);
+      return hipGetLastError();
+    }
+  }
   // Small batches of few experts: 32-token blocks whose waves stream
   // contiguous shares of the K range (NW waves, GK k-steps per load group).
   if (ncb <= 4 && T <= kSmallRouterT) {

@@ -67,14 +67,41 @@ MISALIGNED = ctypes.c_void_p(0x10004)
     (4, 128, 8, 2, 7, INVALID),     # bad dtype
 ])
 def test_gate_topk_validation(L, T, H, E, k, dt, expect):
-    st = L.moe_gate_topk(FAKE, FAKE, None, T, H, E, k, dt, None, FAKE, FAKE, None)
+    st = L.moe_gate_topk(FAKE, FAKE, None, T, H, E, k, dt, None, FAKE, FAKE, None, None, None)
     assert st == expect
 
 
+def test_gate_topk_workspace(L):
+    """The router's workspace: a size query that launches nothing, 0 where it
+    is not used, and the size checked when one is given."""
+    n = ctypes.c_size_t(123)
+    assert L.moe_gate_topk(None, None, None, 16384, 7168, 256, 8, 1, None, None, None, None, ctypes.byref(n),
+                           None) == 0
+    big = n.value
+    assert big >= 16384 * 256 * 4 and big % 256 == 0
+    for T, H, E in ((1, 2048, 128), (128, 2048, 128), (4096, 5120, 128), (512, 7168, 256)):
+        assert L.moe_gate_topk(None, None, None, T, H, E, 1, 1, None, None, None, None, ctypes.byref(n),
+                               None) == 0
+        assert n.value >= T * E * 4, (T, H, E)
+    for T, H, E, dt in ((16384, 7168, 256, 0), (8192, 2048, 128, 1), (16384, 4096, 8, 1), (4096, 2048, 96, 1)):
+        n = ctypes.c_size_t(123)
+        assert L.moe_gate_topk(None, None, None, T, H, E, 2, dt, None, None, None, None, ctypes.byref(n),
+                               None) == 0
+        assert n.value == 0, (T, H, E, dt)
+    n = ctypes.c_size_t(big - 1)
+    assert L.moe_gate_topk(FAKE, FAKE, None, 16384, 7168, 256, 8, 1, None, FAKE, FAKE, FAKE, ctypes.byref(n),
+                           None) == WORKSPACE
+    assert L.moe_gate_topk(FAKE, FAKE, None, 16384, 7168, 256, 8, 1, None, FAKE, FAKE, FAKE, None,
+                           None) == INVALID
+    n = ctypes.c_size_t(big)
+    assert L.moe_gate_topk(FAKE, FAKE, None, 16384, 7168, 256, 8, 1, None, FAKE, FAKE, MISALIGNED,
+                           ctypes.byref(n), None) == INVALID
+
+
 def test_gate_topk_null_and_alignment(L):
-    assert L.moe_gate_topk(None, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None) == INVALID
-    assert L.moe_gate_topk(MISALIGNED, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None) == INVALID
-    assert L.moe_gate_topk(None, None, None, 0, 128, 8, 2, 1, None, None, None, None) == 0  # T=0 no-op
+    assert L.moe_gate_topk(None, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None, None, None) == INVALID
+    assert L.moe_gate_topk(MISALIGNED, FAKE, None, 4, 128, 8, 2, 1, None, FAKE, FAKE, None, None, None) == INVALID
+    assert L.moe_gate_topk(None, None, None, 0, 128, 8, 2, 1, None, None, None, None, None, None) == 0  # T=0 no-op
 
 
 def _hist(L, emap, T=64, k=2, E=8, E_local=None, ws=FAKE, nbytes=10 ** 9):

@@ -251,6 +251,41 @@ def test_router_many_tokens(H, E, k, T):
     np.testing.assert_allclose(G.down(wts), O.topk_weights(z, rid), rtol=1e-6, atol=0)
 
 
+ROUTER_SPLIT = [
+    (7168, 256, 8, 3001),     # DSV3-shaped: 12 tiles x 8 K ranges, ragged last tile
+    (5120, 128, 1, 1030),     # Maverick-shaped, top-1: 5 tiles x 8 ranges of 10 chunks
+    (5120, 128, 1, 3000),     # Maverick-shaped: 12 tiles x 8 ranges, ragged last tile
+    (256, 256, 8, 66000),     # 258 tiles: one K range
+    (2048, 128, 8, 4096),     # Qwen3-shaped, the largest E = 128 batch it takes
+    (2048, 128, 8, 1),        # one token (a 256-row tile of one row)
+    (7168, 256, 8, 77),       # decode-sized DSV3-shaped batch
+]
+
+
+@pytest.mark.parametrize("H,E,k,T", ROUTER_SPLIT, ids=[f"H{h}-E{e}-k{k}-T{t}" for h, e, k, t in ROUTER_SPLIT])
+def test_router_split_matches_one_pass(H, E, k, T):
+    """The router with its workspace (logits summed over K ranges of
+    256-token tiles) gives the one-pass router's logits, ids and weights bit
+    for bit, and the oracle's."""
+    banner("router split", H, E, k, T, "seed 6")
+    shape = dataclasses.replace(CONFIGS["qwen3"], name="router", H=H, E=E, k=k, E_local=E)
+    x, w, b, _ = make_router(shape, T, 1.0, seed=6)
+    assert moe.gate_ws_bytes(T, H, E, torch.bfloat16) > 0
+    dx, dw, db = G.up(x, torch.bfloat16), G.up(w, torch.bfloat16), G.up(b, torch.float32)
+    i1, w1, l1 = moe.moe_gate_topk(dx, dw, db, k, logits=True)
+    i2, w2, l2 = moe.moe_gate_topk(dx, dw, db, k, logits=True, use_ws=False)
+    i3, w3, _ = moe.moe_gate_topk(dx, dw, None, k)   # no bias, no logits
+    torch.cuda.synchronize()
+    assert torch.equal(l1, l2) and torch.equal(i1, i2) and torch.equal(w1, w2)
+    z = O.router_logits(x, w, b)
+    assert np.array_equal(G.down(l1), z), "logits"
+    rid = O.topk_select(z, k)
+    assert np.array_equal(G.down(i1), rid), "ids"
+    np.testing.assert_allclose(G.down(w1), O.topk_weights(z, rid), rtol=1e-6, atol=0)
+    z0 = O.router_logits(x, w, np.zeros_like(b))
+    assert np.array_equal(G.down(i3), O.topk_select(z0, k)), "ids without bias"
+
+
 def test_router_many_tokens_ties():
     """All logits equal: every token takes experts 0..k-1 in order."""
     banner("router ties E=256 T=4096")
