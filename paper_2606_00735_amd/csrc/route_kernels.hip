@@ -675,6 +675,8 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const uint4* __restric
 // ascending slot order (no contraction, so each step rounds like the
 // definition: a product, then a sum).
 // ---------------------------------------------------------------------------
+constexpr int kCombineVecs = 4;  // 16-byte row vectors per lane and slot in flight
+
 __global__ __launch_bounds__(256) void combine_bf16_kernel(const uint4* __restrict__ y, const float* __restrict__ w,
                                                            const int32_t* __restrict__ dest, int T, int k,
                                                            int row_vecs, int M_cap, uint4* __restrict__ out) {
@@ -694,32 +696,50 @@ __global__ __launch_bounds__(256) void combine_bf16_kernel(const uint4* __restri
       wt[j] = w[(size_t)t * k + j];
     }
   }
-  for (int v = lane; v < row_vecs; v += kWave) {
-    float acc[8];
+  // each lane keeps kCombineVecs row vectors (kWave apart) of every slot in
+  // flight; slots are still summed in ascending order per element
+  for (int v0 = lane; v0 < row_vecs; v0 += kCombineVecs * kWave) {
+    float acc[kCombineVecs][8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = 0.0f;
+    for (int u = 0; u < kCombineVecs; ++u)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[u][q] = 0.0f;
 #pragma unroll
     for (int j = 0; j < kMaxTopk; ++j) {
       if (j < k && d[j] >= 0) {
-        const uint4 yv = y[(size_t)d[j] * row_vecs + v];
-        const uint32_t u[4] = {yv.x, yv.y, yv.z, yv.w};
+        uint4 yv[kCombineVecs];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float lo = __uint_as_float(u[q] << 16);
-          const float hi = __uint_as_float(u[q] & 0xffff0000u);
-          const float plo = wt[j] * lo;
-          const float phi = wt[j] * hi;
-          acc[2 * q] = acc[2 * q] + plo;
-          acc[2 * q + 1] = acc[2 * q + 1] + phi;
+        for (int u = 0; u < kCombineVecs; ++u) {
+          const int v = v0 + u * kWave;
+          yv[u] = v < row_vecs ? y[(size_t)d[j] * row_vecs + v] : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kCombineVecs; ++u) {
+          const uint32_t w4[4] = {yv[u].x, yv[u].y, yv[u].z, yv[u].w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float lo = __uint_as_float(w4[q] << 16);
+            const float hi = __uint_as_float(w4[q] & 0xffff0000u);
+            const float plo = wt[j] * lo;
+            const float phi = wt[j] * hi;
+            acc[u][2 * q] = acc[u][2 * q] + plo;
+            acc[u][2 * q + 1] = acc[u][2 * q + 1] + phi;
+          }
         }
       }
     }
-    uint4 o;
-    o.x = pack_bf16x2(acc[0], acc[1]);
-    o.y = pack_bf16x2(acc[2], acc[3]);
-    o.z = pack_bf16x2(acc[4], acc[5]);
-    o.w = pack_bf16x2(acc[6], acc[7]);
-    out[(size_t)t * row_vecs + v] = o;
+#pragma unroll
+    for (int u = 0; u < kCombineVecs; ++u) {
+      const int v = v0 + u * kWave;
+      if (v < row_vecs) {
+        uint4 o;
+        o.x = pack_bf16x2(acc[u][0], acc[u][1]);
+        o.y = pack_bf16x2(acc[u][2], acc[u][3]);
+        o.z = pack_bf16x2(acc[u][4], acc[u][5]);
+        o.w = pack_bf16x2(acc[u][6], acc[u][7]);
+        out[(size_t)t * row_vecs + v] = o;
+      }
+    }
   }
 }
 
