@@ -689,9 +689,22 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   constexpr int CK = MX ? kMxChunk : kBK;  // K elements per chunk
   constexpr int EB = MX ? 1 : 2;           // weight bytes per element (MX scales aside)
   const int nK = a.K / CK;
+  // K ranges the tail split (below) cuts each tile of the last round of an
+  // unsplit launch of `tot` tiles of `tcols` columns into (1: none)
+  auto tail_ranges = [&](int tot, int tcols) {
+    const int r = tot % G;
+    int st = r > 0 ? G / r : 1;
+    if (st > kMaxSplit) st = kMaxSplit;
+    const long long per = (long long)NB * 256 * tcols;  // floats of one split tile
+    while (st > 1 && (st * kMinSplitChunks > nK || (long long)st * r * per > a.part_cap)) --st;
+    return (st > 1 && 3 * r <= a.plan_rows) ? st : 1;
+  };
   int S = 1;
   if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
+    // unsplit with full rounds: the tail split shortens the last round
+    const int st1 = T0 >= G ? tail_ranges(T0, 128) : 1;
+    if (st1 > 1) best = (long long)(T0 / G) * (nK + kSplitOverhead) + (nK + st1 - 1) / st1 + kSplitOverhead;
     for (int sp = 2; sp <= kMaxSplit && sp * kMinSplitChunks <= nK; ++sp) {
       // partials must fit, and their fp32 write + read must not outweigh the
       // weights the launch streams (large row tiles are compute bound)
@@ -714,15 +727,8 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // launch, which finds each tile's rows and columns in the plan.
   int St = 1, rem = 0;
   if (S == 1 && a.part != nullptr && total > 0) {
-    const int r = total % G;
-    int st = r > 0 ? G / r : 1;
-    if (st > kMaxSplit) st = kMaxSplit;
-    const long long per = (long long)NB * 256 * cols;  // floats of one split tile
-    while (st > 1 && (st * kMinSplitChunks > nK || (long long)st * r * per > a.part_cap)) --st;
-    if (st > 1 && 3 * r <= a.plan_rows) {
-      St = st;
-      rem = r;
-    }
+    St = tail_ranges(total, cols);
+    rem = St > 1 ? total % G : 0;
   }
   const int full = total - rem;
   const int n_items = full + rem * St;
