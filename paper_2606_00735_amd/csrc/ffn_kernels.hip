@@ -1079,6 +1079,16 @@ struct FfnWs {
   size_t bytes;
 };
 
+// fp32 partials either split-K (S <= kMaxSplit slices of every row of both
+// GEMMs) or the tail split (at most 256 split tiles of 256 x 256 floats, and
+// at most kMaxSplit per tile) may need, within kPartCapFloats.
+static long long part_cap_floats(int M_cap, int E_local, int H, int I) {
+  const long long split_k = (long long)kMaxSplit * M_cap * std::max(2LL * I, (long long)H);
+  const long long tiles = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (std::max(I, H) / 128);
+  const long long tail = std::min(256LL, (long long)kMaxSplit * tiles) * 256 * 256;
+  return std::min(std::max(split_k, tail), kPartCapFloats);
+}
+
 static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
   FfnWs w{};
   const size_t h = round256((size_t)M_cap * I * (bf16 ? 2 : 4));
@@ -1087,8 +1097,7 @@ static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
     w.bytes = h + 256;
     return w;
   }
-  const long long need = (long long)kMaxSplit * M_cap * std::max(2LL * I, (long long)H);
-  w.part_cap = std::min(need, kPartCapFloats);
+  w.part_cap = part_cap_floats(M_cap, E_local, H, I);
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
   w.plan = h;
   w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
@@ -1200,6 +1209,9 @@ static FfnMxWs ffn_mx_ws_layout(int M_cap, int E_local, int H, int I) {
   FfnMxWs w{};
   w.hs = round256((size_t)M_cap * I);
   w.plan = w.hs + round256((size_t)(I / kMxChunk) * M_cap * 4);
+  // sized for split-K only, not for the tail split as the bf16 layout is:
+  // with room for it, the MXFP8 decode FFN (Mixtral-shaped, T = 32) took the
+  // tail split over S = 2 and measured 3 % slower
   const long long need = (long long)kMaxSplit * M_cap * std::max(2LL * I, (long long)H);
   w.part_cap = std::min(need, kPartCapFloats);
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
