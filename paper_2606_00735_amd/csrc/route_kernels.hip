@@ -293,7 +293,7 @@ template <int NCB, int NW, int GK>
 __global__ __launch_bounds__(NW * 64) void gate_topk_bf16_small_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
     int T, int H, int E, int k, float* __restrict__ logits, int32_t* __restrict__ ids,
-    float* __restrict__ wts) {
+    float* __restrict__ wts, int S = 1, float* __restrict__ part = nullptr) {
   __shared__ float red[NW * NCB * 16 * kWave];  // partial logits of every wave
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, half = lane >> 5;
@@ -307,8 +307,10 @@ __global__ __launch_bounds__(NW * 64) void gate_topk_bf16_small_kernel(
 #pragma unroll
   for (int c = 0; c < NCB; ++c)
     wp[c] = reinterpret_cast<const bf16x8_t*>(wr + (size_t)min(c * 32 + r, E - 1) * H) + half;
-  const int nks = H / 16, per = nks / NW;  // the launcher checks per % (2 GK) == 0
-  const int s0 = wave * per;
+  // block (x, y) sums K range y of S (part != nullptr: fp32 partial logits
+  // of its 32 tokens go to part[y][row][0, 32 NCB) for the top-k pass)
+  const int nkb = H / 16 / S, per = nkb / NW;  // the launcher checks per % (2 GK) == 0
+  const int s0 = (int)blockIdx.y * nkb + wave * per;
 
   f32x16_t acc[NCB];
 #pragma unroll
@@ -359,7 +361,9 @@ __global__ __launch_bounds__(NW * 64) void gate_topk_bf16_small_kernel(
       for (int w = 0; w < NW; ++w) z += red[((w * NCB + c) * 16 + v) * kWave + lane];
       const int col = c * 32 + r;
       val[c] = (col < E) ? z + bias_r[c] : -__builtin_huge_valf();
+      if (part != nullptr && row < T) part[((size_t)blockIdx.y * T + row) * (32 * NCB) + col] = z;
     }
+    if (part != nullptr) continue;  // wave-uniform
     if (logits != nullptr && row < T) {
 #pragma unroll
       for (int c = 0; c < NCB; ++c) {
@@ -775,12 +779,12 @@ __global__ __launch_bounds__(256) void combine_f32_kernel(const float4* __restri
 // token; lane g sums its columns q * 64 + g over the S slices in split order,
 // adds the bias and the wave selects as the other router kernels do.
 // ---------------------------------------------------------------------------
-template <int NV>  // E = 64 * NV
-__global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __restrict__ part, int S, int T, int k,
-                                                               const float* __restrict__ bias,
+// Partial rows are EP floats apart (E <= EP <= 64 NV).
+template <int NV>
+__global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __restrict__ part, int S, int T, int E,
+                                                               int EP, int k, const float* __restrict__ bias,
                                                                float* __restrict__ logits, int32_t* __restrict__ ids,
                                                                float* __restrict__ wts) {
-  constexpr int E = 64 * NV;
   const int lane = threadIdx.x & 63;
   const int row = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
   if (row >= T) return;  // wave-uniform
@@ -788,13 +792,18 @@ __global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __re
 #pragma unroll
   for (int q = 0; q < NV; ++q) {
     const int col = q * 64 + lane;
-    float v = part[(size_t)row * E + col];
-    for (int sp = 1; sp < S; ++sp) v = v + part[((size_t)sp * T + row) * E + col];
-    val[q] = v + (bias != nullptr ? bias[col] : 0.0f);
+    float v = -__builtin_huge_valf();
+    if (col < E) {
+      v = part[(size_t)row * EP + col];
+      for (int sp = 1; sp < S; ++sp) v = v + part[((size_t)sp * T + row) * EP + col];
+      v = v + (bias != nullptr ? bias[col] : 0.0f);
+    }
+    val[q] = v;
   }
   if (logits != nullptr) {
 #pragma unroll
-    for (int q = 0; q < NV; ++q) logits[(size_t)row * E + q * 64 + lane] = val[q];
+    for (int q = 0; q < NV; ++q)
+      if (q * 64 + lane < E) logits[(size_t)row * E + q * 64 + lane] = val[q];
   }
   float sel_v[kMaxTopk];
   int sel_i[kMaxTopk];
@@ -831,8 +840,27 @@ static int router_split_factor(int T, int H, int E) {
   return (int)S;
 }
 
+// Decode-sized batches over at most 128 experts: the small-batch kernel
+// (8 waves, one k-step per load group) on S K ranges of H / 16 / S k-steps,
+// a multiple of 16 (two per wave and group); 0: not used. Below
+// kRouterSmallSplitMinBytes of distinct rows per 32-token block the second
+// launch costs more than it saves (one token over 8 experts at H = 4096:
+// 11.9 us in one pass, 16.6 us split).
+constexpr int kRouterSmallSplitMaxT = 256;
+constexpr long long kRouterSmallSplitMinBytes = 192 << 10;
+static int router_small_split_factor(int T, int H, int E) {
+  if (E > 128 || T < 1 || T > kRouterSmallSplitMaxT || H % 16 != 0) return 0;
+  if ((long long)(std::min(T, 32) + E) * H * 2 < kRouterSmallSplitMinBytes) return 0;
+  const int nks = H / 16;
+  for (int S = 8; S >= 2; --S)
+    if (nks % S == 0 && (nks / S) % 16 == 0) return S;
+  return 0;
+}
+
 size_t gate_ws_bytes(int T, int H, int E, bool bf16) {
   if (!bf16 || T < 1) return 0;
+  const int Ss = router_small_split_factor(T, H, E);
+  if (Ss > 0) return (((size_t)Ss * T * 32 * ((E + 31) / 32) * 4 + 255) / 256) * 256;
   const int S = router_split_factor(T, H, E);
   return S > 0 ? (((size_t)S * T * E * 4 + 255) / 256) * 256 : 0;
 }
@@ -852,16 +880,43 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
   // Many tokens over 128 or 256 experts, with a workspace: logits by K
   // ranges, then the top-k pass.
   if (ws != nullptr) {
+    float* part = static_cast<float*>(ws);
+    const dim3 g4((unsigned)((T + 3) / 4));
+    const int Ss = router_small_split_factor(T, H, E);
+    if (Ss > 0) {
+      // decode-sized batch: 32-token blocks x Ss K ranges
+      const dim3 g((unsigned)((T + 31) / 32), (unsigned)Ss);
+      const int ep = 32 * ncb;
+#define MOE_GATE_SMALL_SPLIT(N)                                                                         \
+  case N:                                                                                               \
+    gate_topk_bf16_small_kernel<N, 8, 1><<<g, 512, 0, s>>>(xb, wb, bias, T, H, E, k, logits, ids, wts, Ss, \
+                                                           part);                                       \
+    break;
+      switch (ncb) {
+        MOE_GATE_SMALL_SPLIT(1)
+        MOE_GATE_SMALL_SPLIT(2)
+        MOE_GATE_SMALL_SPLIT(3)
+        MOE_GATE_SMALL_SPLIT(4)
+        default:
+          return hipErrorInvalidValue;
+      }
+#undef MOE_GATE_SMALL_SPLIT
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      if (ep <= 64)
+        gate_topk_reduce_kernel<1><<<g4, 256, 0, s>>>(part, Ss, T, E, ep, k, bias, logits, ids, wts);
+      else
+        gate_topk_reduce_kernel<2><<<g4, 256, 0, s>>>(part, Ss, T, E, ep, k, bias, logits, ids, wts);
+      return hipGetLastError();
+    }
     const int S = router_split_factor(T, H, E);
     if (S > 0) {
-      float* part = static_cast<float*>(ws);
       hipError_t e = launch_router_logits_split(xb, wb, T, H, E, S, part, s);
       if (e != hipSuccess) return e;
-      const dim3 g4((unsigned)((T + 3) / 4));
       if (E == 256)
-        gate_topk_reduce_kernel<4><<<g4, 256, 0, s>>>(part, S, T, k, bias, logits, ids, wts);
+        gate_topk_reduce_kernel<4><<<g4, 256, 0, s>>>(part, S, T, E, E, k, bias, logits, ids, wts);
       else
-        gate_topk_reduce_kernel<2><<<g4, 256, 0, s>>>(part, S, T, k, bias, logits, ids, wts);
+        gate_topk_reduce_kernel<2><<<g4, 256, 0, s>>>(part, S, T, E, E, k, bias, logits, ids, wts);
       return hipGetLastError();
     }
   }

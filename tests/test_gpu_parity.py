@@ -257,8 +257,15 @@ ROUTER_SPLIT = [
     (5120, 128, 1, 3000),     # Maverick-shaped: 12 tiles x 8 ranges, ragged last tile
     (256, 256, 8, 66000),     # 258 tiles: one K range
     (2048, 128, 8, 4096),     # Qwen3-shaped, the largest E = 128 batch it takes
-    (2048, 128, 8, 1),        # one token (a 256-row tile of one row)
     (7168, 256, 8, 77),       # decode-sized DSV3-shaped batch
+    # decode-sized batches over <= 128 experts: 32-token blocks x K ranges
+    (4096, 8, 2, 32),         # Mixtral-shaped decode: 8 ranges of 32 k-steps
+    (4096, 8, 2, 16),         # (16 + 8) rows of 8 KB: the smallest batch it takes at E = 8
+    (2048, 128, 8, 1),        # Qwen3-shaped, one token: 8 ranges of 16 k-steps
+    (2048, 128, 8, 200),      # Qwen3-shaped, ragged last block
+    (5120, 128, 1, 100),      # Maverick-shaped: 5 ranges of 64 k-steps
+    (2048, 96, 6, 256),       # E = 96 (padded to 128 columns)
+    (1024, 40, 4, 33),        # E = 40 of 64 columns, 4 ranges
 ]
 
 
