@@ -265,7 +265,7 @@ ROUTER_SPLIT = [
     (2048, 128, 8, 200),      # Qwen3-shaped, ragged last block
     (5120, 128, 1, 100),      # Maverick-shaped: 5 ranges of 64 k-steps
     (2048, 96, 6, 256),       # E = 96 (padded to 128 columns)
-    (1024, 40, 4, 33),        # E = 40 of 64 columns, 4 ranges
+    (1536, 40, 4, 33),        # E = 40 of 64 columns, 6 ranges of 16 k-steps
 ]
 
 
