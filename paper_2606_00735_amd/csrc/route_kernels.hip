@@ -576,6 +576,38 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
   }
 }
 
+// One count block (T <= kTokPerBlk): the counts, the local offsets and the
+// block's row bases in one launch (the count table is not needed).
+__global__ __launch_bounds__(256) void hist_scan_one_block_kernel(const int32_t* __restrict__ ids, int T, int k,
+                                                                  SlotMap map, int32_t* __restrict__ counts,
+                                                                  int32_t* __restrict__ offsets,
+                                                                  int32_t* __restrict__ bases,
+                                                                  int32_t* __restrict__ m_loc) {
+  __shared__ int cnt[kMaxExperts];
+  __shared__ int s_tot[4];
+  const int tid = threadIdx.x;
+  const int E = map.n_experts, L = map.n_local;
+  for (int e = tid; e < E; e += 256) cnt[e] = 0;
+  __syncthreads();
+  for (int p = tid; p < T * k; p += 256) {
+    const int e = ids[p];
+    if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += 256) counts[e] = cnt[e];
+  const int v = tid < L ? cnt[map.expert_of[tid]] : 0;
+  int total;
+  const int excl = block_exclusive_scan_256(v, s_tot, &total);
+  if (tid < L) {
+    offsets[tid + 1] = excl + v;
+    bases[tid] = excl;
+  }
+  if (tid == 0) {
+    offsets[0] = 0;
+    *m_loc = total;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Dispatch permutation, step 1: positions. Block b re-reads the ids of its
 // kTokPerBlk tokens in rounds of 256 (one token per thread). The rank of an
@@ -1026,6 +1058,10 @@ hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map
   const int n_blk = (T + kTokPerBlk - 1) / kTokPerBlk;
   int32_t *table, *bases, *m_loc;
   hist_ws_split(ws, T, map.n_experts, map.n_local, &table, &bases, &m_loc);
+  if (n_blk == 1) {
+    hist_scan_one_block_kernel<<<1, 256, 0, s>>>(ids, T, k, map, counts, offsets, bases, m_loc);
+    return hipGetLastError();
+  }
   if (n_blk > 0) {
     hist_kernel<<<n_blk, 256, 0, s>>>(ids, T, k, map.n_experts, table);
     hipError_t e = hipGetLastError();
