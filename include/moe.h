@@ -82,16 +82,22 @@ int moe_abi_version(void);
  * topk_w     [T, k]  fp32        gate weights
  * Limits: 1 <= E <= 256, 1 <= k <= min(E, 16), H % 8 == 0 (bf16: H % 64 == 0).
  * ws         optional workspace: with ws == NULL and ws_bytes != NULL the
- *            call stores the byte count in *ws_bytes and launches nothing
- *            (the count is 0 where no workspace is used: fp32, E other than
- *            128 or 256, E = 128 with more than 4096 tokens); with ws and
- *            ws_bytes both
- *            NULL the router runs without it. Given one (16-byte aligned,
- *            *ws_bytes at least the count, else MOE_ERR_WORKSPACE), bf16
- *            routers over 128 or 256 experts sum the logits over K ranges of
- *            256-token tiles into fp32 partials there and add them in a fixed
- *            order, so a CU loads 256 tokens' rows and a K range of the router
- *            rows instead of every router row for each 64 tokens.
+ *            call stores the byte count in *ws_bytes and launches nothing;
+ *            with ws and ws_bytes both NULL the router runs in one pass
+ *            without it. Given one (16-byte aligned, *ws_bytes at least the
+ *            count, else MOE_ERR_WORKSPACE), bf16 routers compute the logits
+ *            as fp32 partial sums over K ranges there and add them in a
+ *            fixed order before the top-k:
+ *              - batches of at most 256 tokens over at most 128 experts
+ *                (when a 32-token block's distinct x and router rows reach
+ *                192 KB): 32-token blocks times up to 8 K ranges;
+ *              - 256 experts (any batch) or 128 experts (up to 4096 tokens):
+ *                256-token tiles times K ranges, so a CU loads 256 tokens'
+ *                rows and a K range of the router rows instead of every
+ *                router row for each 64 tokens.
+ *            The count is 0 where no workspace is used (fp32 and every other
+ *            case). It depends on the device's compute-unit count: query it
+ *            with the device the call will run on current.
  * T == 0 is a no-op. The kernel accumulates in fp32; inputs whose products
  * and partial sums are exact in fp32 give order-independent logits (and the
  * same logits with or without the workspace).
