@@ -91,7 +91,8 @@ int moe_abi_version(void);
  *              - batches of at most 256 tokens over at most 128 experts
  *                (when a 32-token block's distinct x and router rows reach
  *                192 KB): 32-token blocks times up to 8 K ranges;
- *              - 256 experts (any batch) or 128 experts (up to 4096 tokens):
+ *              - 256 experts (any batch) or 128 experts (up to 4096 tokens,
+ *                8192 when H >= 4096):
  *                256-token tiles times K ranges, so a CU loads 256 tokens'
  *                rows and a K range of the router rows instead of every
  *                router row for each 64 tokens.

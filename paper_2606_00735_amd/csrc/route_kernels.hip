@@ -811,7 +811,9 @@ __global__ __launch_bounds__(256) void combine_f32_kernel(const float4* __restri
 // token; lane g sums its columns q * 64 + g over the S slices in split order,
 // adds the bias and the wave selects as the other router kernels do.
 // ---------------------------------------------------------------------------
-// Partial rows are EP floats apart (E <= EP <= 64 NV).
+constexpr int kMaxRouterSplit = 8;  // K ranges of the split routers, at most
+
+// Partial rows are EP floats apart (E <= EP <= 64 NV); 1 <= S <= 8.
 template <int NV>
 __global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __restrict__ part, int S, int T, int E,
                                                                int EP, int k, const float* __restrict__ bias,
@@ -826,8 +828,15 @@ __global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __re
     const int col = q * 64 + lane;
     float v = -__builtin_huge_valf();
     if (col < E) {
-      v = part[(size_t)row * EP + col];
-      for (int sp = 1; sp < S; ++sp) v = v + part[((size_t)sp * T + row) * EP + col];
+      // every slice's load in flight at once, then the sum in split order
+      float p[kMaxRouterSplit];
+#pragma unroll
+      for (int sp = 0; sp < kMaxRouterSplit; ++sp)
+        p[sp] = sp < S ? part[((size_t)sp * T + row) * EP + col] : 0.0f;
+      v = p[0];
+#pragma unroll
+      for (int sp = 1; sp < kMaxRouterSplit; ++sp)
+        if (sp < S) v = v + p[sp];
       v = v + (bias != nullptr ? bias[col] : 0.0f);
     }
     val[q] = v;
@@ -850,11 +859,16 @@ static int device_cus() {
   return n;
 }
 
-// Largest batch the split router takes for E = 128: beyond it the one-pass
-// kernels fill the CUs with 128-token blocks and were measured as fast (at
-// E = 256 the one-pass kernel re-reads all 256 router rows per 64 tokens, so
-// the split router takes every batch).
+// Largest batch the split router takes for E = 128 (kRouterSplitMaxT128, or
+// kRouterSplitMaxT128Wide for rows of at least 4096 elements): beyond it
+// the one-pass kernels fill the CUs with 128-token blocks and were measured
+// as fast or faster with the last-level cache flushed before each call
+// (H = 5120: 8192 tokens 56 us split vs 83 one pass, 32768 tokens 152 vs
+// 144; H = 2048: 8192 tokens 46 vs 46, 16384 tokens 69 vs 64). At E = 256
+// the one-pass kernel re-reads all 256 router rows per 64 tokens, so the
+// split router takes every batch.
 constexpr int kRouterSplitMaxT128 = 4096;
+constexpr int kRouterSplitMaxT128Wide = 8192;
 constexpr size_t kRouterSplitMaxBytes = 256ull << 20;  // partial logits at most
 
 // K ranges of the split router for T tokens (0: not used). E = 128 or 256
@@ -862,7 +876,7 @@ constexpr size_t kRouterSplitMaxBytes = 256ull << 20;  // partial logits at most
 // the partials within kRouterSplitMaxBytes.
 static int router_split_factor(int T, int H, int E) {
   if ((E != 128 && E != 256) || T < 1 || H % kGateBK != 0) return 0;
-  if (E == 128 && T > kRouterSplitMaxT128) return 0;
+  if (E == 128 && T > (H >= 4096 ? kRouterSplitMaxT128Wide : kRouterSplitMaxT128)) return 0;
   const long long tiles = (T + 255) / 256;
   const int nK = H / kGateBK;
   long long S = device_cus() / tiles;
