@@ -852,6 +852,7 @@ __global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __re
   write_topk(sel_v, sel_i, lane, k, row, ids, wts);
 }
 
+// Compute units of the current device (256 if the runtime cannot say).
 static int device_cus() {
   int dev = 0, n = 0;
   if (hipGetDevice(&dev) != hipSuccess) return 256;
@@ -1009,11 +1010,7 @@ hipError_t launch_gate_topk(const void* x, const void* wr, const float* bias, in
   // More than 32 experts: 8-wave blocks of 64 tokens (E_pad of 128 or 256)
   // when they have each CU load fewer rows than 128-token blocks.
   if (ncb > 1) {
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess) {
-      int n = 0;
-      if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) cus = n;
-    }
+    const int cus = device_cus();
     const int ep = ncb <= 4 ? 128 : 256;
     auto rows_per_cu = [&](int bt) {
       const long long blocks = (T + bt - 1) / bt;
@@ -1097,10 +1094,7 @@ hipError_t launch_permute(const void* x, const int32_t* ids, const SlotMap& map,
   // x_perm == nullptr: positions only (the FFN gathers the rows itself)
   if (e != hipSuccess || map.n_local == 0 || M_cap == 0 || x_perm == nullptr) return e;
   const int row_vecs = (H * (bf16 ? 2 : 4)) / 16;
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    cus = 256;
+  const int cus = device_cus();
   const long long want = ((long long)M_cap + 3) / 4;
   const unsigned grid = (unsigned)std::min<long long>(want, (long long)cus * 8);
   gather_rows_kernel<<<grid, 256, 0, s>>>(static_cast<const uint4*>(x), row_vecs, T, k, perm_src, m_loc, M_cap,
