@@ -42,8 +42,11 @@ REDUCED = [
     ("qwen3", 200, 1.0),
     ("qwen3", 256, 1.5),
     ("dsv3_shard", 512, 0.0),
+    ("dsv3_shard", 512, 1.0),
     ("dsv3_shard", 384, 1.5),
+    ("maverick_shard", 1024, 0.0),
     ("maverick_shard", 1024, 1.0),
+    ("maverick_shard", 1024, 1.5),
 ]
 
 
