@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 2
+#define MOE_ABI_VERSION 3
 #define MOE_MAX_EXPERTS 256 /* E and E_local limit */
 #define MOE_MAX_TOPK 16
 
@@ -174,11 +174,23 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  * offsets      [E_local+1] int32 (device, from moe_expert_histogram_scan);
  *              clamped to [0, M_cap] inside the kernels
  * y_perm       [M_cap, H] dt, rows [0, offsets[E_local]) written
- * ws           holds h [M_cap, I] dt; for bf16 also the fp32 partial sums
- *              of split-K tiles (used when every expert has at most 64
- *              rows, or for the tiles of a last, at most half-full round of
- *              tiles; summed in a fixed order, so results are deterministic)
- *              and the GEMMs' per-XCD tile counters (cleared by the call)
+ * ws           holds h [M_cap, I] dt; for bf16 also work counters, the
+ *              fp32 partial sums of tiles split along K (summed in a fixed
+ *              order, so results are deterministic) and a split plan.
+ *              bf16: the workspace's first 16 KiB are counters that must be
+ *              zero before the first call that uses the workspace (allocate
+ *              it zero-filled); every call leaves them zero again. Calls on
+ *              one workspace must not overlap.
+ *              Schedule (bf16): when no expert has more than 32 rows each
+ *              GEMM's (tile, K chunk) units are dealt to the CUs in equal
+ *              shares and tiles split between CUs are finished inside the
+ *              GEMM launch; otherwise whole tiles run in rounds, with
+ *              split-K for tile-starved launches and a split of a partly
+ *              filled last round, whose partials a launch after each GEMM
+ *              sums. When no expert can have more than 32 rows (M_cap <= 32;
+ *              for the _gather variant min(T, M_cap) <= 32, since a token
+ *              adds at most one row to an expert) those launches are left
+ *              out: two kernel launches in all.
  * Limits: 0 <= E_local <= 256 (0 is a no-op); bf16: H % 128 == 0 and
  * I % 128 == 0; fp32: H % 4 == 0 and I % 4 == 0.
  */
@@ -338,7 +350,8 @@ moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, cons
  * w_gate, w_up [n_rot, I, H]; w_down [n_rot, H, I]   dt, rows strided by
  *          ldw_gu and ldw_dn as in moe_grouped_swiglu_ffn (0: dense)
  * y_scratch [maxM, H] dt       output rows (contents unspecified afterwards)
- * ws       workspace for maxM (query with ws == NULL)
+ * ws       workspace for maxM (query with ws == NULL); bf16: zero-filled
+ *          before its first use, as for moe_grouped_swiglu_ffn
  * us_out   HOST [nM]: median microseconds per run
  * us_all   HOST [nM * iters] or NULL: every timed run, in order
  * Blocks the calling thread until the sweep is done. Limits: 1 <= nM <= 64,

@@ -12,6 +12,7 @@ marshals torch tensors into those calls.
 """
 from ._lib import (  # noqa: F401
     EXPORTED,
+    FFN_COUNTER_BYTES,
     LIB_PATH,
     MoeError,
     MxTensor,

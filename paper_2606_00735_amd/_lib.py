@@ -95,7 +95,7 @@ def load_library(path: str = LIB_PATH):
     L.moe_grouped_swiglu_ffn_mx.restype = _I
     L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _PSZ,
                                             _P]
-    if L.moe_abi_version() != 2:
+    if L.moe_abi_version() != 3:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
     return L
@@ -316,7 +316,7 @@ def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_per
     dt = _dtype_code(x_perm)
     need = ffn_ws_bytes(E_local, H, I, M_cap, x_perm.dtype)
     if ws is None:
-        ws = torch.empty(need, dtype=torch.uint8, device=x_perm.device)
+        ws = torch.zeros(need, dtype=torch.uint8, device=x_perm.device)  # counters start at zero
     y_perm = torch.empty((M_cap, H), dtype=x_perm.dtype, device=x_perm.device) if y_perm is None else y_perm
     n = ctypes.c_size_t(ws.numel() * ws.element_size())
     pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x_perm.dtype)
@@ -343,7 +343,7 @@ def moe_grouped_swiglu_ffn_gather(x, perm_src, k, w_gate, w_up, w_down, offsets,
     dt = _dtype_code(x)
     need = ffn_ws_bytes(E_local, H, I, M_cap, x.dtype)
     if ws is None:
-        ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+        ws = torch.zeros(need, dtype=torch.uint8, device=x.device)  # counters start at zero
     y_perm = torch.empty((M_cap, H), dtype=x.dtype, device=x.device) if y_perm is None else y_perm
     n = ctypes.c_size_t(ws.numel() * ws.element_size())
     pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x.dtype)
@@ -384,7 +384,7 @@ def moe_load_sweep(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch=No
                           warmup, iters, None, None, ctypes.byref(n), None, None, None)
     _check("moe_load_sweep", st)
     if ws is None:
-        ws = torch.empty(n.value, dtype=torch.uint8, device=x.device)
+        ws = torch.zeros(n.value, dtype=torch.uint8, device=x.device)  # counters start at zero
     if y_scratch is None:
         y_scratch = torch.empty((max_m, H), dtype=x.dtype, device=x.device)
     us = np.zeros(nM, np.float32)
@@ -440,10 +440,14 @@ def moe_layer(x, w_router, bias, k, expert_map, w_gate, w_up, w_down, logits=Fal
                 perm_src=perm_src, dest=dest, y_perm=y_perm, h=fws, out=out)
 
 
+FFN_COUNTER_BYTES = 16384  # bf16 FFN workspace: counters first, then h
+
+
 def ffn_hidden(ws, M_cap, I, dtype):
     """View of the expert hidden activations h [M_cap, I] held in an FFN workspace."""
     es = 2 if dtype == torch.bfloat16 else 4
-    return ws[: M_cap * I * es].view(dtype).view(M_cap, I)
+    off = FFN_COUNTER_BYTES if dtype == torch.bfloat16 else 0
+    return ws[off: off + M_cap * I * es].view(dtype).view(M_cap, I)
 
 
 # ---------------------------------------------------------------------------

@@ -27,13 +27,26 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: a ROCm toolchain is required to build libmoe")
 
 
+FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wall", "-Wno-unused-function"]
+
+
 def command(out: str = LIB, extra=()) -> list:
+    """One hipcc command that compiles and links every source."""
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    return [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-Wall", "-Wno-unused-function",
-            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+    return [hipcc(), *FLAGS, "-shared", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
             "-x", "hip", *srcs, *extra, "-o", out]
+
+
+def compile_commands(objdir: str) -> list:
+    """(object path, hipcc command) per source, for a parallel build."""
+    out = []
+    for s in SOURCES:
+        obj = os.path.join(objdir, s + ".o")
+        out.append((obj, [hipcc(), *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+                          "-x", "hip", "-c", os.path.join(CSRC, s), "-o", obj]))
+    return out
 
 
 STAMP = LIB + ".srchash"
@@ -60,10 +73,7 @@ def is_fresh() -> bool:
         return False
 
 
-def build(verbose: bool = False) -> str:
-    """Compile libmoe.so next to this file; returns its path."""
-    tmp = LIB + ".tmp"
-    cmd = command(tmp)
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -73,6 +83,19 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile libmoe.so next to this file (one hipcc per source, in
+    parallel, then a link step); returns its path."""
+    import concurrent.futures as cf
+    import tempfile
+    tmp = LIB + ".tmp"
+    with tempfile.TemporaryDirectory(prefix="libmoe_build_") as objdir:
+        jobs = compile_commands(objdir)
+        with cf.ThreadPoolExecutor(len(jobs)) as ex:
+            list(ex.map(lambda j: _run(j[1], verbose), jobs))
+        _run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *[o for o, _ in jobs], "-o", tmp], verbose)
     os.replace(tmp, LIB)
     with open(STAMP, "w") as fh:
         fh.write(source_hash())

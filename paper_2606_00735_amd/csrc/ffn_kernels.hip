@@ -84,6 +84,20 @@ struct GemmArgs {
   // MXFP8 codes), >= K; expert e's matrix starts at row e * N. A stride off
   // a power of two spreads a tile's rows over more HBM channels.
   int ldb;
+  // Counter of finished blocks for the reset of the work counters (zero
+  // before the launch; the last block to finish zeroes it and the queue), or
+  // nullptr.
+  int32_t* done;
+  // Decode schedule (bf16; see decode_schedule): with sk != 0 a launch in
+  // which every expert has at most sk_rows rows takes it; skpart
+  // holds two fp32 slots of NB x sk_rows x 128 floats per block, tcnt one
+  // arrival counter per block (zero before the launch; left zero).
+  // no_reduce != 0: no reduction launch follows this one.
+  int sk;
+  int sk_rows;
+  float* skpart;
+  int32_t* tcnt;
+  int no_reduce;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -113,7 +127,31 @@ __device__ __forceinline__ float silu_mul_fast(float g, float u) {
 // output (r, c) of matrix b (r, c within the tile) go to
 // pbase[b * pstride + r * ld + col0 + c]; each lane writes its 4 consecutive
 // columns per group as one 16-byte store.
-template <int MI, int NI, int NB, int WM, int WN>
+// 16-byte stores and loads at agent scope, as two 64-bit relaxed atomic
+// accesses (gfx950 gives them the sc1 cache policy): the store writes through
+// to the device's point of coherence and the load reads from it, so a block
+// on another XCD sees the data within the same launch once the store has
+// completed. They are ordinary instructions to the compiler, which tracks
+// their completion.
+__device__ __forceinline__ void st_coh4(float* p, f32x4_t v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  const uint64_t lo = (uint64_t)__float_as_uint(v[0]) | ((uint64_t)__float_as_uint(v[1]) << 32);
+  const uint64_t hi = (uint64_t)__float_as_uint(v[2]) | ((uint64_t)__float_as_uint(v[3]) << 32);
+  __hip_atomic_store(q, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ f32x4_t ld_coh4(const float* p) {
+  const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
+  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return f32x4_t{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
+                 __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+}
+
+// COH: the sums are stored with st_coh4, for a block on another XCD to read
+// in the same launch (see decode_schedule); the stores have completed on
+// return.
+template <int MI, int NI, int NB, int WM, int WN, bool COH = false>
 __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI], int m0, int m_end, int col0,
                                                int ld, int wm, int wn, int lane, float* pbase, size_t pstride) {
 #pragma unroll
@@ -126,13 +164,20 @@ __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI]
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
-          for (int g = 0; g < 4; ++g)
-            *reinterpret_cast<float4*>(prow + j * 32 + 8 * g) =
-                make_float4(acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
-                            acc[b][i][j][4 * g + 3]);
+          for (int g = 0; g < 4; ++g) {
+            float* p = prow + j * 32 + 8 * g;
+            if (COH) {
+              st_coh4(p, f32x4_t{acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
+                                 acc[b][i][j][4 * g + 3]});
+            } else {
+              *reinterpret_cast<float4*>(p) = make_float4(acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1],
+                                                          acc[b][i][j][4 * g + 2], acc[b][i][j][4 * g + 3]);
+            }
+          }
       }
     }
   }
+  if (COH) wait_vmcnt<0>();
 }
 
 // One BM x BN output tile (two of them, gate and up, when DUAL) over the whole
@@ -141,7 +186,7 @@ __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI]
 // SPLIT: only K chunks [kc0, kc1) are summed and the fp32 sums of output
 // (r, c) (r: row within the tile, c: column within the tile) go to
 // pbase[b * pstride + r * pld + pcol0 + c] instead of C.
-template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
+template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false, bool COH = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                           int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
                                           size_t pstride = 0, int pld = 0, int pcol0 = 0) {
@@ -250,7 +295,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   // owns 4 consecutive columns per group g = v / 4 and stores them as one
   // 8-byte write (or, for a split-K partial, one 16-byte fp32 write).
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
     return;
   }
 #pragma unroll
@@ -600,7 +645,7 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, bf16_t* smem, int cl
 
 // One split-K tile of BN columns (128, or 256 for a wide single GEMM): K
 // chunks [kc0, kc1), fp32 sums to pbase (row stride pld, column base pcol0).
-template <bool DUAL, bool MX, int BN>
+template <bool DUAL, bool MX, int BN, bool COH = false>
 __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
                                                int n0, int kc0, int kc1, float* pbase, size_t ps, int pld,
                                                int pcol0) {
@@ -611,6 +656,12 @@ __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, 
       gemm_tile_mx<128, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else
       gemm_tile_mx<256, BN, 4, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+  } else if constexpr (COH) {
+    // decode schedule: at most kSkRows rows a tile
+    if (cls == 0)
+      gemm_tile<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+    else
+      gemm_tile<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
   } else {
     if (cls == 0)
       gemm_tile<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
@@ -650,6 +701,113 @@ __device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_sta
   return t;
 }
 
+// ---------------------------------------------------------------------------
+// Decode schedule (bf16 launches in which no expert exceeds sk_rows rows:
+// decode-sized batches and lightly loaded experts). The work is
+// streaming the active experts' weights, and a launch often has fewer tiles
+// than CUs or a partly filled last round, so instead of whole tiles each
+// block takes an exact, contiguous share of the launch's (tile, K chunk)
+// units (stream-K): tile t's chunks are units [t nK, t nK + nK), tiles in
+// the order of decode_tile, and block bo (blocks numbered XCD by XCD, so
+// consecutive shares sit on one XCD) takes units [U bo / Ga, U (bo + 1) / Ga).
+// A tile whose chunks fall into the shares of several blocks is finished by
+// the last of them to arrive: each writes its fp32 sums to a slot of its own
+// with write-through (agent-scope) stores, waits for them to complete, and
+// increments the counter of the tile's first block; the block that sees the
+// final count adds the slots in block order (a fixed order, so results do not
+// depend on timing) with agent-scope loads, applies the epilogue and resets
+// the counter. No block ever waits for another.
+// ---------------------------------------------------------------------------
+constexpr int kSkMinChunks = 2;  // K chunks per block share, at least (when the launch has as many)
+struct SkPart {
+  long long U, Ga;
+  __device__ long long start(long long b) const { return U * b / Ga; }
+  // the block whose share holds unit x
+  __device__ int block_of(long long x) const { return (int)(((x + 1) * Ga + U - 1) / U - 1); }
+};
+
+// Sum of the nc contributors' slots of a split tile (rows [m0, m_end) of C,
+// columns [n0, n0 + 128)) in contributor order, the epilogue, and bf16
+// stores; every thread of the block takes 4 columns of a row at a time and
+// loads the slots of up to kFixBatch contributors before waiting for them.
+constexpr int kFixBatch = 8;
+template <bool DUAL>
+__device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int bf, int nc, int j0) {
+  constexpr int NB = DUAL ? 2 : 1;
+  const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
+  const int items = (m_end - m0) * 32;
+  for (int it = (int)threadIdx.x; it < items; it += kThreads) {
+    const int r = it >> 5, c = (it & 31) * 4;
+    const float* p0 = a.skpart + (size_t)r * 128 + c;
+    f32x4_t g = f32x4_t{}, u = f32x4_t{};
+    for (int q0 = 0; q0 < nc; q0 += kFixBatch) {
+      f32x4_t vg[kFixBatch], vu[kFixBatch];
+#pragma unroll
+      for (int j = 0; j < kFixBatch; ++j) {
+        const int q = q0 + j < nc ? q0 + j : nc - 1;  // past the last contributor: a repeated, unused load
+        const float* p = p0 + ((size_t)(bf + q) * 2 + (q == 0 ? j0 : 0)) * slot_f;
+        vg[j] = ld_coh4(p);
+        if (DUAL) vu[j] = ld_coh4(p + plane);
+      }
+#pragma unroll
+      for (int j = 0; j < kFixBatch; ++j)
+        if (q0 + j < nc) {
+          g += vg[j];
+          if (DUAL) u += vu[j];
+        }
+    }
+    float o[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) o[v] = DUAL ? silu_mul_fast(g[v], u[v]) : g[v];
+    uint2 packed;
+    packed.x = pack_bf16x2(o[0], o[1]);
+    packed.y = pack_bf16x2(o[2], o[3]);
+    *reinterpret_cast<uint2*>(a.C + (size_t)(m0 + r) * a.N + n0 + c) = packed;
+  }
+}
+
+template <bool DUAL>
+__device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem, int T0, const int* s_start,
+                                                const int* s_row0, const int* s_rows) {
+  constexpr int NB = DUAL ? 2 : 1;
+  __shared__ int s_last;
+  const int G = gridDim.x, b = blockIdx.x;
+  const int bo = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const int nK = a.K / kBK;
+  SkPart P;
+  P.U = (long long)T0 * nK;
+  P.Ga = max(1LL, min((long long)G, P.U / kSkMinChunks));  // every block with work takes >= kSkMinChunks
+  if (bo >= P.Ga) return;
+  const long long u0 = P.start(bo), u1 = P.start(bo + 1);
+  const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
+  for (long long u = u0; u < u1;) {
+    const int t = (int)(u / nK);
+    const int kc0 = (int)(u - (long long)t * nK);
+    const int kc1 = (int)min((long long)nK, kc0 + (u1 - u));
+    const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128);
+    const int cls = tile_class(tr.left);
+    if (kc0 == 0 && kc1 == nK) {
+      run_tile<DUAL, false, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+    } else {
+      const long long t0 = (long long)t * nK;
+      const int bf = P.block_of(t0);
+      const int nc = P.block_of(t0 + nK - 1) - bf + 1;
+      const int j0 = P.start(bf) == t0 ? 0 : 1;
+      float* mine = a.skpart + ((size_t)bo * 2 + (u == u0 ? 0 : 1)) * slot_f;
+      run_split_tile<DUAL, false, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128,
+                                            0);
+      __syncthreads();  // every wave's write-through stores have completed
+      if (threadIdx.x == 0) s_last = atomicAdd(a.tcnt + bf, 1) == nc - 1;
+      __syncthreads();
+      if (s_last) {
+        sk_fixup<DUAL>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0);
+        if (threadIdx.x == 0) __hip_atomic_store(a.tcnt + bf, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    u += kc1 - kc0;
+  }
+}
+
 // Body of the grouped GEMM kernels (bf16 or MXFP8; a K chunk is 64 bf16 or
 // 128 E4M3 elements, 128 bytes of a row either way).
 template <bool DUAL, bool MX>
@@ -681,6 +839,23 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   int ex[4], tot[4];
   block_scan<4>(v, ex, tot, s_tot);
   const int T0 = tot[0], R = tot[1], n_big = tot[2], n_active = tot[3];
+  // Decode schedule when every expert fits a slot's rows. Otherwise tiles
+  // split along K need the reduction launch; when the host launches none
+  // (it saw that no expert can exceed the slot rows, so only offsets that
+  // break that bound get here) nothing is split.
+  const bool can_split = a.part != nullptr && !a.no_reduce;
+  if constexpr (!MX) {
+    if (a.sk && __syncthreads_count(tid < E && rows > a.sk_rows) == 0) {
+      if (tid < E) s_start[tid] = ex[0];
+      if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
+        a.plan[0] = 1;  // nothing for a reduction launch to do
+        a.plan[2] = 1;
+      }
+      __syncthreads();
+      decode_schedule<DUAL>(a, smem, T0, s_start, s_row0, s_rows);
+      return;
+    }
+  }
 
   // Single-output GEMM: 256-column tiles move a third fewer bytes per MFMA
   // than 128-column ones but halve the tile count; use them when every CU
@@ -700,7 +875,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     return (st > 1 && 3 * r <= a.plan_rows) ? st : 1;
   };
   int S = 1;
-  if (!wide && T0 > 0 && a.part != nullptr && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
+  if (!wide && T0 > 0 && can_split && R <= a.plan_rows && (n_big == 0 || T0 < G)) {
     long long best = (long long)((T0 + G - 1) / G) * (nK + kSplitOverhead);
     // unsplit with full rounds: the tail split shortens the last round
     const int st1 = T0 >= G ? tail_ranges(T0, 128) : 1;
@@ -726,7 +901,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // per tile ([tile][b][split][256][cols]) and finished by the reduction
   // launch, which finds each tile's rows and columns in the plan.
   int St = 1, rem = 0;
-  if (S == 1 && a.part != nullptr && total > 0) {
+  if (S == 1 && can_split && total > 0) {
     St = tail_ranges(total, cols);
     rem = St > 1 ? total % G : 0;
   }
@@ -826,6 +1001,12 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
       if (tid == 0) s_item = item_of(j_next);
       __syncthreads();
       item = s_item;
+    }
+    // The last block to finish (every other block has drawn its last item)
+    // zeroes the counters for the next launch.
+    if (tid == 0 && a.done != nullptr && atomicAdd(a.done, 1) == G - 1) {
+      for (int q = 0; q < 8; ++q) __hip_atomic_store(a.queue + q, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.done, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     return;
   }
@@ -1067,15 +1248,31 @@ __global__ void set_offsets_kernel(int32_t* offsets, int m) {
 // ---------------------------------------------------------------------------
 static size_t round256(size_t n) { return ((n + 255) / 256) * 256; }
 
-// bf16 workspace: h [M_cap, I] | split-K plan | split-K partials | the two
-// GEMMs' per-XCD work counters (8 ints each). A split
+// bf16 workspace: counters (kCntBytes at offset 0, the same place whatever
+// the sizes, so a buffer can serve calls of any size) | h [M_cap, I] |
+// split-K plan | fp32 partials (split-K, tail split or the decode
+// schedule's slots). The counters must be zero before the first call on a
+// workspace; every call leaves them zero. A split
 // launch has R <= M_cap partial rows for offsets that are a valid scan (and
 // R <= 64 E_local when every expert is small), and S <= 8. The kernel splits
 // only when R fits the plan's row map and its partials fit in part_cap.
+constexpr size_t kCntBytes = 16384;
+constexpr int kMaxBlocks = 1024;  // grid limit of a GEMM launch (tcnt entries)
+// Rows of a decode-schedule slot: the largest expert the decode schedule
+// takes. Its fix-up moves every split tile's partial sums through the
+// point of coherence, which outweighs the gain beyond about 32 rows (a
+// one-expert launch of 64 or 128 rows ran 5-60 % slower than split-K with a
+// reduction launch; at 1-16 rows it runs 3-36 % faster).
+constexpr int kSkRows = 32;
+// int offsets within the counters
+constexpr int kQueueGU = 0, kDoneGU = 8, kQueueDN = 16, kDoneDN = 24, kTcntGU = 64, kTcntDN = 64 + kMaxBlocks;
+static_assert((kTcntDN + kMaxBlocks) * 4 <= (int)kCntBytes, "counters");
+
 struct FfnWs {
-  size_t h, plan, part, queue;  // byte offsets
-  long long part_cap;           // floats
-  int plan_rows;                // rows of the plan's row map
+  size_t h, plan, part;  // byte offsets
+  long long part_cap;    // floats
+  int plan_rows;         // rows of the plan's row map
+  bool sk_ok;            // the partial region holds the decode schedule's slots
   size_t bytes;
 };
 
@@ -1089,7 +1286,16 @@ static long long part_cap_floats(int M_cap, int E_local, int H, int I) {
   return std::min(std::max(split_k, tail), kPartCapFloats);
 }
 
-static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
+static int device_cu_count();
+
+// the decode schedule's slots: two per block, 2 x kSkRows x 128 floats each
+static long long sk_slot_floats() { return 2LL * std::min(device_cu_count(), kMaxBlocks) * 2 * kSkRows * 128; }
+
+// Layout of an FFN workspace of at most `cap` bytes (SIZE_MAX: as large as
+// the call can use). A smaller capacity shrinks only the partial region:
+// fewer tiles can then split, and below the slots' size the decode schedule
+// is off. The fixed part (counters, h, plan) must fit: see ffn_ws_fixed.
+static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16, size_t cap = SIZE_MAX) {
   FfnWs w{};
   const size_t h = round256((size_t)M_cap * I * (bf16 ? 2 : 4));
   w.h = 0;
@@ -1097,13 +1303,22 @@ static FfnWs ffn_ws_layout(int M_cap, int E_local, int H, int I, bool bf16) {
     w.bytes = h + 256;
     return w;
   }
-  w.part_cap = part_cap_floats(M_cap, E_local, H, I);
+  w.h = kCntBytes;
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
-  w.plan = h;
+  w.plan = w.h + h;
   w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
-  w.queue = w.part + round256((size_t)w.part_cap * 4);
-  w.bytes = w.queue + 256 + 256;
+  const long long full = std::max(part_cap_floats(M_cap, E_local, H, I), sk_slot_floats());
+  size_t part_bytes = round256((size_t)full * 4);
+  if (cap != SIZE_MAX) part_bytes = std::min(part_bytes, cap > w.part ? ((cap - w.part) & ~(size_t)255) : 0);
+  w.part_cap = std::min(part_cap_floats(M_cap, E_local, H, I), (long long)(part_bytes / 4));
+  w.sk_ok = (long long)(part_bytes / 4) >= sk_slot_floats();
+  w.bytes = w.part + part_bytes;
   return w;
+}
+
+size_t ffn_ws_fixed(int M_cap, int E_local, int H, int I, bool bf16) {
+  const FfnWs w = ffn_ws_layout(M_cap, E_local, H, I, bf16, 0);
+  return bf16 ? w.part : w.bytes;
 }
 
 size_t ffn_ws_bytes(int M_cap, int E_local, int H, int I, bool bf16) {
@@ -1124,9 +1339,10 @@ static int device_cu_count() {
 
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
                       const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
-                      void* y_perm, void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T) {
+                      void* y_perm, void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T,
+                      size_t ws_cap) {
   if (E_local == 0 || M_cap == 0) return hipSuccess;
-  const FfnWs L = ffn_ws_layout(M_cap, E_local, H, I, bf16);
+  const FfnWs L = ffn_ws_layout(M_cap, E_local, H, I, bf16, ws_cap);
   char* wsb = static_cast<char*>(ws);
   void* h = wsb + L.h;
   if (!bf16) {
@@ -1149,47 +1365,64 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   // tiles than blocks, so the grid covers at least 8 of those.
   auto grid_for = [&](int N) {
     const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128) * kMaxSplit;
-    long long g = cus;  // one 8-wave block per CU
+    long long g = std::min(cus, kMaxBlocks);  // one 8-wave block per CU
     if (ub < g) g = ub;
     if (g >= 8) g &= ~7LL;
     return (unsigned)(g < 1 ? 1 : g);
   };
   float* part = reinterpret_cast<float*>(wsb + L.part);
   int32_t* plan = reinterpret_cast<int32_t*>(wsb + L.plan);
+  int32_t* cnt = reinterpret_cast<int32_t*>(wsb);
   // reduce grid: one float4 column group per thread, grid-stride over 4
   // blocks per CU (a split launch has up to max(M_cap, 64 E_local) rows of
   // N columns to finish, a tail split up to G / 2 tiles of 256 x 256)
   auto reduce_grid = [&](int) { return (unsigned)(4 * cus); };
-  int32_t* queue = reinterpret_cast<int32_t*>(wsb + L.queue);
-  clear_counters_kernel<<<1, 64, 0, s>>>(queue, 16);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // The GEMMs take the decode schedule whenever no expert has more than
+  // kSkRows rows, and finish its split tiles inside their launches. When no
+  // expert can have more (a token contributes at most one row to an expert,
+  // so with the row gather the bound is min(T, M_cap)), the reduction
+  // launches are skipped: the call is two launches.
+  const int row_bound = a_src != nullptr ? std::min(a_T, M_cap) : M_cap;
+  const bool sk = L.sk_ok && row_bound <= kSkRows;
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
               part, L.part_cap, plan, L.plan_rows};
-  g1.queue = queue;
+  g1.queue = cnt + kQueueGU;
+  g1.done = cnt + kDoneGU;
   g1.a_src = a_src;
   g1.a_div = a_div;
   g1.a_T = a_T;
   g1.ldb = ld_gu;
+  g1.sk = L.sk_ok ? 1 : 0;
+  g1.no_reduce = sk ? 1 : 0;
+  g1.sk_rows = kSkRows;
+  g1.skpart = part;
+  g1.tcnt = cnt + kTcntGU;
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // A GEMM can split only if its K range holds two splits of kMinSplitChunks.
   const bool split_gu = H / kBK >= 2 * kMinSplitChunks, split_dn = I / kBK >= 2 * kMinSplitChunks;
-  if (split_gu) {
+  if (split_gu && !sk) {
     split_reduce_kernel<true><<<reduce_grid(I), 256, 0, s>>>(part, plan, I, static_cast<bf16_t*>(h));
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   GemmArgs g2{static_cast<const bf16_t*>(h), static_cast<const bf16_t*>(w_down), nullptr,
               static_cast<bf16_t*>(y_perm), offsets, E_local, M_cap, H, I, part, L.part_cap, plan, L.plan_rows};
-  g2.queue = queue + 8;
+  g2.queue = cnt + kQueueDN;
+  g2.done = cnt + kDoneDN;
   g2.ldb = ld_dn;
+  g2.sk = g1.sk;
+  g2.no_reduce = g1.no_reduce;
+  g2.sk_rows = kSkRows;
+  g2.skpart = part;
+  g2.tcnt = cnt + kTcntDN;
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (split_dn) split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
+  if (split_dn && !sk)
+    split_reduce_kernel<false><<<reduce_grid(H), 256, 0, s>>>(part, plan, H, static_cast<bf16_t*>(y_perm));
   return hipGetLastError();
 }
 

@@ -27,12 +27,16 @@ hipError_t launch_combine(const void* y, const float* w, const int32_t* dest, in
                           bool bf16, void* out, hipStream_t s);
 
 size_t ffn_ws_bytes(int M_cap, int E_local, int H, int I, bool bf16);
+// bytes of a workspace that cannot shrink (counters, h, plan); a workspace of
+// at least this many bytes serves a call, with less room to split tiles
+size_t ffn_ws_fixed(int M_cap, int E_local, int H, int I, bool bf16);
 // a_src != nullptr (bf16 only): the gate/up GEMM's row m is row
 // a_src[m] / a_div of x_perm, which then holds a_T rows (see GemmArgs).
+// ws_cap: bytes of ws when smaller than ffn_ws_bytes (>= ffn_ws_fixed).
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
                       const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
                       void* y_perm, void* ws, hipStream_t s, const int32_t* a_src = nullptr, int a_div = 1,
-                      int a_T = 0);
+                      int a_T = 0, size_t ws_cap = SIZE_MAX);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
 // MXFP8: code rows of weight operands (and of quantiser outputs) are

@@ -25,7 +25,7 @@ def L():
 
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "moe.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:moe_status|const char\*|int)\s+(moe_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:moe_status|const char\*|int|size_t)\s+(moe_\w+)\s*\(", text, re.M)))
 
 
 def test_header_declares_the_six_entry_points():
@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.moe_abi_version() == 2
+    assert L.moe_abi_version() == 3
     assert L.moe_status_string(0) == b"ok"
     assert L.moe_status_string(3) == b"workspace too small"
     assert L.moe_status_string(99) == b"unknown status"

@@ -337,26 +337,37 @@ def test_ffn_stage_on_oracle_inputs():
 
 
 SPLIT_CASES = [
-    # (H, I, rows per local expert, S of the down GEMM): experts of at most 64
-    # rows, or launches with fewer tiles than CUs, take the split-K path
+    # (H, I, rows per local expert, S of the down GEMM's split-K plan).
+    # Launches where no expert exceeds 32 rows take the decode schedule
+    # (equal shares of (tile, K chunk) units per CU, split tiles finished in
+    # the GEMM; the plan then says 1); other launches with experts of at most
+    # 64 rows, or with fewer tiles than CUs, take split-K.
     (1024, 2048, [1, 64, 0, 30], 4),       # gate/up S = 2, down S = 4
     (4096, 14336, [64], 8),                # Mixtral-shaped expert: gate/up S = 2, down S = 8
-    (4096, 14336, [1], 8),
+    (4096, 14336, [1], 1),                 # decode schedule
+    (4096, 14336, [32, 7, 0, 19], 1),      # decode schedule at the 32-row bound
     (1024, 2048, [65, 3, 0, 1], 4),        # a 65-row expert, but fewer tiles than CUs: still split
     (7168, 2048, [256], 4),                # a 256-row DSV3-shaped expert: gate/up S = 8, down S = 4
     (5120, 8192, [400, 100, 32], 3),       # Maverick-shaped experts of mixed size: down S = 3
     (7168, 2048, [1, 33], 2),              # DSV3-shaped experts: gate/up S = 8, down S = 2
-    (7168, 2048, [1], 4),                  # one DSV3-shaped expert: gate/up S = 8, down S = 4
-    (5120, 8192, [1], 6),                  # Maverick-shaped expert: gate/up S = 4, down S = 6
-    (2048, 768, [5], 1),                   # Qwen3-shaped: gate/up S = 4; the down GEMM (K = 768) cannot split
+    (7168, 2048, [1], 1),                  # one DSV3-shaped expert: decode schedule
+    (5120, 8192, [1], 1),                  # one Maverick-shaped expert: decode schedule
+    (2048, 768, [5], 1),                   # one Qwen3-shaped expert: decode schedule
+    (2048, 768, [128, 1, 60, 0, 127], 1),  # split-K gate/up; the down GEMM (K = 768) cannot split
 ]
 
 
 def _down_split_factor(ws, M_cap, I):
     """S of the last (down) GEMM, from the split-K plan that follows h in the
-    workspace (white-box: shows which path a case exercised)."""
-    off = ((M_cap * I * 2 + 255) // 256) * 256
+    workspace (white-box: shows which path a case exercised; 1 also for the
+    decode schedule, whose split tiles are finished inside the GEMM)."""
+    off = moe.FFN_COUNTER_BYTES + ((M_cap * I * 2 + 255) // 256) * 256
     return int(ws[off:off + 4].view(torch.int32).item())
+
+
+def _counters_zero(ws):
+    """The workspace's counters are left zero by every call."""
+    return bool(torch.all(ws[:moe.FFN_COUNTER_BYTES] == 0).item())
 
 
 @pytest.mark.parametrize("H,I,rows,S_down", SPLIT_CASES,
@@ -378,6 +389,7 @@ def test_ffn_split_k(H, I, rows, S_down):
     y, ws = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff)
     torch.cuda.synchronize()
     assert _down_split_factor(ws, M_cap, I) == S_down
+    assert _counters_zero(ws)
     h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
     G.check_bf16(h, h_ref, "split h")
     G.check_bf16(G.down(y)[:m], y_ref, "split y", scale=G.down_scale(h_ref, wd, offsets))
@@ -385,6 +397,7 @@ def test_ffn_split_k(H, I, rows, S_down):
     y2, _ = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff, ws=ws)
     torch.cuda.synchronize()
     assert torch.equal(y2[:m], y[:m])
+    assert _counters_zero(ws)
 
 
 TAIL_CASES = [
@@ -415,7 +428,7 @@ def test_ffn_tail_split(H, I, rows, plan):
     y, ws = moe.moe_grouped_swiglu_ffn(G.up(xp, torch.bfloat16), G.up(wg, torch.bfloat16),
                                        G.up(wu, torch.bfloat16), G.up(wd, torch.bfloat16), G.up_i32(offsets))
     torch.cuda.synchronize()
-    off = ((M_cap * I * 2 + 255) // 256) * 256
+    off = moe.FFN_COUNTER_BYTES + ((M_cap * I * 2 + 255) // 256) * 256
     got = ws[off:off + 20].view(torch.int32).cpu().numpy()
     assert (got[0], got[2], got[3], got[4]) == plan, got[:5]
     h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
@@ -457,7 +470,7 @@ def test_ffn_ragged_tails(H, I, rows, plan):
     dx, doff = G.up(xp, torch.bfloat16), G.up_i32(offsets)
     y, ws = moe.moe_grouped_swiglu_ffn(dx, dg, du, dd, doff)
     torch.cuda.synchronize()
-    off = ((M_cap * I * 2 + 255) // 256) * 256
+    off = moe.FFN_COUNTER_BYTES + ((M_cap * I * 2 + 255) // 256) * 256
     got = ws[off:off + 20].view(torch.int32).cpu().numpy()
     assert (got[0], got[4]) == plan, got[:5]
     h = G.down(moe.ffn_hidden(ws, M_cap, I, torch.bfloat16))[:m]
