@@ -224,6 +224,37 @@ moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src,
                                          void* y_perm, void* ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
+ * moe_grouped_swiglu_ffn_noalloc - moe_grouped_swiglu_ffn for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).
+ *
+ * Same arguments, results and limits as moe_grouped_swiglu_ffn, without the
+ * workspace: the call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine) and uses instead this library's scratch, a
+ * device array of moe_ffn_scratch_bytes() bytes (32 MiB) in each GPU's copy
+ * of the code object, held until the process ends. Its counters are cleared
+ * on `stream` by the first call on a device; every call leaves them zero.
+ * The scratch must hold the workspace's fixed part, the counters (16 KiB),
+ * h [M_cap, I] and the split plan, i.e. roughly M_cap * I * sizeof(dt) +
+ * 4 * max(M_cap, 64 E_local) + 16 KiB bytes (decode-sized batches: e.g.
+ * M_cap <= 500 rows at I = 14336 in bf16); larger calls return
+ * MOE_ERR_WORKSPACE and launch nothing. The rest of the scratch holds
+ * partial sums of split tiles; where it is smaller than the workspace
+ * moe_grouped_swiglu_ffn would use, fewer tiles are split (results stay
+ * within the same tolerances, but need not be bitwise those of
+ * moe_grouped_swiglu_ffn). All calls on one GPU share its scratch, whatever
+ * their stream: calls that overlap in time on one GPU race, so serialise
+ * them (one stream, or events).
+ */
+moe_status moe_grouped_swiglu_ffn_noalloc(const void* x_perm, const void* w_gate, const void* w_up,
+                                          const void* w_down, const int32_t* offsets, int E_local,
+                                          int H, int I, int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt,
+                                          void* y_perm, hipStream_t stream);
+
+/* Bytes of the scratch that moe_grouped_swiglu_ffn_noalloc uses on each GPU. */
+size_t moe_ffn_scratch_bytes(void);
+
+/*
  * moe_unpermute_combine - gather and weighted sum back to token order.
  *
  * out[t,:] = round_dt( sum over j ascending with dest[t*k+j] >= 0 of

@@ -30,6 +30,7 @@ from ._lib import (  # noqa: F401
     moe_grouped_swiglu_ffn,
     moe_grouped_swiglu_ffn_gather,
     moe_grouped_swiglu_ffn_mx,
+    moe_grouped_swiglu_ffn_noalloc,
     moe_grouped_swiglu_mx,
     moe_layer,
     moe_load_sweep,

@@ -26,7 +26,7 @@ EXPORTED = ("moe_status_string", "moe_abi_version", "moe_gate_topk", "moe_expert
             "moe_fit_latency_model", "moe_place_greedy", "moe_place_incremental", "moe_placement_cost",
             "moe_window_push", "moe_drift_distance", "moe_mx_quantize", "moe_grouped_swiglu_mx",
             "moe_grouped_gemm_mx", "moe_grouped_swiglu_ffn_mx", "moe_load_sweep_mx",
-            "moe_grouped_swiglu_ffn_gather")
+            "moe_grouped_swiglu_ffn_gather", "moe_grouped_swiglu_ffn_noalloc", "moe_ffn_scratch_bytes")
 
 
 class MoeError(RuntimeError):
@@ -95,6 +95,10 @@ def load_library(path: str = LIB_PATH):
     L.moe_grouped_swiglu_ffn_mx.restype = _I
     L.moe_grouped_swiglu_ffn_mx.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P, _P, _PSZ,
                                             _P]
+    L.moe_grouped_swiglu_ffn_noalloc.restype = _I
+    L.moe_grouped_swiglu_ffn_noalloc.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P, _P]
+    L.moe_ffn_scratch_bytes.restype = _SZ
+    L.moe_ffn_scratch_bytes.argtypes = []
     if L.moe_abi_version() != 3:
         raise RuntimeError("libmoe ABI version mismatch")
     _lib = L
@@ -326,6 +330,26 @@ def moe_grouped_swiglu_ffn(x_perm, w_gate, w_up, w_down, offsets, ws=None, y_per
                                   _stream())
     _check("moe_grouped_swiglu_ffn", st)
     return y_perm, ws
+
+
+def moe_grouped_swiglu_ffn_noalloc(x_perm, w_gate, w_up, w_down, offsets, y_perm):
+    """moe_grouped_swiglu_ffn on the library's per-GPU scratch: allocates
+    nothing (y_perm [M_cap, H] must be given). Returns y_perm."""
+    L = load_library()
+    M_cap, H = x_perm.shape
+    E_local, I, H2 = w_gate.shape
+    if H2 != H or tuple(w_up.shape) != (E_local, I, H) or tuple(w_down.shape) != (E_local, H, I):
+        raise ValueError("expert weights must be w_gate/w_up [E_local, I, H] and w_down [E_local, H, I]")
+    if offsets.numel() != E_local + 1:
+        raise ValueError("offsets must have E_local + 1 entries")
+    if tuple(y_perm.shape) != (M_cap, H):
+        raise ValueError("y_perm must be [M_cap, H]")
+    pg, pu, pd, ld_gu, ld_dn = _ffn_weights(w_gate, w_up, w_down, x_perm.dtype)
+    st = L.moe_grouped_swiglu_ffn_noalloc(_dev(x_perm, "x_perm"), pg, pu, pd,
+                                          _dev(offsets, "offsets", torch.int32), E_local, H, I, ld_gu, ld_dn, M_cap,
+                                          _dtype_code(x_perm), _dev(y_perm, "y_perm", x_perm.dtype), _stream())
+    _check("moe_grouped_swiglu_ffn_noalloc", st)
+    return y_perm
 
 
 def moe_grouped_swiglu_ffn_gather(x, perm_src, k, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):

@@ -15,6 +15,7 @@
 // consecutive tile indices share a weight column block, so blocks running at
 // the same time read the same weights.
 #include <algorithm>
+#include <mutex>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -1618,6 +1619,41 @@ hipError_t launch_router_logits_split(const void* x, const void* wr, int T, int 
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of the FFN entry point that allocates nothing
+// (moe_grouped_swiglu_ffn_noalloc): the workspace of its calls, one copy per
+// GPU in the code object's device memory, held until the process ends. In
+// host code `scratch` only names the symbol; its address on a device comes
+// from hipGetSymbolAddress with that device current, and only that address
+// is passed to kernels.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t ffn_scratch(void** out, hipStream_t s) {
+  static std::mutex mu;
+  static void* ptrs[64] = {nullptr};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    // the counters must start at zero (every call leaves them zero); a
+    // kernel rather than a memset, so that a first call under graph capture
+    // records no memset node
+    clear_counters_kernel<<<1, 1024, 0, s>>>(static_cast<int32_t*>(p), (int)(kCntBytes / 4));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s) {

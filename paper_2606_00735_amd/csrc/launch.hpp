@@ -37,6 +37,10 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
                       void* y_perm, void* ws, hipStream_t s, const int32_t* a_src = nullptr, int a_div = 1,
                       int a_T = 0, size_t ws_cap = SIZE_MAX);
+// The FFN scratch of this process on the current device (kScratchBytes),
+// resolved on first use; its counters are cleared on stream s then.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+hipError_t ffn_scratch(void** out, hipStream_t s);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 
 // MXFP8: code rows of weight operands (and of quantiser outputs) are

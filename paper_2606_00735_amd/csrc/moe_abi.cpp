@@ -271,6 +271,30 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
                                     dt == MOE_BF16, y_perm, ws, stream));
 }
 
+moe_status moe_grouped_swiglu_ffn_noalloc(const void* x_perm, const void* w_gate, const void* w_up,
+                                          const void* w_down, const int32_t* offsets, int E_local, int H, int I,
+                                          int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt, void* y_perm,
+                                          hipStream_t stream) {
+  moe_status st = ffn_shape_ok(E_local, H, I, M_cap, dt);
+  if (st != MOE_OK) return st;
+  int ld_gu = 0, ld_dn = 0;
+  if ((st = resolve_ld(ldw_gu, H, dt, &ld_gu)) != MOE_OK || (st = resolve_ld(ldw_dn, I, dt, &ld_dn)) != MOE_OK)
+    return st;
+  // the part of the workspace that cannot shrink must fit the scratch
+  if (moe::ffn_ws_fixed(M_cap, E_local, H, I, dt == MOE_BF16) > moe::kScratchBytes) return MOE_ERR_WORKSPACE;
+  if (E_local == 0 || M_cap == 0) return MOE_OK;
+  if (!x_perm || !w_gate || !w_up || !w_down || !offsets || !y_perm) return MOE_ERR_INVALID_ARG;
+  if (!aligned16(x_perm) || !aligned16(w_gate) || !aligned16(w_up) || !aligned16(w_down) || !aligned16(y_perm) ||
+      !aligned4(offsets))
+    return MOE_ERR_INVALID_ARG;
+  void* ws = nullptr;
+  if (moe::ffn_scratch(&ws, stream) != hipSuccess) return MOE_ERR_HIP;
+  return hip_status(moe::launch_ffn(x_perm, w_gate, w_up, w_down, offsets, E_local, H, I, ld_gu, ld_dn, M_cap,
+                                    dt == MOE_BF16, y_perm, ws, stream, nullptr, 1, 0, moe::kScratchBytes));
+}
+
+size_t moe_ffn_scratch_bytes(void) { return moe::kScratchBytes; }
+
 moe_status moe_grouped_swiglu_ffn_gather(const void* x, const int32_t* perm_src, int T, int k, const void* w_gate,
                                          const void* w_up, const void* w_down, const int32_t* offsets, int E_local,
                                          int H, int I, int ldw_gu, int ldw_dn, int M_cap, moe_dtype dt,
