@@ -252,68 +252,280 @@ def main():
                 cases.append((Tb, a, bb, st_b["grouped_swiglu_ffn"]))
         result["mx_ffn"] = mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, args.steps,
                                       key=lambda Tb, a: f"{args.config}-T{Tb}-a{a:g}-s{args.seed}-mx")
+    sweeps = {}
     if not args.no_extras:
-        # skew table: same weights, other token counts and skews of this config
+        # every (T, alpha) point of every workload, the headline workload's
+        # weights reused, each other workload's generated and uploaded once
         table = []
-        for Tb in shape.Ts:
-            for a in shape.alphas:
-                xs, _, bs, _ = make_router(shape, Tb, a, seed=args.seed)
-                xb = up(xs)
-                bb = make_bufs(Tb, xb) if (Tb != T) else dict(bufs)
-                bb["bias"] = up(bs, torch.float32)
-                ms_b, st_b = run_timed(xb, bb, Tb, max(5, args.steps // 2), 3)
-                wb = layer_work(shape, Tb, bb["counts"].cpu().numpy(), li.local)
-                fu = st_b["grouped_swiglu_ffn"]
-                table.append({"T": Tb, "alpha": a, "us_per_layer": round(ms_b * 1e3, 2),
-                              "layer_tflops": round(wb["layer_flops"] / (ms_b * 1e-3) / 1e12, 2),
-                              "ffn_us": round(fu, 2), "M_loc": wb["m_loc"], "active": wb["active"],
-                              "ffn_tflops": round(wb["ffn_flops"] / (fu * 1e-6) / 1e12, 2),
-                              "ffn_gbps": round(wb["ffn_bytes"] / (fu * 1e-6) / 1e9, 1),
-                              "ffn_frac_mfma": round(wb["ffn_flops"] / (fu * 1e-6) / 1e12 / peak_f, 4),
-                              "ffn_frac_hbm": round(wb["ffn_bytes"] / (fu * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)})
+        for name, sh in CONFIGS.items():
+            if name == args.config:
+                rows = skew_rows(moe, torch, np, sh, li.local, li.expert_map, wg, wu, wd, args)
+            else:
+                rows = workload_skew_rows(moe, torch, np, name, args)
+            table.extend(rows)
         result["skew_table"] = table
-        # latency vs load on one expert, weight copies rotated past the 256 MB cache
-        e_bytes = 3 * H * I * (2 if dt == torch.bfloat16 else 4)
-        n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
-        g1, u1, d1 = make_experts(shape, [int(li.local[0])], seed=args.seed)
-        rep = lambda a: moe.pad_weight_rows(up(a).repeat(n_rot, 1, 1))
-        xs = up(make_router(shape, max(SWEEP_MS), 0.0, seed=args.seed)[0])
-        med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), SWEEP_MS, warmup=3, iters=args.sweep_iters)
-        med = [float(v) for v in med]
-        result["load_sweep"] = {"M": SWEEP_MS, "us": [round(float(v), 2) for v in med], "n_rot": n_rot,
-                                "tflops": [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, u in
-                                           zip(SWEEP_MS, med)],
-                                "gbps": [round((e_bytes + 2.0 * m * H * 2) / (u * 1e-6) / 1e9, 1) for m, u in
-                                         zip(SWEEP_MS, med)]}
+        # latency vs load on one expert of every workload, cold and at steady
+        # state (Section 4.2.1), weight copies rotated past the 256 MB cache
+        for name, sh in CONFIGS.items():
+            sweeps[name] = sweep_section(moe, torch, np, sh, args.seed, args.sweep_iters)
+        result["load_sweep"] = sweeps
         if dt == torch.bfloat16:
-            # the same expert in MXFP8 (weights 1 byte + a scale byte per 32)
-            mx_bytes = 3 * H * I * (1 + 1 / 32)
-            n_rot_mx = max(1, -(-2 * MALL_BYTES // int(mx_bytes)))
-            rep_mx = lambda a: moe.moe_mx_quantize(up(a).repeat(n_rot_mx, 1, 1).contiguous())
-            tg, tu, td = rep_mx(g1), rep_mx(u1), rep_mx(d1)
-            med_mx, _ = moe.moe_load_sweep_mx(moe.moe_mx_quantize(xs), tg, tu, td, SWEEP_MS, warmup=3,
-                                              iters=args.sweep_iters)
-            med_mx = [float(v) for v in med_mx]
-            del tg, tu, td
-            result["load_sweep_mx"] = {
-                "M": SWEEP_MS, "us": [round(float(v), 2) for v in med_mx], "n_rot": n_rot_mx,
-                "tflops": [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, u in zip(SWEEP_MS, med_mx)],
-                "gbps": [round((mx_bytes + m * H * (1 + 1 / 32) + 2.0 * m * H) / (u * 1e-6) / 1e9, 1)
-                         for m, u in zip(SWEEP_MS, med_mx)],
-                "speedup_vs_bf16": [round(b / m, 2) for b, m in zip(med, med_mx)]}
+            result["load_sweep_mx"] = mx_sweep_section(moe, torch, np, shape, li, args, sweeps.get(args.config))
 
     placement_inputs = None
     if not args.no_extras:
         result["reference_peaks"] = reference_peaks(torch, np, w, T, H, I, dt)
         result["sclk"] = read_sclk()
-        result["placement"], placement_inputs = placement_section(moe, args.seed)
+        result["placement"], placement_inputs = placement_section(moe, args.seed, sweeps.get("dsv3_shard"))
 
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(li, args.cpu_seconds)
+        result["cpu_baseline"]["single_thread"] = cpu_single_thread(li)
         if placement_inputs is not None:
             result["cpu_baseline"]["placement"] = placement_oracle_timing(*placement_inputs)
 
     print(json.dumps(result), flush=True)
+
+
+def _up(torch, np, a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda().to(dtype).contiguous()
+
+
+def time_layer(moe, torch, np, x, wr, bias, k, emap, wg, wu, wd, bb, steps, warmup, fuse):
+    """`steps` timed layer passes (after `warmup`), HIP events around each
+    stage on the current stream; returns (mean layer ms, per-stage mean us)."""
+    names = ["gate_topk", "histogram_scan", "permute", "grouped_swiglu_ffn", "combine"]
+    T, E = x.shape[0], wr.shape[0]
+    for _ in range(warmup):
+        moe.moe_layer(x, wr, bias, k, emap, wg, wu, wd, bufs=bb, fuse_gather=fuse)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
+    for s_ in range(steps):
+        ev = evs[s_]
+        ev[0].record()
+        ids, wts, _ = moe.moe_gate_topk(x, wr, bias, k, ids=bb["ids"], weights=bb["weights"], ws=bb["gate_ws"])
+        ev[1].record()
+        counts, offsets, hws = moe.moe_expert_histogram_scan(ids, E, emap, ws=bb["hist_ws"], counts=bb["counts"],
+                                                             offsets=bb["offsets"])
+        ev[2].record()
+        xp, ps, dest = moe.moe_permute(x, ids, emap, hws, x_perm=bb.get("x_perm"), perm_src=bb["perm_src"],
+                                       dest=bb["dest"], gather=not fuse)
+        ev[3].record()
+        if fuse:
+            yp, _ = moe.moe_grouped_swiglu_ffn_gather(x, ps, k, wg, wu, wd, offsets, ws=bb["ffn_ws"],
+                                                      y_perm=bb["y_perm"])
+        else:
+            yp, _ = moe.moe_grouped_swiglu_ffn(xp, wg, wu, wd, offsets, ws=bb["ffn_ws"], y_perm=bb["y_perm"])
+        ev[4].record()
+        moe.moe_unpermute_combine(yp, wts, dest, T, out=bb["out"])
+        ev[5].record()
+    torch.cuda.synchronize()
+    per = {n: [evs[s_][i].elapsed_time(evs[s_][i + 1]) * 1e3 for s_ in range(steps)] for i, n in enumerate(names)}
+    stage = {n: float(np.mean(v)) for n, v in per.items()}
+    return sum(stage.values()) * 1e-3, stage
+
+
+def skew_rows(moe, torch, np, sh, local, emap, wg, wu, wd, args):
+    """One row per (T, alpha) of a workload: layer time and the FFN against
+    both roofline denominators (weights already on the GPU)."""
+    from synth import make_router
+    bf16 = sh.dtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    peak_f = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    rows = []
+    for Tb in sh.Ts:
+        for a in sh.alphas:
+            xs, w_r, bs, _ = make_router(sh, Tb, a, seed=args.seed)
+            xb, wrb, bb_bias = _up(torch, np, xs, dt), _up(torch, np, w_r, dt), _up(torch, np, bs, torch.float32)
+            bb = {}
+            moe.moe_layer(xb, wrb, bb_bias, sh.k, emap, wg, wu, wd, bufs=bb, fuse_gather=bf16)
+            # each point first runs its own layer for ~0.2 s, so it is timed at
+            # its own operating point (clock), not at the one the previous,
+            # possibly much heavier, point left behind
+            torch.cuda.synchronize()
+            t_w = time.perf_counter()
+            n_w = 0
+            while time.perf_counter() - t_w < 0.2:
+                for _ in range(4):
+                    moe.moe_layer(xb, wrb, bb_bias, sh.k, emap, wg, wu, wd, bufs=bb, fuse_gather=bf16)
+                n_w += 4
+                torch.cuda.synchronize()
+            ms_b, st_b = time_layer(moe, torch, np, xb, wrb, bb_bias, sh.k, emap, wg, wu, wd, bb,
+                                    max(5, args.steps // 2), 3, bf16)
+            wb = layer_work(sh, Tb, bb["counts"].cpu().numpy(), local)
+            fu = st_b["grouped_swiglu_ffn"]
+            cnt = bb["counts"].cpu().numpy()[np.asarray(local)]
+            rows.append({"workload": sh.name, "T": Tb, "alpha": a, "us_per_layer": round(ms_b * 1e3, 2),
+                         "layer_tflops": round(wb["layer_flops"] / (ms_b * 1e-3) / 1e12, 2),
+                         "stages_us": {n: round(v, 2) for n, v in st_b.items()},
+                         "ffn_us": round(fu, 2), "M_loc": wb["m_loc"], "active": wb["active"],
+                         "max_rows_per_expert": int(cnt.max()) if cnt.size else 0,
+                         "ffn_tflops": round(wb["ffn_flops"] / (fu * 1e-6) / 1e12, 2),
+                         "ffn_gbps": round(wb["ffn_bytes"] / (fu * 1e-6) / 1e9, 1),
+                         "ffn_frac_mfma": round(wb["ffn_flops"] / (fu * 1e-6) / 1e12 / peak_f, 4),
+                         "ffn_frac_hbm": round(wb["ffn_bytes"] / (fu * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                         "ffn_binding_frac": round(max(wb["ffn_flops"] / (peak_f * 1e12),
+                                                       wb["ffn_bytes"] / (PEAK_HBM_GBPS * 1e9)) / (fu * 1e-6), 4)})
+            del bb, xb
+    return rows
+
+
+def workload_skew_rows(moe, torch, np, name, args):
+    """skew_rows for a workload whose weights are generated here (and freed)."""
+    from synth import CONFIGS, make_layer
+    sh = CONFIGS[name]
+    li = make_layer(sh, 1, 0.0, seed=args.seed)
+    dt = torch.bfloat16 if sh.dtype == "bf16" else torch.float32
+    ws = [_up(torch, np, a, dt) for a in (li.w_gate, li.w_up, li.w_down)]
+    if dt == torch.bfloat16:
+        ws = [moe.pad_weight_rows(t) for t in ws]
+    del li.w_gate, li.w_up, li.w_down
+    rows = skew_rows(moe, torch, np, sh, li.local, li.expert_map, *ws, args)
+    del ws
+    torch.cuda.empty_cache()
+    return rows
+
+
+def sclk_now():
+    """Current shader clock (MHz) from the driver's DPM table in sysfs, or None."""
+    import glob
+    import re
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            with open(path) as fh:
+                txt = fh.read()
+        except OSError:
+            continue
+        for ln in txt.splitlines():
+            if ln.rstrip().endswith("*"):
+                m = re.search(r"(\d+)\s*mhz", ln, re.I)
+                if m:
+                    return int(m.group(1))
+    return None
+
+
+class ClockSampler:
+    """Reads sclk every `period` s in a thread while the block runs; the
+    summary leaves out deep-sleep readings (< 400 MHz, idle gaps between
+    launches)."""
+
+    def __init__(self, period=0.002):
+        import threading
+        self.period, self.samples, self._stop = period, [], threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = sclk_now()
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+    def median(self):
+        import statistics
+        busy = [v for v in self.samples if v >= 400]
+        return int(statistics.median(busy)) if busy else None
+
+
+def sweep_section(moe, torch, np, sh, seed, iters):
+    """Latency vs token load of one expert of workload `sh` (Section 4.2.1).
+
+    cold:   each point alone (3 warm-up runs, then `iters` timed runs), the
+            GPU otherwise idle;
+    steady: first the GPU is held under the expert's largest load until the
+            shader clock settles (three consecutive 50 ms windows within 2 %,
+            at least 2 s, at most 20 s), then every point is preceded by
+            about 30 ms of that load, so each is timed at the operating point
+            of sustained MoE work.
+    Every point records the median shader clock sampled while it ran."""
+    from synth import make_experts, make_router
+    from synth.moe_inputs import local_subset
+    H, I = sh.H, sh.I
+    bf16 = sh.dtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    es = 2 if bf16 else 4
+    e_bytes = 3 * H * I * es
+    n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
+    g1, u1, d1 = make_experts(sh, [int(local_subset(sh, seed)[0])], seed=seed)
+    if bf16:
+        rep = lambda a: moe.pad_weight_rows(_up(torch, np, a, dt).repeat(n_rot, 1, 1))
+    else:
+        rep = lambda a: _up(torch, np, a, dt).repeat(n_rot, 1, 1).contiguous()
+    wg, wu, wd = rep(g1), rep(u1), rep(d1)
+    Mmax = max(SWEEP_MS)
+    xs = _up(torch, np, make_router(sh, Mmax, 0.0, seed=seed)[0], dt)
+    y = torch.empty((Mmax, H), dtype=dt, device="cuda")
+    ws = None
+
+    def point(M, warmup, n):
+        nonlocal ws
+        with ClockSampler() as cs:
+            med, _ = moe.moe_load_sweep(xs, wg, wu, wd, [M], warmup=warmup, iters=n, y_scratch=y, ws=ws)
+        return float(med[0]), cs.median()
+
+    # workspace sized for the largest load, shared by every call
+    ffn_bytes = moe.ffn_ws_bytes(1, H, I, Mmax, dt)
+    ws = torch.zeros(ffn_bytes + 256, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    time.sleep(0.5)
+    cold = [point(M, 3, iters) for M in SWEEP_MS]
+    # heat: repeat the largest load in ~50 ms windows until the clock settles
+    t_big = max(cold[-1][0], 1.0) * 1e-6
+    n_burst = max(1, int(0.05 / t_big))
+    hist, t0 = [], time.perf_counter()
+    while True:
+        _, c = point(Mmax, 0, n_burst)
+        hist.append(c or 0)
+        el = time.perf_counter() - t0
+        last = hist[-3:]
+        if el > 20.0 or (el > 2.0 and len(last) == 3 and min(last) > 0 and max(last) <= 1.02 * min(last)):
+            break
+    n_keep = max(1, int(0.03 / t_big))
+    steady = []
+    for M in SWEEP_MS:
+        point(Mmax, 0, n_keep)
+        steady.append(point(M, 0, iters))
+    del wg, wu, wd, xs, y, ws
+    torch.cuda.empty_cache()
+    fl = lambda pts: [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, (u, _) in zip(SWEEP_MS, pts)]
+    gb = lambda pts: [round((e_bytes + 2.0 * m * H * es) / (u * 1e-6) / 1e9, 1) for m, (u, _) in zip(SWEEP_MS, pts)]
+    return {"workload": sh.name, "H": H, "I": I, "M": SWEEP_MS, "n_rot": n_rot, "iters": iters,
+            "cold": {"us": [round(u, 2) for u, _ in cold], "sclk_mhz": [c for _, c in cold],
+                     "tflops": fl(cold), "gbps": gb(cold)},
+            "steady": {"us": [round(u, 2) for u, _ in steady], "sclk_mhz": [c for _, c in steady],
+                       "tflops": fl(steady), "gbps": gb(steady),
+                       "warmup_s": round(time.perf_counter() - t0, 1), "warmup_sclk_mhz": hist[-3:]}}
+
+
+def mx_sweep_section(moe, torch, np, shape, li, args, bf16_sweep):
+    """The MXFP8 FFN on the same expert as the workload's bf16 sweep (cold)."""
+    from synth import make_experts, make_router
+    H, I = shape.H, shape.I
+    mx_bytes = 3 * H * I * (1 + 1 / 32)
+    n_rot = max(1, -(-2 * MALL_BYTES // int(mx_bytes)))
+    g1, u1, d1 = make_experts(shape, [int(li.local[0])], seed=args.seed)
+    rep = lambda a: moe.moe_mx_quantize(_up(torch, np, a, torch.bfloat16).repeat(n_rot, 1, 1).contiguous())
+    tg, tu, td = rep(g1), rep(u1), rep(d1)
+    xs = _up(torch, np, make_router(shape, max(SWEEP_MS), 0.0, seed=args.seed)[0], torch.bfloat16)
+    med, _ = moe.moe_load_sweep_mx(moe.moe_mx_quantize(xs), tg, tu, td, SWEEP_MS, warmup=3, iters=args.sweep_iters)
+    med = [float(v) for v in med]
+    del tg, tu, td
+    torch.cuda.empty_cache()
+    out = {"workload": shape.name, "M": SWEEP_MS, "us": [round(v, 2) for v in med], "n_rot": n_rot,
+           "tflops": [round(6.0 * H * I * m / (u * 1e-6) / 1e12, 2) for m, u in zip(SWEEP_MS, med)],
+           "gbps": [round((mx_bytes + m * H * (1 + 1 / 32) + 2.0 * m * H) / (u * 1e-6) / 1e9, 1)
+                    for m, u in zip(SWEEP_MS, med)]}
+    if bf16_sweep is not None:
+        out["speedup_vs_bf16_cold"] = [round(b / m, 2) for b, m in zip(bf16_sweep["cold"]["us"], med)]
+    return out
 
 
 def mx_section(moe, torch, np, shape, li, wg, wu, wd, cases, steps, key):
@@ -401,7 +613,10 @@ def reference_peaks(torch, np, w, T, H, I, dt):
 
 
 def read_sclk():
-    """Current shader clock as rocm-smi reports it (None if unavailable)."""
+    """Current shader clock as the driver reports it (None if unavailable)."""
+    v = sclk_now()
+    if v is not None:
+        return f"{v} MHz"
     import subprocess
     try:
         r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
@@ -417,14 +632,15 @@ PLACE_LAYERS, PLACE_GPUS, PLACE_T = 58, 8, 4096
 PLACE_SWEEP_MS = [1, 8, 64, 256, 1024, 4096]
 
 
-def placement_section(moe, seed):
+def placement_section(moe, seed, dsv3_sweep=None):
     """ViBE's placement control path on this GPU for a DSV3-shaped model:
     58 MoE layers x 256 experts over 8 GPUs (32 slots each), f_g fitted from a
     sweep of one DSV3-shaped expert on this GPU and scaled per GPU by up to
     7 % (seeded), synthetic activation matrices with the rank-bias skew
     (alpha = 1) before and after a routing drift (8 rank swaps per layer).
     Times are HIP-event medians of the GPU calls; predicted layer latencies
-    come from moe_placement_cost."""
+    come from moe_placement_cost. With `dsv3_sweep` (sweep_section's result
+    for the DSV3-shaped workload) f is fitted from its steady-state curve."""
     import numpy as np
     import torch
     from synth import CONFIGS, make_activation_matrix, make_experts, make_router
@@ -433,13 +649,18 @@ def placement_section(moe, seed):
     Lyr, G, E, k = PLACE_LAYERS, PLACE_GPUS, shape.E, shape.k
     cap = E // G
     up = lambda a, dt=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(dt).contiguous()
-    g1, u1, d1 = make_experts(shape, [0], seed=seed)
-    e_bytes = 3 * shape.H * shape.I * 2
-    n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
-    rep = lambda a: moe.pad_weight_rows(up(a).repeat(n_rot, 1, 1))
-    xs = up(make_router(shape, max(PLACE_SWEEP_MS), 0.0, seed=seed)[0])
-    med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), PLACE_SWEEP_MS, warmup=3, iters=10)
-    kn, kt = moe.moe_fit_latency_model(PLACE_SWEEP_MS, med)
+    if dsv3_sweep is not None:
+        f_src = "steady-state sweep of the DSV3-shaped expert (load_sweep)"
+        kn, kt = moe.moe_fit_latency_model(dsv3_sweep["M"], dsv3_sweep["steady"]["us"])
+    else:
+        f_src = "cold sweep of the DSV3-shaped expert"
+        g1, u1, d1 = make_experts(shape, [0], seed=seed)
+        e_bytes = 3 * shape.H * shape.I * 2
+        n_rot = max(1, -(-2 * MALL_BYTES // e_bytes))
+        rep = lambda a: moe.pad_weight_rows(up(a).repeat(n_rot, 1, 1))
+        xs = up(make_router(shape, max(PLACE_SWEEP_MS), 0.0, seed=seed)[0])
+        med, _ = moe.moe_load_sweep(xs, rep(g1), rep(u1), rep(d1), PLACE_SWEEP_MS, warmup=3, iters=10)
+        kn, kt = moe.moe_fit_latency_model(PLACE_SWEEP_MS, med)
     scale = 1.0 + 0.07 * np.random.default_rng(seed + 7).random(G)
     KN, KT = np.tile(kn, (G, 1)), np.outer(scale, kt)
     W1 = make_activation_matrix(Lyr, E, PLACE_T, k, 1.0, seed)
@@ -486,7 +707,7 @@ def placement_section(moe, seed):
     out = {
         "workload": f"{Lyr} MoE layers x {E} experts on {G} GPUs ({cap} slots each), DSV3-shaped expert "
                     f"f_g from this GPU's sweep x (1 + 0.07 u_g), T={PLACE_T} tokens top-{k} per layer, alpha=1",
-        "f_knots": {"n": [int(v) for v in kn], "us": [round(float(v), 2) for v in kt]},
+        "f_knots": {"n": [int(v) for v in kn], "us": [round(float(v), 2) for v in kt], "source": f_src},
         "gpu_speed_scale": [round(float(v), 4) for v in scale],
         "greedy_us": round(t_greedy, 2), "incremental_us": round(t_incr, 2),
         "drift_distance_us": round(t_drift, 2), "window_push_us": round(t_push, 2),
@@ -513,6 +734,54 @@ def placement_oracle_timing(W1, W2, KN, KT, cap, layers=8):
     return {"greedy_ms_per_layer": round(t_g / layers * 1e3, 3),
             "incremental_ms_per_layer": round(t_i / layers * 1e3, 3), "cores": 1,
             "sample": f"first {layers} of {W1.shape[0]} layers (pure Python, one thread)"}
+
+
+def cpu_model_name():
+    """The host CPU as lscpu names it (model, family/model/stepping, sockets)."""
+    import subprocess
+    info = {}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for ln in out.splitlines():
+            if ":" in ln:
+                k, v = ln.split(":", 1)
+                info[k.strip()] = v.strip()
+    except Exception:
+        pass
+    name = info.get("Model name") or info.get("BIOS Model name") or "unknown"
+    extra = ", ".join(f"{k} {info[k]}" for k in ("CPU family", "Model", "Stepping", "Socket(s)", "CPU max MHz")
+                      if k in info)
+    return f"{name} ({extra})" if extra else name
+
+
+def cpu_single_thread(li):
+    """The oracle with one BLAS thread on the decode-sized and tiny workloads
+    (whole layer, every token)."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import moe_oracle as O
+    from synth import CONFIGS, make_layer
+    out = []
+    for name, T, a in (("tiny", 64, 1.0), ("mixtral", 32, 0.0), ("qwen3", 128, 0.0)):
+        sh = CONFIGS[name]
+        if li.shape.name == name:   # the headline workload's weights, this batch's router inputs
+            from synth import make_router
+            lj = li
+            x, w_r, bias, _ = make_router(sh, T, a, seed=li.seed)
+        else:
+            lj = make_layer(sh, T, a, seed=li.seed)
+            x, w_r, bias = lj.x, lj.w_router, lj.bias
+        with threadpool_limits(1):
+            t = time.perf_counter()
+            r = O.moe_layer(x, w_r, bias, sh.k, lj.expert_map, lj.w_gate, lj.w_up, lj.w_down,
+                            bf16=sh.dtype == "bf16")
+            dt = time.perf_counter() - t
+        w = layer_work(sh, T, r["counts"], lj.local)
+        out.append({"workload": name, "T": T, "alpha": a, "seconds": round(dt, 3),
+                    "tflops": round(w["layer_flops"] / dt / 1e12, 6), "us_per_layer": round(dt * 1e6, 1),
+                    "cores": 1})
+        del lj
+    return out
 
 
 def cpu_baseline(li, target_s):
@@ -544,12 +813,7 @@ def cpu_baseline(li, target_s):
         times += [run(n)[0] for _ in range(2)]
     dt = float(np.median(times))
     w = layer_work(shape, n, r["counts"], li.local)
-    model = "unknown"
-    try:
-        with open("/proc/cpuinfo") as fh:
-            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), model)
-    except OSError:
-        pass
+    model = cpu_model_name()
     return {"value": round(w["layer_flops"] / dt / 1e12, 5), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "seconds": round(dt, 2), "runs": len(times), "cpu_model": model,
             "affinity_cpus": len(os.sched_getaffinity(0)),
