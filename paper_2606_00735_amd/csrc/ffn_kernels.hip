@@ -679,8 +679,29 @@ struct TileRef {
   int e, m0, m_end, n0, left;
 };
 
+// Order of one expert's tiles (n_mt row tiles x n_nt column tiles): bands of
+// up to kBand row tiles; in a band the row tiles of a column block are
+// consecutive, then the next column block. An XCD runs 32 consecutive tiles
+// at a time, which for an expert with many row tiles is then 8 column
+// blocks x 4 row tiles (12 operand tiles per K chunk in its L2) instead of,
+// e.g., 3 column blocks x 12 row tiles (15).
+constexpr int kBand = 4;
+__device__ __forceinline__ void tile_rc(int local, int n_mt, int n_nt, int& mt, int& nt) {
+  const int full = n_mt / kBand, per_band = kBand * n_nt;
+  const int b = local / per_band;
+  if (b < full) {
+    const int l2 = local - b * per_band;
+    nt = l2 / kBand;
+    mt = b * kBand + (l2 - nt * kBand);
+  } else {
+    const int rb = n_mt - full * kBand, l2 = local - full * per_band;
+    nt = l2 / rb;
+    mt = full * kBand + (l2 - nt * rb);
+  }
+}
+
 __device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_start, const int* s_row0,
-                                               const int* s_rows, int cols) {
+                                               const int* s_rows, int cols, int N) {
   // last expert whose first tile is <= tile (experts with no tiles share
   // their start with the next one, so the last match is the owner)
   int lo = 0, hi = E - 1;
@@ -692,9 +713,8 @@ __device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_sta
   t.e = lo;
   const int local = tile - s_start[lo];
   const int er = s_rows[lo];
-  const int n_mt = row_tiles(er);
-  // row tile fastest: all row tiles of a weight column block run together
-  const int nt = local / n_mt, mt = local - nt * n_mt;
+  int nt, mt;
+  tile_rc(local, row_tiles(er), N / cols, mt, nt);
   t.m0 = s_row0[lo] + mt * 256;
   t.left = er - mt * 256;  // rows from m0 to the expert's end, >= 1
   t.m_end = t.m0 + (t.left < 256 ? t.left : 256);
@@ -785,7 +805,7 @@ __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem,
     const int t = (int)(u / nK);
     const int kc0 = (int)(u - (long long)t * nK);
     const int kc1 = (int)min((long long)nK, kc0 + (u1 - u));
-    const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128);
+    const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128, a.N);
     const int cls = tile_class(tr.left);
     if (kc0 == 0 && kc1 == nK) {
       run_tile<DUAL, false, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
@@ -924,7 +944,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     if (S > 1 && tid < E)
       for (int r = 0; r < s_rows[tid]; ++r) a.plan[kPlanHead + s_srow0[tid] + r] = s_row0[tid] + r;
     if (St > 1 && tid < rem) {
-      const TileRef t = decode_tile(full + tid, E, s_start, s_row0, s_rows, cols);
+      const TileRef t = decode_tile(full + tid, E, s_start, s_row0, s_rows, cols, a.N);
       a.plan[kPlanHead + 3 * tid] = t.m0;
       a.plan[kPlanHead + 3 * tid + 1] = t.m_end;
       a.plan[kPlanHead + 3 * tid + 2] = t.n0;
@@ -943,9 +963,9 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
       const int e = lo;
       const int local = item - s_start[e];
       const int er = s_rows[e];
-      const int n_mt = row_tiles(er);
       const int sp = local % S, rest = local / S;
-      const int nt = rest / n_mt, mt = rest - nt * n_mt;
+      int nt, mt;
+      tile_rc(rest, row_tiles(er), a.N / 128, mt, nt);
       const int kc0 = sp * nK / S, kc1 = (sp + 1) * nK / S;
       const int m0 = s_row0[e] + mt * 256;
       const int left = er - mt * 256;
@@ -959,7 +979,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     if (item >= full) {
       // a split of a tail tile
       const int u = item - full, pr = u / St, sp = u - pr * St;
-      const TileRef t = decode_tile(full + pr, E, s_start, s_row0, s_rows, cols);
+      const TileRef t = decode_tile(full + pr, E, s_start, s_row0, s_rows, cols, a.N);
       const int kc0 = sp * nK / St, kc1 = (sp + 1) * nK / St;
       const size_t tsz = (size_t)256 * cols;
       float* pbase = a.part + ((size_t)pr * NB * St + sp) * tsz;
@@ -974,7 +994,7 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
                                     St * tsz, cols, 0);
       return;
     }
-    const TileRef t = decode_tile(item, E, s_start, s_row0, s_rows, cols);
+    const TileRef t = decode_tile(item, E, s_start, s_row0, s_rows, cols, a.N);
     const int cls = tile_class(t.left);
     if (!DUAL && wide)
       run_tile<DUAL, MX, !DUAL>(a, smem, cls, t.e, t.m0, t.m_end, t.n0);
