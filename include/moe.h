@@ -203,8 +203,11 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
  * moe_grouped_swiglu_ffn_gather - moe_grouped_swiglu_ffn with the dispatch
  * gather folded into the gate/up GEMM's operand loads.
  *
- * Computes exactly what moe_permute followed by moe_grouped_swiglu_ffn
- * computes (bitwise the same y_perm and h), but row r of the expert input is
+ * Computes what moe_permute followed by moe_grouped_swiglu_ffn computes
+ * (bitwise the same y_perm and h whenever both take the same schedule; with
+ * T <= 32 this one may finish split tiles in its GEMM launches where the
+ * permuted call, bounded only by M_cap, splits differently, and results then
+ * agree within the FFN's tolerance), but row r of the expert input is
  * read as x[perm_src[r] / k] (the token of flat assignment perm_src[r],
  * Section 2's dispatch) instead of from a permuted copy, so the x_perm write
  * and re-read are skipped: call moe_permute with x_perm = NULL for perm_src.
@@ -354,11 +357,13 @@ moe_status moe_grouped_gemm_mx(const uint8_t* aq, const uint32_t* as, const uint
  * moe_grouped_gemm_mx with W_down (wdq [E_local, H, I], wds
  * [E_local, I/128, H]) into y_perm [M_cap, H] bf16. Weight code rows are
  * ldw_gu (W_gate, W_up) and ldw_dn (W_down) bytes apart (0: dense).
- * ws holds h codes [M_cap, I] at offset 0 and their scales [I/128, M_cap]
- * at offset M_cap * I rounded up to 256 bytes, then the fp32 partial sums
- * of split-K tiles (used as in moe_grouped_swiglu_ffn; summed in a fixed
- * order, so results are deterministic) and the per-XCD tile counters.
- * Calls that share a workspace must not overlap.
+ * ws starts with 16 KiB of counters that must be zero before the first call
+ * on the workspace (every call leaves them zero), then h codes [M_cap, I]
+ * and, 256-byte aligned after them, their scales [I/128, M_cap], then the
+ * split plan and the fp32 partial sums of tiles split along K (summed in a
+ * fixed order, so results are deterministic). The schedules and launches
+ * are those of moe_grouped_swiglu_ffn, with M_cap as the bound on an
+ * expert's rows. Calls that share a workspace must not overlap.
  */
 moe_status moe_grouped_swiglu_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq,
                                      const uint32_t* wgs, const uint8_t* wuq, const uint32_t* wus,

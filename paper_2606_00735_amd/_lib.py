@@ -684,7 +684,8 @@ def ffn_mx_ws_bytes(E_local, H, I, M_cap):
 
 def moe_grouped_swiglu_ffn_mx(x, w_gate, w_up, w_down, offsets, ws=None, y_perm=None):
     """MXFP8 expert FFN. Returns (y_perm [M_cap, H] bf16, ws); ws holds h codes
-    [M_cap, I] at byte 0 and h scales [I/128, M_cap] after them (256-aligned)."""
+    [M_cap, I] at byte FFN_COUNTER_BYTES and h scales [I/128, M_cap] after
+    them (256-aligned)."""
     L = load_library()
     M_cap, H = x.shape
     E_local, I, _ = w_gate.shape
@@ -692,7 +693,7 @@ def moe_grouped_swiglu_ffn_mx(x, w_gate, w_up, w_down, offsets, ws=None, y_perm=
         raise ValueError("offsets must have E_local + 1 entries")
     dev = x.codes.device
     if ws is None:
-        ws = torch.empty(ffn_mx_ws_bytes(E_local, H, I, M_cap), dtype=torch.uint8, device=dev)
+        ws = torch.zeros(ffn_mx_ws_bytes(E_local, H, I, M_cap), dtype=torch.uint8, device=dev)  # counters start at zero
     if y_perm is None:
         y_perm = torch.empty((M_cap, H), dtype=torch.bfloat16, device=dev)
     n = ctypes.c_size_t(ws.numel())
@@ -729,7 +730,7 @@ def moe_load_sweep_mx(x, w_gate, w_up, w_down, Ms, warmup=3, iters=10, y_scratch
             H, I, w_gate.ld, w_down.ld, Ms.ctypes.data_as(ctypes.c_void_p), nM, warmup, iters)
     st = L.moe_load_sweep_mx(*args, None, None, ctypes.byref(n), None, None, _stream())
     _check("moe_load_sweep_mx", st)
-    ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    ws = torch.zeros(n.value, dtype=torch.uint8, device=dev)  # counters start at zero
     y = torch.empty((max_m, H), dtype=torch.bfloat16, device=dev) if y_scratch is None else y_scratch
     med = np.zeros(nM, np.float32)
     allv = np.zeros((nM, iters), np.float32) if keep_all else None

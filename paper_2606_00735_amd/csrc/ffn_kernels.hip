@@ -357,7 +357,7 @@ __device__ __forceinline__ uint4 lds16(const bf16_t* lds, int row, int chunk) {
 // scale dwords; otherwise C is written as bf16.
 // SPLIT: only K chunks [kc0, kc1) are summed, the fp32 sums written as in
 // gemm_tile.
-template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false>
+template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false, bool COH = false>
 __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                              int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
                                              size_t pstride = 0, int pld = 0, int pcol0 = 0) {
@@ -498,7 +498,7 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
   pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(kc1 - kc0, smem, St::STAGE / 2, issue, read, mma, mix);
 
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
     return;
   }
 
@@ -650,7 +650,13 @@ template <bool DUAL, bool MX, int BN, bool COH = false>
 __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
                                                int n0, int kc0, int kc1, float* pbase, size_t ps, int pld,
                                                int pcol0) {
-  if constexpr (MX) {
+  if constexpr (MX && COH) {
+    // decode schedule: at most kSkRows rows a tile
+    if (cls == 0)
+      gemm_tile_mx<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+    else
+      gemm_tile_mx<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+  } else if constexpr (MX) {
     if (cls == 0)
       gemm_tile_mx<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
     else if (cls == 1)
@@ -722,6 +728,23 @@ __device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_sta
   return t;
 }
 
+// Four h values of columns [c, c + 4) of `row`, quantised with the other 28
+// of their 32-column block, which the 7 other lanes of this lane's aligned
+// group of 8 hold; the group's first lane writes the scale code.
+__device__ __forceinline__ void mx_quant_store4(float h0, float h1, float h2, float h3, int row, int c, int N,
+                                                int M_cap, uint8_t* C8, uint32_t* Cs) {
+  float amax = fmaxf(fmaxf(fabsf(h0), fabsf(h1)), fmaxf(fabsf(h2), fabsf(h3)));
+  amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
+  amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
+  const uint32_t code = mx_scale_code(amax);
+  const float inv = mx_inv_scale(code);
+  *reinterpret_cast<uint32_t*>(C8 + (size_t)row * N + c) = e4m3x4(h0 * inv, h1 * inv, h2 * inv, h3 * inv);
+  if ((c & (kMxBlock - 1)) == 0)
+    reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
+        static_cast<uint8_t>(code);
+}
+
 // ---------------------------------------------------------------------------
 // Decode schedule (bf16 launches in which no expert exceeds sk_rows rows:
 // decode-sized batches and lightly loaded experts). The work is
@@ -740,6 +763,10 @@ __device__ __forceinline__ TileRef decode_tile(int tile, int E, const int* s_sta
 // the counter. No block ever waits for another.
 // ---------------------------------------------------------------------------
 constexpr int kSkMinChunks = 2;  // K chunks per block share, at least (when the launch has as many)
+// Largest expert for which the decode schedule is preferred when a
+// reduction launch follows anyway (same-process A/B, one to eight
+// Mixtral-shaped experts: faster up to 13-16 rows, 3-10 % slower at 29-32).
+constexpr int kSkPrefRows = 16;
 struct SkPart {
   long long U, Ga;
   __device__ long long start(long long b) const { return U * b / Ga; }
@@ -752,7 +779,7 @@ struct SkPart {
 // stores; every thread of the block takes 4 columns of a row at a time and
 // loads the slots of up to kFixBatch contributors before waiting for them.
 constexpr int kFixBatch = 8;
-template <bool DUAL>
+template <bool DUAL, bool MX>
 __device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int bf, int nc, int j0) {
   constexpr int NB = DUAL ? 2 : 1;
   const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
@@ -780,21 +807,27 @@ __device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, i
     float o[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) o[v] = DUAL ? silu_mul_fast(g[v], u[v]) : g[v];
-    uint2 packed;
-    packed.x = pack_bf16x2(o[0], o[1]);
-    packed.y = pack_bf16x2(o[2], o[3]);
-    *reinterpret_cast<uint2*>(a.C + (size_t)(m0 + r) * a.N + n0 + c) = packed;
+    if (MX && DUAL) {
+      // h as MXFP8: the aligned 8 lanes around this one hold one 32-column
+      // block of the row (items come in whole rows of 32 lanes)
+      mx_quant_store4(o[0], o[1], o[2], o[3], m0 + r, n0 + c, a.N, a.M_cap, reinterpret_cast<uint8_t*>(a.C), a.Cs);
+    } else {
+      uint2 packed;
+      packed.x = pack_bf16x2(o[0], o[1]);
+      packed.y = pack_bf16x2(o[2], o[3]);
+      *reinterpret_cast<uint2*>(a.C + (size_t)(m0 + r) * a.N + n0 + c) = packed;
+    }
   }
 }
 
-template <bool DUAL>
+template <bool DUAL, bool MX>
 __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem, int T0, const int* s_start,
                                                 const int* s_row0, const int* s_rows) {
   constexpr int NB = DUAL ? 2 : 1;
   __shared__ int s_last;
   const int G = gridDim.x, b = blockIdx.x;
   const int bo = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
-  const int nK = a.K / kBK;
+  const int nK = a.K / (MX ? kMxChunk : kBK);
   SkPart P;
   P.U = (long long)T0 * nK;
   P.Ga = max(1LL, min((long long)G, P.U / kSkMinChunks));  // every block with work takes >= kSkMinChunks
@@ -808,20 +841,19 @@ __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem,
     const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128, a.N);
     const int cls = tile_class(tr.left);
     if (kc0 == 0 && kc1 == nK) {
-      run_tile<DUAL, false, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+      run_tile<DUAL, MX, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
     } else {
       const long long t0 = (long long)t * nK;
       const int bf = P.block_of(t0);
       const int nc = P.block_of(t0 + nK - 1) - bf + 1;
       const int j0 = P.start(bf) == t0 ? 0 : 1;
       float* mine = a.skpart + ((size_t)bo * 2 + (u == u0 ? 0 : 1)) * slot_f;
-      run_split_tile<DUAL, false, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128,
-                                            0);
+      run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128, 0);
       __syncthreads();  // every wave's write-through stores have completed
       if (threadIdx.x == 0) s_last = atomicAdd(a.tcnt + bf, 1) == nc - 1;
       __syncthreads();
       if (s_last) {
-        sk_fixup<DUAL>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0);
+        sk_fixup<DUAL, MX>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0);
         if (threadIdx.x == 0) __hip_atomic_store(a.tcnt + bf, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -865,17 +897,19 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // (it saw that no expert can exceed the slot rows, so only offsets that
   // break that bound get here) nothing is split.
   const bool can_split = a.part != nullptr && !a.no_reduce;
-  if constexpr (!MX) {
-    if (a.sk && __syncthreads_count(tid < E && rows > a.sk_rows) == 0) {
-      if (tid < E) s_start[tid] = ex[0];
-      if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
-        a.plan[0] = 1;  // nothing for a reduction launch to do
-        a.plan[2] = 1;
-      }
-      __syncthreads();
-      decode_schedule<DUAL>(a, smem, T0, s_start, s_row0, s_rows);
-      return;
+  // The decode schedule's fix-ups move more partial sums the more rows a
+  // split tile holds: above kSkPrefRows rows the round schedule with split-K
+  // and a reduction launch is faster, if that launch follows.
+  const bool sk_fits = a.sk && __syncthreads_count(tid < E && rows > a.sk_rows) == 0;
+  if (sk_fits && (a.no_reduce || __syncthreads_count(tid < E && rows > kSkPrefRows) == 0)) {
+    if (tid < E) s_start[tid] = ex[0];
+    if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
+      a.plan[0] = 1;  // nothing for a reduction launch to do
+      a.plan[2] = 1;
     }
+    __syncthreads();
+    decode_schedule<DUAL, MX>(a, smem, T0, s_start, s_row0, s_rows);
+    return;
   }
 
   // Single-output GEMM: 256-column tiles move a third fewer bytes per MFMA
@@ -1139,23 +1173,6 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     packed.y = pack_bf16x2(g.z, g.w);
     *reinterpret_cast<uint2*>(C + (size_t)plan[kPlanHead + j] * N + c) = packed;
   }
-}
-
-// Four h values of columns [c, c + 4) of `row`, quantised with the other 28
-// of their 32-column block, which the 7 other lanes of this lane's aligned
-// group of 8 hold; the group's first lane writes the scale code.
-__device__ __forceinline__ void mx_quant_store4(float h0, float h1, float h2, float h3, int row, int c, int N,
-                                                int M_cap, uint8_t* C8, uint32_t* Cs) {
-  float amax = fmaxf(fmaxf(fabsf(h0), fabsf(h1)), fmaxf(fabsf(h2), fabsf(h3)));
-  amax = fmaxf(amax, __shfl_xor(amax, 1, kWave));
-  amax = fmaxf(amax, __shfl_xor(amax, 2, kWave));
-  amax = fmaxf(amax, __shfl_xor(amax, 4, kWave));
-  const uint32_t code = mx_scale_code(amax);
-  const float inv = mx_inv_scale(code);
-  *reinterpret_cast<uint32_t*>(C8 + (size_t)row * N + c) = e4m3x4(h0 * inv, h1 * inv, h2 * inv, h3 * inv);
-  if ((c & (kMxBlock - 1)) == 0)
-    reinterpret_cast<uint8_t*>(Cs + (size_t)(c / kMxChunk) * M_cap + row)[(c / kMxBlock) & 3] =
-        static_cast<uint8_t>(code);
 }
 
 // The MXFP8 gate/up reduction: sums the S partials of gate and up for 4
@@ -1450,10 +1467,11 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
 // ---------------------------------------------------------------------------
 // MXFP8 expert FFN: gate/up (MXFP8 in, MXFP8 h out), then down (bf16 out)
 // ---------------------------------------------------------------------------
-// MXFP8 FFN workspace: h codes [M_cap, I] | h scale dwords [I/128][M_cap] |
-// split-K plan | fp32 partials, sized as for the bf16 FFN | work counters.
+// MXFP8 FFN workspace: counters (kCntBytes, zero before first use, as for
+// bf16) | h codes [M_cap, I] | h scale dwords [I/128][M_cap] | split-K plan |
+// fp32 partials (split-K, or the decode schedule's slots).
 struct FfnMxWs {
-  size_t hs, plan, part, queue;  // byte offsets (h codes at 0)
+  size_t hq, hs, plan, part;  // byte offsets
   long long part_cap;
   int plan_rows;
   size_t bytes;
@@ -1461,7 +1479,8 @@ struct FfnMxWs {
 
 static FfnMxWs ffn_mx_ws_layout(int M_cap, int E_local, int H, int I) {
   FfnMxWs w{};
-  w.hs = round256((size_t)M_cap * I);
+  w.hq = kCntBytes;
+  w.hs = w.hq + round256((size_t)M_cap * I);
   w.plan = w.hs + round256((size_t)(I / kMxChunk) * M_cap * 4);
   // sized for split-K only, not for the tail split as the bf16 layout is:
   // with room for it, the MXFP8 decode FFN (Mixtral-shaped, T = 32) took the
@@ -1470,8 +1489,7 @@ static FfnMxWs ffn_mx_ws_layout(int M_cap, int E_local, int H, int I) {
   w.part_cap = std::min(need, kPartCapFloats);
   w.plan_rows = std::max(M_cap, kSmallM * E_local);
   w.part = w.plan + round256((size_t)(kPlanHead + (size_t)w.plan_rows) * 4);
-  w.queue = w.part + round256((size_t)w.part_cap * 4);
-  w.bytes = w.queue + 256 + 256;
+  w.bytes = w.part + round256((size_t)std::max(w.part_cap, sk_slot_floats()) * 4);
   return w;
 }
 
@@ -1483,7 +1501,7 @@ size_t ffn_mx_ws_bytes(int M_cap, int E_local, int H, int I) {
 // when split-K is possible), a multiple of 8.
 static unsigned mx_grid(int M_cap, int E_local, int N, bool split) {
   const long long ub = ((long long)(M_cap + kSmallM - 1) / kSmallM + E_local) * (N / 128) * (split ? kMaxSplit : 1);
-  long long g = device_cu_count();
+  long long g = std::min(device_cu_count(), kMaxBlocks);
   if (ub < g) g = ub;
   if (g >= 8) g &= ~7LL;
   return (unsigned)(g < 1 ? 1 : g);
@@ -1499,7 +1517,24 @@ struct MxSplit {
   int32_t* plan;
   int plan_rows;
   int32_t* queue;  // per-XCD work counters or nullptr
+  int32_t* done;   // finished-block counter (the queue's reset) or nullptr
+  int32_t* tcnt;   // decode schedule: tile arrival counters, or nullptr (off)
+  bool no_reduce;  // no reduction launch follows (nothing may split)
 };
+
+static void mx_split_args(GemmArgs& g, const MxSplit& sp) {
+  g.part = sp.part;
+  g.part_cap = sp.part_cap;
+  g.plan = sp.plan;
+  g.plan_rows = sp.plan_rows;
+  g.queue = sp.queue;
+  g.done = sp.done;
+  g.sk = sp.tcnt != nullptr ? 1 : 0;
+  g.sk_rows = kSkRows;
+  g.skpart = sp.part;
+  g.tcnt = sp.tcnt;
+  g.no_reduce = sp.no_reduce ? 1 : 0;
+}
 
 static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
                             const uint8_t* wuq, const uint32_t* wus, const int32_t* offsets, int E_local, int H,
@@ -1516,19 +1551,15 @@ static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t
   g.N = I;
   g.K = H;
   g.ldb = ldw;
-  g.part = sp.part;
-  g.part_cap = sp.part_cap;
-  g.plan = sp.plan;
-  g.plan_rows = sp.plan_rows;
-  g.queue = sp.queue;
+  mx_split_args(g, sp);
   g.As = xs;
   g.Bs0 = wgs;
   g.Bs1 = wus;
   g.Cs = hs;
   const bool split = sp.plan != nullptr && H / kMxChunk >= 2 * kMinSplitChunks;
-  grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I, split), kThreads, 0, s>>>(g);
+  grouped_gemm_mx_kernel<true><<<mx_grid(M_cap, E_local, I, split || g.sk), kThreads, 0, s>>>(g);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !split) return e;
+  if (e != hipSuccess || !split || sp.no_reduce) return e;
   split_reduce_mx_kernel<<<mx_reduce_grid(sp.plan_rows, I / 4), 256, 0, s>>>(sp.part, sp.plan, I, M_cap,
                                                                                      hq, hs);
   return hipGetLastError();
@@ -1547,17 +1578,13 @@ static hipError_t gemm_mx(const uint8_t* aq, const uint32_t* as, const uint8_t* 
   g.N = N;
   g.K = K;
   g.ldb = ldb;
-  g.part = sp.part;
-  g.part_cap = sp.part_cap;
-  g.plan = sp.plan;
-  g.plan_rows = sp.plan_rows;
-  g.queue = sp.queue;
+  mx_split_args(g, sp);
   g.As = as;
   g.Bs0 = bs;
   const bool split = sp.plan != nullptr && K / kMxChunk >= 2 * kMinSplitChunks;
-  grouped_gemm_mx_kernel<false><<<mx_grid(M_cap, E_local, N, split), kThreads, 0, s>>>(g);
+  grouped_gemm_mx_kernel<false><<<mx_grid(M_cap, E_local, N, split || g.sk), kThreads, 0, s>>>(g);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !split) return e;
+  if (e != hipSuccess || !split || sp.no_reduce) return e;
   split_reduce_kernel<false><<<mx_reduce_grid(sp.plan_rows, N / 4), 256, 0, s>>>(sp.part, sp.plan, N,
                                                                                   static_cast<bf16_t*>(c));
   return hipGetLastError();
@@ -1584,18 +1611,18 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   if (E_local == 0 || M_cap == 0) return hipSuccess;
   const FfnMxWs L = ffn_mx_ws_layout(M_cap, E_local, H, I);
   char* w = static_cast<char*>(ws);
-  uint8_t* hq = reinterpret_cast<uint8_t*>(w);
+  uint8_t* hq = reinterpret_cast<uint8_t*>(w + L.hq);
   uint32_t* hs = reinterpret_cast<uint32_t*>(w + L.hs);
-  int32_t* queue = reinterpret_cast<int32_t*>(w + L.queue);
-  clear_counters_kernel<<<1, 64, 0, s>>>(queue, 16);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  int32_t* cnt = reinterpret_cast<int32_t*>(w);
+  // as in launch_ffn: the decode schedule finishes its split tiles inside the
+  // GEMM launches; when no expert can exceed kSkRows rows no reduction follows
+  const bool no_reduce = M_cap <= kSkRows;
   const MxSplit sp1{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
-                    L.plan_rows, queue};
-  e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld_gu, M_cap, hq, hs, sp1, s);
+                    L.plan_rows, cnt + kQueueGU, cnt + kDoneGU, cnt + kTcntGU, no_reduce};
+  hipError_t e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld_gu, M_cap, hq, hs, sp1, s);
   if (e != hipSuccess) return e;
-  MxSplit sp2 = sp1;
-  sp2.queue = queue + 8;
+  const MxSplit sp2{sp1.part, sp1.part_cap, sp1.plan, sp1.plan_rows, cnt + kQueueDN, cnt + kDoneDN, cnt + kTcntDN,
+                    no_reduce};
   return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, ld_dn, M_cap, y_perm, sp2, s);
 }
 

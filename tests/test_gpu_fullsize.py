@@ -67,13 +67,14 @@ def test_fullsize(name, T, alpha):
     print("  stats", stats, flush=True)
 
     if bf16:
+        # the bench's configuration, every element against the oracle again
+        # (the gathering FFN may take another schedule than the permuted one:
+        # its row bound is min(T, M_cap), not M_cap)
         fb = G.poison_bufs(T, k, H, E, len(local), dt)
         fb.pop("x_perm")
-        f = moe.moe_layer(dx, dwr, db, k, li.expert_map, *padded, bufs=fb, fuse_gather=True)
+        f = moe.moe_layer(dx, dwr, db, k, li.expert_map, *padded, logits=True, bufs=fb, fuse_gather=True)
         torch.cuda.synchronize()
         assert f["x_perm"] is None
-        h_g = moe.ffn_hidden(g["h"], T * k, I, dt)[:m]
-        h_f = moe.ffn_hidden(f["h"], T * k, I, dt)[:m]
-        assert torch.equal(h_f, h_g), "bench configuration: h"
-        assert torch.equal(f["y_perm"][:m], g["y_perm"][:m]), "bench configuration: y_perm"
-        assert torch.equal(f["out"], g["out"]), "bench configuration: out"
+        f["x_perm"] = g["x_perm"]  # not built by this configuration; checked above
+        fstats = G.compare_layer(li, f, r, f"bench configuration {name} T={T} a={alpha}")
+        print("  bench configuration stats", fstats, flush=True)

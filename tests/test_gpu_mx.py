@@ -295,8 +295,10 @@ def _ffn_case(H, I, rows, seed, rerun=False):
     torch.cuda.synchronize()
     M_cap = xp.shape[0]
     wsn = ws.cpu().numpy()
-    hs_off = ((M_cap * I + 255) // 256) * 256
-    ghq = wsn[:M_cap * I].reshape(M_cap, I)[:m]
+    hq_off = moe.FFN_COUNTER_BYTES
+    hs_off = hq_off + ((M_cap * I + 255) // 256) * 256
+    ghq = wsn[hq_off:hq_off + M_cap * I].reshape(M_cap, I)[:m]
+    assert not wsn[:hq_off].any(), "the workspace's counters must be left zero"
     ghs_dw = torch.from_numpy(wsn[hs_off:hs_off + (I // 128) * M_cap * 4].view(np.int32).reshape(I // 128, M_cap))
     ghs = gpu_scales(ghs_dw, M_cap, I)[:m]
     hq, hs, h32, y_ref, mag, P = X.grouped_swiglu_ffn_mx(xq[:m], xs[:m], gq, gs, uq, us, dq, ds, offsets, parts=True)
@@ -330,6 +332,31 @@ def test_ffn_mx(H, I, rows):
     assert same, "moe_grouped_swiglu_mx and the FFN's h differ"
 
 
+MX_DECODE_CASES = [
+    # no expert above 16 rows: the decode schedule (equal shares of (tile, K
+    # chunk) units per CU, split tiles finished inside the GEMMs); with M_cap
+    # at most 32 no reduction launch follows
+    (4096, 14336, [9, 3, 0, 11]),     # Mixtral-shaped experts, M_cap 26
+    (7168, 2048, [1, 16, 16]),        # DSV3-shaped experts, M_cap 36 (reductions launched, nothing to do)
+    (2048, 768, [3, 0, 7, 1]),        # Qwen3-shaped experts, M_cap 14
+    (4096, 2048, [20, 30]),           # 30 rows but M_cap 53: split-K instead (plan checked below)
+]
+
+
+@pytest.mark.parametrize("H,I,rows", MX_DECODE_CASES, ids=[f"H{h}-I{i}-rows{'_'.join(map(str, r))}"
+                                                           for h, i, r in MX_DECODE_CASES])
+def test_ffn_mx_decode_schedule(H, I, rows):
+    """The rules of the module docstring, a bitwise rerun, and the plan
+    showing that nothing was left for a reduction launch."""
+    banner("mx ffn decode schedule", H, I, rows, "seed 13")
+    ws, M_cap, _ = _ffn_case(H, I, rows, seed=13, rerun=True)
+    hs_off = moe.FFN_COUNTER_BYTES + ((M_cap * I + 255) // 256) * 256
+    plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
+    got = ws[plan_off:plan_off + 12].view(torch.int32).cpu().numpy()
+    if max(rows) <= 16:
+        assert got[0] == 1 and got[2] == 1, got
+
+
 MX_SPLIT_CASES = [
     # (H, I, rows per expert, S of the down GEMM), worked out by hand from the
     # split rule on 256 CUs (K chunks of 128): one 64-row Mixtral-shaped expert
@@ -349,7 +376,7 @@ MX_SPLIT_CASES = [
 def test_ffn_mx_split_k(H, I, rows, S_down):
     banner("mx ffn split-K", H, I, rows, "seed 5")
     ws, M_cap, _ = _ffn_case(H, I, rows, seed=5)
-    hs_off = ((M_cap * I + 255) // 256) * 256
+    hs_off = moe.FFN_COUNTER_BYTES + ((M_cap * I + 255) // 256) * 256
     plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
     assert int(ws[plan_off:plan_off + 4].view(torch.int32).item()) == S_down
 
@@ -367,7 +394,7 @@ MX_TAIL_CASES = [
 def test_ffn_mx_tail_split(H, I, rows, plan):
     banner("mx ffn tail split", H, I, rows, "seed 4")
     ws, M_cap, _ = _ffn_case(H, I, rows, seed=4, rerun=True)
-    hs_off = ((M_cap * I + 255) // 256) * 256
+    hs_off = moe.FFN_COUNTER_BYTES + ((M_cap * I + 255) // 256) * 256
     plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
     got = ws[plan_off:plan_off + 20].view(torch.int32).cpu().numpy()
     assert (got[0], got[2], got[3], got[4]) == plan, got[:5]

@@ -338,14 +338,17 @@ def test_ffn_stage_on_oracle_inputs():
 
 SPLIT_CASES = [
     # (H, I, rows per local expert, S of the down GEMM's split-K plan).
-    # Launches where no expert exceeds 32 rows take the decode schedule
+    # Launches where no expert exceeds 16 rows take the decode schedule
     # (equal shares of (tile, K chunk) units per CU, split tiles finished in
-    # the GEMM; the plan then says 1); other launches with experts of at most
-    # 64 rows, or with fewer tiles than CUs, take split-K.
+    # the GEMM; the plan then says 1), and so do launches of up to 32 rows
+    # per expert when no reduction launch follows (M_cap <= 32); other
+    # launches with experts of at most 64 rows, or with fewer tiles than CUs,
+    # take split-K.
     (1024, 2048, [1, 64, 0, 30], 4),       # gate/up S = 2, down S = 4
     (4096, 14336, [64], 8),                # Mixtral-shaped expert: gate/up S = 2, down S = 8
     (4096, 14336, [1], 1),                 # decode schedule
-    (4096, 14336, [32, 7, 0, 19], 1),      # decode schedule at the 32-row bound
+    (4096, 14336, [16, 7, 0, 11], 1),      # decode schedule at its preferred 16-row bound
+    (4096, 14336, [32, 7, 0, 19], 8),      # 17-32 rows with a reduction launch to follow: split-K, down S = 8
     (1024, 2048, [65, 3, 0, 1], 4),        # a 65-row expert, but fewer tiles than CUs: still split
     (7168, 2048, [256], 4),                # a 256-row DSV3-shaped expert: gate/up S = 8, down S = 4
     (5120, 8192, [400, 100, 32], 3),       # Maverick-shaped experts of mixed size: down S = 3
