@@ -99,6 +99,10 @@ struct GemmArgs {
   float* skpart;
   int32_t* tcnt;
   int no_reduce;
+  // Verdict of the XCD check (see xcd_probe_kernel; 1: block b of a launch
+  // runs on XCD b % 8), or nullptr. The decode schedule reads it to choose
+  // L2-local partial sums; results do not depend on it.
+  const int32_t* xcd_state;
 };
 
 // Split-K plan written by block 0 of a grouped GEMM for split_reduce_kernel:
@@ -149,12 +153,14 @@ __device__ __forceinline__ f32x4_t ld_coh4(const float* p) {
                  __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
 }
 
-// COH: the sums are stored with st_coh4, for a block on another XCD to read
-// in the same launch (see decode_schedule); the stores have completed on
-// return.
+// COH: the sums are for another block to read in the same launch (see
+// decode_schedule) and the stores have completed on return; coh: stored with
+// st_coh4, for a block on another XCD, else with ordinary stores, which a
+// block on the same XCD reads from their shared L2.
 template <int MI, int NI, int NB, int WM, int WN, bool COH = false>
 __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI], int m0, int m_end, int col0,
-                                               int ld, int wm, int wn, int lane, float* pbase, size_t pstride) {
+                                               int ld, int wm, int wn, int lane, float* pbase, size_t pstride,
+                                               bool coh) {
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int r = wm * WM + i * 32 + (lane & 31);  // row within the tile
@@ -167,7 +173,7 @@ __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI]
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             float* p = prow + j * 32 + 8 * g;
-            if (COH) {
+            if (COH && coh) {
               st_coh4(p, f32x4_t{acc[b][i][j][4 * g], acc[b][i][j][4 * g + 1], acc[b][i][j][4 * g + 2],
                                  acc[b][i][j][4 * g + 3]});
             } else {
@@ -190,7 +196,7 @@ __device__ __forceinline__ void split_epilogue(const f32x16_t (&acc)[NB][MI][NI]
 template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false, bool COH = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                           int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
-                                          size_t pstride = 0, int pld = 0, int pcol0 = 0) {
+                                          size_t pstride = 0, int pld = 0, int pcol0 = 0, bool coh = true) {
   using St = Stages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -296,7 +302,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, bf16_t* smem, int e
   // owns 4 consecutive columns per group g = v / 4 and stores them as one
   // 8-byte write (or, for a split-K partial, one 16-byte fp32 write).
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride, coh);
     return;
   }
 #pragma unroll
@@ -360,7 +366,7 @@ __device__ __forceinline__ uint4 lds16(const bf16_t* lds, int row, int chunk) {
 template <int BM, int BN, int WAVES_M, bool DUAL, bool SPLIT = false, bool COH = false>
 __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, int e, int m0, int m_end, int n0,
                                              int kc0 = 0, int kc1 = -1, float* pbase = nullptr,
-                                             size_t pstride = 0, int pld = 0, int pcol0 = 0) {
+                                             size_t pstride = 0, int pld = 0, int pcol0 = 0, bool coh = true) {
   using St = MxStages<BM, BN, DUAL>;
   constexpr int NB = DUAL ? 2 : 1;
   constexpr int WAVES_N = kWaves / WAVES_M;
@@ -498,7 +504,7 @@ __device__ __forceinline__ void gemm_tile_mx(const GemmArgs& a, bf16_t* smem, in
   pipeline_xk<St::NS, St::LOADS, kMxChunk / 64, true>(kc1 - kc0, smem, St::STAGE / 2, issue, read, mma, mix);
 
   if (SPLIT) {
-    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride);
+    split_epilogue<MI, NI, NB, WM, WN, COH>(acc, m0, m_end, pcol0, pld, wm, wn, lane, pbase, pstride, coh);
     return;
   }
 
@@ -583,18 +589,28 @@ __device__ __forceinline__ int tile_class(int left) { return left > 128 ? 2 : (l
 // only if the partials fit and their bytes stay below the weight bytes the
 // launch streams. Every block sees the same offsets, so every block makes
 // the same choice.
+// Inclusive sum over the lanes of a wave by DPP (a few cycles a step, where
+// lane shuffles through LDS take about a hundred): Hillis-Steele within each
+// row of 16 lanes (row_shr 1, 2, 4, 8; lanes shifted in from outside the row
+// add 0), then lane 15 of rows 0 and 2 added to rows 1 and 3 (row_bcast:15),
+// then lane 31 to rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 template <int NV>
 __device__ __forceinline__ void block_scan(int (&v)[NV], int (&excl)[NV], int (&total)[NV], int (*s_tot)[kWaves]) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int inc[NV];
 #pragma unroll
   for (int q = 0; q < NV; ++q) {
-    inc[q] = v[q];
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int n = __shfl_up(inc[q], off, kWave);
-      if (lane >= off) inc[q] += n;
-    }
+    inc[q] = wave_incl_scan(v[q]);
     if (lane == 63) s_tot[q][wave] = inc[q];
   }
   __syncthreads();
@@ -649,13 +665,13 @@ __device__ __forceinline__ void run_tile(const GemmArgs& a, bf16_t* smem, int cl
 template <bool DUAL, bool MX, int BN, bool COH = false>
 __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, int cls, int e, int m0, int m_end,
                                                int n0, int kc0, int kc1, float* pbase, size_t ps, int pld,
-                                               int pcol0) {
+                                               int pcol0, bool coh = true) {
   if constexpr (MX && COH) {
     // decode schedule: at most kSkRows rows a tile
     if (cls == 0)
-      gemm_tile_mx<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+      gemm_tile_mx<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0, coh);
     else
-      gemm_tile_mx<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+      gemm_tile_mx<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0, coh);
   } else if constexpr (MX) {
     if (cls == 0)
       gemm_tile_mx<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
@@ -666,9 +682,9 @@ __device__ __forceinline__ void run_split_tile(const GemmArgs& a, bf16_t* smem, 
   } else if constexpr (COH) {
     // decode schedule: at most kSkRows rows a tile
     if (cls == 0)
-      gemm_tile<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+      gemm_tile<64, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0, coh);
     else
-      gemm_tile<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
+      gemm_tile<128, BN, 2, DUAL, true, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0, coh);
   } else {
     if (cls == 0)
       gemm_tile<64, BN, 2, DUAL, true>(a, smem, e, m0, m_end, n0, kc0, kc1, pbase, ps, pld, pcol0);
@@ -746,44 +762,72 @@ __device__ __forceinline__ void mx_quant_store4(float h0, float h1, float h2, fl
 }
 
 // ---------------------------------------------------------------------------
-// Decode schedule (bf16 launches in which no expert exceeds sk_rows rows:
-// decode-sized batches and lightly loaded experts). The work is
-// streaming the active experts' weights, and a launch often has fewer tiles
-// than CUs or a partly filled last round, so instead of whole tiles each
-// block takes an exact, contiguous share of the launch's (tile, K chunk)
-// units (stream-K): tile t's chunks are units [t nK, t nK + nK), tiles in
-// the order of decode_tile, and block bo (blocks numbered XCD by XCD, so
-// consecutive shares sit on one XCD) takes units [U bo / Ga, U (bo + 1) / Ga).
+// Decode schedule (launches in which no expert exceeds sk_rows rows:
+// decode-sized batches and lightly loaded experts; bf16 and MXFP8). The work
+// is streaming the active experts' weights, and a launch often has fewer
+// tiles than CUs or a partly filled last round, so instead of whole tiles
+// each block takes an exact, contiguous share of the launch's
+// (tile, K chunk) units (stream-K): tile t's chunks are units
+// [t nK, t nK + nK), tiles in the order of decode_tile. Blocks are numbered
+// XCD by XCD (bo), so consecutive shares sit on one XCD. Two partitions:
+//  * per XCD: the tiles are first dealt to the 8 XCDs in contiguous ranges
+//    cut at tile boundaries, then each XCD's units to its blocks, so all
+//    blocks sharing a tile share one L2;
+//  * global: the units of the launch are cut among all blocks.
+// The per-XCD partition is used when its largest share is at most one unit
+// above the global one's (the tile count divides evenly over the XCDs, or
+// the shares are bounded by kSkMinChunks rather than by the blocks).
 // A tile whose chunks fall into the shares of several blocks is finished by
-// the last of them to arrive: each writes its fp32 sums to a slot of its own
-// with write-through (agent-scope) stores, waits for them to complete, and
-// increments the counter of the tile's first block; the block that sees the
-// final count adds the slots in block order (a fixed order, so results do not
-// depend on timing) with agent-scope loads, applies the epilogue and resets
-// the counter. No block ever waits for another.
+// the last of them to arrive: each writes its fp32 sums to a slot of its own,
+// waits for the stores to complete, and increments the counter of the tile's
+// first block; the block that sees the final count adds the slots in block
+// order (a fixed order, so results do not depend on timing), applies the
+// epilogue and resets the counter. No block ever waits for another. The
+// slots go through the XCD's L2 (ordinary stores and loads) when the
+// partition is per XCD and the XCD check confirmed that block b runs on XCD
+// b % 8; otherwise through the device's point of coherence (st_coh4 /
+// ld_coh4). Which of the two does not change a bit of the results.
 // ---------------------------------------------------------------------------
 constexpr int kSkMinChunks = 2;  // K chunks per block share, at least (when the launch has as many)
 // Largest expert for which the decode schedule is preferred when a
 // reduction launch follows anyway (same-process A/B, one to eight
 // Mixtral-shaped experts: faster up to 13-16 rows, 3-10 % slower at 29-32).
 constexpr int kSkPrefRows = 16;
+// floor(n / d) for 0 <= n, 0 < d: 32-bit division when n fits (the GPU has
+// no integer divider; a 64-bit division costs several times a 32-bit one)
+__device__ __forceinline__ long long sk_div(long long n, long long d) {
+  if (((unsigned long long)n | (unsigned long long)d) < (1ULL << 32)) return (long long)((uint32_t)n / (uint32_t)d);
+  return n / d;
+}
+// Units [u0, u0 + U) shared by blocks [b0, b0 + Ga) (share order).
 struct SkPart {
-  long long U, Ga;
-  __device__ long long start(long long b) const { return U * b / Ga; }
+  long long U, Ga, u0;
+  int b0;
+  // first unit of block bo's share
+  __device__ long long start(int bo) const { return u0 + sk_div(U * (bo - b0), Ga); }
   // the block whose share holds unit x
-  __device__ int block_of(long long x) const { return (int)(((x + 1) * Ga + U - 1) / U - 1); }
+  __device__ int block_of(long long x) const { return b0 + (int)(sk_div((x - u0 + 1) * Ga + U - 1, U) - 1); }
 };
+__device__ __forceinline__ long long sk_blocks(long long U, long long G) {
+  return max(1LL, min(G, U / kSkMinChunks));  // every block with work takes >= kSkMinChunks
+}
 
 // Sum of the nc contributors' slots of a split tile (rows [m0, m_end) of C,
-// columns [n0, n0 + 128)) in contributor order, the epilogue, and bf16
-// stores; every thread of the block takes 4 columns of a row at a time and
-// loads the slots of up to kFixBatch contributors before waiting for them.
+// columns [n0, n0 + 128)) in contributor order, the epilogue, and bf16 (or
+// MXFP8 h) stores; every thread of the block takes 4 columns of a row at a
+// time and loads the slots of up to kFixBatch contributors before waiting
+// for them. coh: the slots were written with st_coh4, else with ordinary
+// stores on this block's XCD.
 constexpr int kFixBatch = 8;
 template <bool DUAL, bool MX>
-__device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int bf, int nc, int j0) {
+__device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int bf, int nc, int j0,
+                                         bool coh) {
   constexpr int NB = DUAL ? 2 : 1;
   const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
   const int items = (m_end - m0) * 32;
+  // the CU's L1 holds no line of these slots from before their stores (each
+  // slot is written and read once a launch); invalidate it all the same
+  if (!coh) asm volatile("buffer_inv sc0" ::: "memory");
   for (int it = (int)threadIdx.x; it < items; it += kThreads) {
     const int r = it >> 5, c = (it & 31) * 4;
     const float* p0 = a.skpart + (size_t)r * 128 + c;
@@ -794,8 +838,13 @@ __device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, i
       for (int j = 0; j < kFixBatch; ++j) {
         const int q = q0 + j < nc ? q0 + j : nc - 1;  // past the last contributor: a repeated, unused load
         const float* p = p0 + ((size_t)(bf + q) * 2 + (q == 0 ? j0 : 0)) * slot_f;
-        vg[j] = ld_coh4(p);
-        if (DUAL) vu[j] = ld_coh4(p + plane);
+        if (coh) {
+          vg[j] = ld_coh4(p);
+          if (DUAL) vu[j] = ld_coh4(p + plane);
+        } else {
+          vg[j] = *reinterpret_cast<const f32x4_t*>(p);
+          if (DUAL) vu[j] = *reinterpret_cast<const f32x4_t*>(p + plane);
+        }
       }
 #pragma unroll
       for (int j = 0; j < kFixBatch; ++j)
@@ -820,24 +869,52 @@ __device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, i
   }
 }
 
+// xcd_ok: the XCD check's verdict (1: block b runs on XCD b % 8).
 template <bool DUAL, bool MX>
 __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem, int T0, const int* s_start,
-                                                const int* s_row0, const int* s_rows) {
+                                                const int* s_row0, const int* s_rows, bool xcd_ok) {
   constexpr int NB = DUAL ? 2 : 1;
   __shared__ int s_last;
   const int G = gridDim.x, b = blockIdx.x;
-  const int bo = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const bool g8 = (G & 7) == 0;
+  const int gx = G >> 3;  // blocks per XCD
+  const int bo = g8 ? (b & 7) * gx + (b >> 3) : b;
   const int nK = a.K / (MX ? kMxChunk : kBK);
+  // T0 * 8 stays far inside int: T0 <= E_local * N / 128 here
   SkPart P;
   P.U = (long long)T0 * nK;
-  P.Ga = max(1LL, min((long long)G, P.U / kSkMinChunks));  // every block with work takes >= kSkMinChunks
-  if (bo >= P.Ga) return;
-  const long long u0 = P.start(bo), u1 = P.start(bo + 1);
+  P.Ga = sk_blocks(P.U, G);
+  P.u0 = 0;
+  P.b0 = 0;
+  // per XCD when the tiles divide evenly over the XCDs (shares then differ
+  // from the global ones by at most a unit), else when the largest share
+  // grows by at most one unit (in float: a heuristic, and every block computes
+  // the same values, so every block takes the same decision)
+  bool per_xcd = g8 && (T0 & 7) == 0;
+  if (g8 && !per_xcd) {
+    float big = 0.0f;
+    for (int x = 0; x < 8; ++x) {
+      const long long ux = (long long)((T0 * (x + 1) >> 3) - (T0 * x >> 3)) * nK;
+      if (ux > 0) big = fmaxf(big, ceilf((float)ux / (float)sk_blocks(ux, gx)));
+    }
+    per_xcd = big <= ceilf((float)P.U / (float)P.Ga) + 1.0f;
+  }
+  if (per_xcd) {
+    const int x = b & 7;
+    const long long t_lo = T0 * x >> 3, t_hi = T0 * (x + 1) >> 3;
+    P.U = (t_hi - t_lo) * nK;
+    P.Ga = sk_blocks(P.U, gx);
+    P.u0 = t_lo * nK;
+    P.b0 = x * gx;
+  }
+  const bool coh = !(per_xcd && xcd_ok);
+  if (P.U == 0 || bo - P.b0 >= P.Ga) return;
+  const long long u_beg = P.start(bo), u_end = P.start(bo + 1);
   const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
-  for (long long u = u0; u < u1;) {
-    const int t = (int)(u / nK);
+  for (long long u = u_beg; u < u_end;) {
+    const int t = (int)sk_div(u, nK);
     const int kc0 = (int)(u - (long long)t * nK);
-    const int kc1 = (int)min((long long)nK, kc0 + (u1 - u));
+    const int kc1 = (int)min((long long)nK, kc0 + (u_end - u));
     const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128, a.N);
     const int cls = tile_class(tr.left);
     if (kc0 == 0 && kc1 == nK) {
@@ -847,13 +924,14 @@ __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem,
       const int bf = P.block_of(t0);
       const int nc = P.block_of(t0 + nK - 1) - bf + 1;
       const int j0 = P.start(bf) == t0 ? 0 : 1;
-      float* mine = a.skpart + ((size_t)bo * 2 + (u == u0 ? 0 : 1)) * slot_f;
-      run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128, 0);
-      __syncthreads();  // every wave's write-through stores have completed
+      float* mine = a.skpart + ((size_t)bo * 2 + (u == u_beg ? 0 : 1)) * slot_f;
+      run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128, 0,
+                                          coh);
+      __syncthreads();  // every wave's stores have completed
       if (threadIdx.x == 0) s_last = atomicAdd(a.tcnt + bf, 1) == nc - 1;
       __syncthreads();
       if (s_last) {
-        sk_fixup<DUAL, MX>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0);
+        sk_fixup<DUAL, MX>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0, coh);
         if (threadIdx.x == 0) __hip_atomic_store(a.tcnt + bf, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -872,10 +950,16 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   __shared__ int s_row0[kMaxExperts];
   __shared__ int s_rows[kMaxExperts];
   __shared__ int s_srow0[kMaxExperts];
-  __shared__ int s_tot[4][kWaves];
+  __shared__ int s_tot[6][kWaves];
 
   const int tid = threadIdx.x;
   const int E = a.E_local, G = gridDim.x;
+  __shared__ int s_xcd;
+  // the XCD check's verdict, loaded early (its latency overlaps the scan);
+  // an ordinary load: the verdict only ever changes from 0 (none yet, read
+  // as "not confirmed") to its final value, so a stale copy is safe
+  int xcd = 0;
+  if (a.sk && a.xcd_state != nullptr && tid == 0) xcd = *a.xcd_state;
 
   // Rows of each expert, clamped so no access leaves [0, M_cap).
   int rows = 0;
@@ -887,10 +971,12 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
     s_row0[tid] = o0;
     s_rows[tid] = rows;
   }
-  // tiles at 128 columns, rows, experts above 64 rows, experts with rows
-  int v[4] = {row_tiles(rows) * (a.N / 128), rows, rows > kSmallM ? 1 : 0, rows > 0 ? 1 : 0};
-  int ex[4], tot[4];
-  block_scan<4>(v, ex, tot, s_tot);
+  // tiles at 128 columns, rows, experts above 64 rows, experts with rows,
+  // experts above the decode schedule's slot rows and above kSkPrefRows
+  int v[6] = {row_tiles(rows) * (a.N / 128), rows, rows > kSmallM ? 1 : 0, rows > 0 ? 1 : 0,
+              rows > a.sk_rows ? 1 : 0, rows > kSkPrefRows ? 1 : 0};
+  int ex[6], tot[6];
+  block_scan<6>(v, ex, tot, s_tot);
   const int T0 = tot[0], R = tot[1], n_big = tot[2], n_active = tot[3];
   // Decode schedule when every expert fits a slot's rows. Otherwise tiles
   // split along K need the reduction launch; when the host launches none
@@ -900,15 +986,16 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // The decode schedule's fix-ups move more partial sums the more rows a
   // split tile holds: above kSkPrefRows rows the round schedule with split-K
   // and a reduction launch is faster, if that launch follows.
-  const bool sk_fits = a.sk && __syncthreads_count(tid < E && rows > a.sk_rows) == 0;
-  if (sk_fits && (a.no_reduce || __syncthreads_count(tid < E && rows > kSkPrefRows) == 0)) {
+  const bool sk_fits = a.sk && tot[4] == 0;
+  if (sk_fits && (a.no_reduce || tot[5] == 0)) {
     if (tid < E) s_start[tid] = ex[0];
+    if (tid == 0) s_xcd = xcd;
     if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
       a.plan[0] = 1;  // nothing for a reduction launch to do
       a.plan[2] = 1;
     }
     __syncthreads();
-    decode_schedule<DUAL, MX>(a, smem, T0, s_start, s_row0, s_rows);
+    decode_schedule<DUAL, MX>(a, smem, T0, s_start, s_row0, s_rows, s_xcd == 1);
     return;
   }
 
@@ -1375,6 +1462,88 @@ static int device_cu_count() {
   return cached[dev];
 }
 
+// XCD check. The decode schedule keeps partial sums in an XCD's L2 only if
+// the blocks that share them run on one XCD, i.e. if workgroup b of a launch
+// runs on XCD b % 8 (the hardware deals workgroups to the XCDs round robin).
+// This kernel checks that once per device: block b compares the XCC_ID
+// hardware register with b % 8; the last block to finish publishes the
+// verdict in st[0] (1: every block matched, 2: some did not; 0 until then).
+// st[1] counts mismatches, st[2] finished blocks. It has the GEMMs' block
+// size and holds a comparable share of LDS, so blocks are placed as theirs.
+static __device__ int32_t xcd_check[4];
+__global__ __launch_bounds__(kThreads) void xcd_probe_kernel(int32_t* st) {
+  __shared__ int32_t s_pad[32768];
+  int x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(x));
+  s_pad[threadIdx.x * 64] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (s_pad[0] != (int)(blockIdx.x & 7)) atomicAdd(st + 1, 1);
+    __threadfence();
+    if (atomicAdd(st + 2, 1) == (int)gridDim.x - 1) {
+      __threadfence();
+      const int bad = __hip_atomic_load(st + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(st, bad == 0 ? 1 : 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// The XCD check's verdict on the current device for a launch on stream s,
+// or nullptr (kernels then keep partial sums at the point of coherence; the
+// results are the same). The check is launched on stream s by the first call
+// on the device that is not under graph capture. Its verdict goes to launches
+// on that stream (ordered after it) and, once the check has completed, to
+// launches on any stream, so that no launch runs while the verdict changes.
+static const int32_t* xcd_state(hipStream_t s) {
+  struct Dev {
+    int32_t* ptr;
+    hipEvent_t done;
+    hipStream_t stream;
+    bool launched, ready;
+  };
+  static std::mutex mu;
+  static Dev devs[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  Dev& d = devs[dev];
+  if (d.ptr == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(xcd_check)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    d.ptr = static_cast<int32_t*>(p);
+  }
+  if (!d.launched) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    if (d.done == nullptr && hipEventCreateWithFlags(&d.done, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      d.done = nullptr;
+      return nullptr;
+    }
+    xcd_probe_kernel<<<kMaxBlocks, kThreads, 0, s>>>(d.ptr);
+    if (hipGetLastError() != hipSuccess || hipEventRecord(d.done, s) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    d.launched = true;
+    d.stream = s;
+  }
+  if (!d.ready) {
+    const hipError_t q = hipEventQuery(d.done);
+    if (q == hipSuccess)
+      d.ready = true;
+    else if (q != hipErrorNotReady)
+      (void)hipGetLastError();
+  }
+  return d.ready || s == d.stream ? d.ptr : nullptr;
+}
+
 hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, const void* w_down,
                       const int32_t* offsets, int E_local, int H, int I, int ld_gu, int ld_dn, int M_cap, bool bf16,
                       void* y_perm, void* ws, hipStream_t s, const int32_t* a_src, int a_div, int a_T,
@@ -1436,6 +1605,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   g1.sk_rows = kSkRows;
   g1.skpart = part;
   g1.tcnt = cnt + kTcntGU;
+  g1.xcd_state = L.sk_ok ? xcd_state(s) : nullptr;
   grouped_gemm_bf16_kernel<true><<<grid_for(I), kThreads, 0, s>>>(g1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1456,6 +1626,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   g2.sk_rows = kSkRows;
   g2.skpart = part;
   g2.tcnt = cnt + kTcntDN;
+  g2.xcd_state = g1.xcd_state;
   grouped_gemm_bf16_kernel<false><<<grid_for(H), kThreads, 0, s>>>(g2);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1520,6 +1691,7 @@ struct MxSplit {
   int32_t* done;   // finished-block counter (the queue's reset) or nullptr
   int32_t* tcnt;   // decode schedule: tile arrival counters, or nullptr (off)
   bool no_reduce;  // no reduction launch follows (nothing may split)
+  const int32_t* xcd;  // the XCD check's verdict (see xcd_state), or nullptr
 };
 
 static void mx_split_args(GemmArgs& g, const MxSplit& sp) {
@@ -1534,6 +1706,7 @@ static void mx_split_args(GemmArgs& g, const MxSplit& sp) {
   g.skpart = sp.part;
   g.tcnt = sp.tcnt;
   g.no_reduce = sp.no_reduce ? 1 : 0;
+  g.xcd_state = sp.xcd;
 }
 
 static hipError_t gateup_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* wgq, const uint32_t* wgs,
@@ -1618,11 +1791,11 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   // GEMM launches; when no expert can exceed kSkRows rows no reduction follows
   const bool no_reduce = M_cap <= kSkRows;
   const MxSplit sp1{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
-                    L.plan_rows, cnt + kQueueGU, cnt + kDoneGU, cnt + kTcntGU, no_reduce};
+                    L.plan_rows, cnt + kQueueGU, cnt + kDoneGU, cnt + kTcntGU, no_reduce, xcd_state(s)};
   hipError_t e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld_gu, M_cap, hq, hs, sp1, s);
   if (e != hipSuccess) return e;
   const MxSplit sp2{sp1.part, sp1.part_cap, sp1.plan, sp1.plan_rows, cnt + kQueueDN, cnt + kDoneDN, cnt + kTcntDN,
-                    no_reduce};
+                    no_reduce, sp1.xcd};
   return gemm_mx(hq, hs, wdq, wds, offsets, E_local, H, I, ld_dn, M_cap, y_perm, sp2, s);
 }
 

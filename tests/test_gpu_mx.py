@@ -3,11 +3,14 @@ against the MXFP8 oracle, through the C ABI.
 
 Rules (fixed before any GPU run):
 * quantisation (codes and scale codes): bit-exact.
-* GEMM outputs: the hardware's FP8 dot products are not exact; a probe of
-  the scaled MFMA put its error at up to 1.5e-4 of the sum of the term
-  magnitudes, so each output may differ from the fp64 result by
-  MFMA_F8_REL = 2^-10 of sum |a_i b_i| (about 6x that), plus one bf16
-  rounding on each side.
+* GEMM outputs: each product of two E4M3 codes and their power-of-two
+  scales is exact in fp32, so an output differs from the exact sum only by
+  its fp32 summation, in whatever order the hardware and the split schedule
+  take: K - 1 additions, each rounded to nearest (or kept exact) with a
+  relative error of at most 2^-24, bound the error by about (K - 1) 2^-24 sum |a_i b_i| (the standard
+  recursive-summation bound), 2^-10.2 sum |a_i b_i| at the largest K here
+  (14336). Each output may therefore differ from the fp64 result by
+  MFMA_F8_REL = 2^-10 of sum |a_i b_i|, plus one bf16 rounding on each side.
 * h (quantised in the gate/up epilogue from fp32 G, U that differ from the
   oracle's within the rule above): the scale code of each block must be one
   the oracle allows for some h within the error bound of its block, and each
