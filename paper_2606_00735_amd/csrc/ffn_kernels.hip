@@ -985,9 +985,11 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   const bool can_split = a.part != nullptr && !a.no_reduce;
   // The decode schedule's fix-ups move more partial sums the more rows a
   // split tile holds: above kSkPrefRows rows the round schedule with split-K
-  // and a reduction launch is faster, if that launch follows.
+  // and a reduction launch is faster, if that launch follows, unless the
+  // launch is tile-starved (no more tiles than half the blocks, which the
+  // round schedule could only fill by splitting every tile).
   const bool sk_fits = a.sk && tot[4] == 0;
-  if (sk_fits && (a.no_reduce || tot[5] == 0)) {
+  if (sk_fits && (a.no_reduce || tot[5] == 0 || 2 * T0 <= G)) {
     if (tid < E) s_start[tid] = ex[0];
     if (tid == 0) s_xcd = xcd;
     if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
@@ -1384,11 +1386,14 @@ static size_t round256(size_t n) { return ((n + 255) / 256) * 256; }
 constexpr size_t kCntBytes = 16384;
 constexpr int kMaxBlocks = 1024;  // grid limit of a GEMM launch (tcnt entries)
 // Rows of a decode-schedule slot: the largest expert the decode schedule
-// takes. Its fix-up moves every split tile's partial sums through the
-// point of coherence, which outweighs the gain beyond about 32 rows (a
-// one-expert launch of 64 or 128 rows ran 5-60 % slower than split-K with a
-// reduction launch; at 1-16 rows it runs 3-36 % faster).
-constexpr int kSkRows = 32;
+// takes (it finishes split tiles through the XCD's L2). Same-process A/B on
+// one expert: 27-36 % faster than split-K with reduction launches at 48-64
+// rows, 20-30 % at 80-128 rows. The host leaves out the reduction launches
+// when no expert can exceed kSkHostRows rows; between that and kSkRows the
+// GEMMs take the decode schedule only when tile-starved (on skewed batches
+// of many experts with up to 128 rows it was 20-30 % slower than rounds).
+constexpr int kSkRows = 128;
+constexpr int kSkHostRows = 64;
 // int offsets within the counters
 constexpr int kQueueGU = 0, kDoneGU = 8, kQueueDN = 16, kDoneDN = 24, kTcntGU = 64, kTcntDN = 64 + kMaxBlocks;
 static_assert((kTcntDN + kMaxBlocks) * 4 <= (int)kCntBytes, "counters");
@@ -1584,13 +1589,14 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
   // blocks per CU (a split launch has up to max(M_cap, 64 E_local) rows of
   // N columns to finish, a tail split up to G / 2 tiles of 256 x 256)
   auto reduce_grid = [&](int) { return (unsigned)(4 * cus); };
-  // The GEMMs take the decode schedule whenever no expert has more than
-  // kSkRows rows, and finish its split tiles inside their launches. When no
-  // expert can have more (a token contributes at most one row to an expert,
-  // so with the row gather the bound is min(T, M_cap)), the reduction
-  // launches are skipped: the call is two launches.
+  // The GEMMs take the decode schedule when no expert has more than
+  // kSkHostRows rows (or, tile-starved, kSkRows), and finish its split tiles
+  // inside their launches. When no expert can have more than kSkHostRows (a
+  // token contributes at most one row to an expert, so with the row gather
+  // the bound is min(T, M_cap)), the reduction launches are skipped: the
+  // call is two launches.
   const int row_bound = a_src != nullptr ? std::min(a_T, M_cap) : M_cap;
-  const bool sk = L.sk_ok && row_bound <= kSkRows;
+  const bool sk = L.sk_ok && row_bound <= kSkHostRows;
   GemmArgs g1{static_cast<const bf16_t*>(x_perm), static_cast<const bf16_t*>(w_gate),
               static_cast<const bf16_t*>(w_up), static_cast<bf16_t*>(h), offsets, E_local, M_cap, I, H,
               part, L.part_cap, plan, L.plan_rows};
@@ -1788,8 +1794,9 @@ hipError_t launch_ffn_mx(const uint8_t* xq, const uint32_t* xs, const uint8_t* w
   uint32_t* hs = reinterpret_cast<uint32_t*>(w + L.hs);
   int32_t* cnt = reinterpret_cast<int32_t*>(w);
   // as in launch_ffn: the decode schedule finishes its split tiles inside the
-  // GEMM launches; when no expert can exceed kSkRows rows no reduction follows
-  const bool no_reduce = M_cap <= kSkRows;
+  // GEMM launches; when no expert can exceed kSkHostRows rows no reduction
+  // follows
+  const bool no_reduce = M_cap <= kSkHostRows;
   const MxSplit sp1{reinterpret_cast<float*>(w + L.part), L.part_cap, reinterpret_cast<int32_t*>(w + L.plan),
                     L.plan_rows, cnt + kQueueGU, cnt + kDoneGU, cnt + kTcntGU, no_reduce, xcd_state(s)};
   hipError_t e = gateup_mx(xq, xs, wgq, wgs, wuq, wus, offsets, E_local, H, I, ld_gu, M_cap, hq, hs, sp1, s);

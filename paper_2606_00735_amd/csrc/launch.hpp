@@ -39,7 +39,7 @@ hipError_t launch_ffn(const void* x_perm, const void* w_gate, const void* w_up, 
                       int a_T = 0, size_t ws_cap = SIZE_MAX);
 // The FFN scratch of this process on the current device (kScratchBytes),
 // resolved on first use; its counters are cleared on stream s then.
-constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr size_t kScratchBytes = (size_t)128 << 20;
 hipError_t ffn_scratch(void** out, hipStream_t s);
 hipError_t launch_set_offsets(int32_t* offsets, int m, hipStream_t s);
 

@@ -336,13 +336,16 @@ def test_ffn_mx(H, I, rows):
 
 
 MX_DECODE_CASES = [
-    # no expert above 16 rows: the decode schedule (equal shares of (tile, K
-    # chunk) units per CU, split tiles finished inside the GEMMs); with M_cap
-    # at most 32 no reduction launch follows
+    # the decode schedule (equal shares of (tile, K chunk) units per CU,
+    # split tiles finished inside the GEMMs) when no expert exceeds 16 rows,
+    # or 64 rows when no reduction launch follows (M_cap at most 64), or 128
+    # rows in launches with no more tiles than half the CUs
     (4096, 14336, [9, 3, 0, 11]),     # Mixtral-shaped experts, M_cap 26
-    (7168, 2048, [1, 16, 16]),        # DSV3-shaped experts, M_cap 36 (reductions launched, nothing to do)
+    (7168, 2048, [1, 16, 16]),        # DSV3-shaped experts, M_cap 36
     (2048, 768, [3, 0, 7, 1]),        # Qwen3-shaped experts, M_cap 14
-    (4096, 2048, [20, 30]),           # 30 rows but M_cap 53: split-K instead (plan checked below)
+    (4096, 2048, [20, 30]),           # 30 rows, M_cap 53
+    (4096, 2048, [20, 30, 40]),       # 40 rows, M_cap 93, 48 gate/up and 96 down tiles: decode
+    (4096, 2048, [100, 30, 120]),     # 120 rows, M_cap 253, tile-starved: decode
 ]
 
 
@@ -356,18 +359,17 @@ def test_ffn_mx_decode_schedule(H, I, rows):
     hs_off = moe.FFN_COUNTER_BYTES + ((M_cap * I + 255) // 256) * 256
     plan_off = hs_off + (((I // 128) * M_cap * 4 + 255) // 256) * 256
     got = ws[plan_off:plan_off + 12].view(torch.int32).cpu().numpy()
-    if max(rows) <= 16:
-        assert got[0] == 1 and got[2] == 1, got
+    assert got[0] == 1 and got[2] == 1, got  # every case here takes the decode schedule
 
 
 MX_SPLIT_CASES = [
     # (H, I, rows per expert, S of the down GEMM), worked out by hand from the
-    # split rule on 256 CUs (K chunks of 128): one 64-row Mixtral-shaped expert
-    # (gate/up S = 2, down S = 8); one 256-row DSV3-shaped expert (gate/up S = 7,
-    # down S = 2: partial bytes equal to the weight bytes are still allowed);
-    # Qwen3-shaped, 5 rows (gate/up S = 2; the down GEMM's 6 chunks cannot
-    # split); Maverick-shaped experts of 400, 100 and 32 rows (down S = 3)
-    (4096, 14336, [64], 8),
+    # split rule on 256 CUs (K chunks of 128): Mixtral-shaped experts of up to
+    # 40 rows, 160 down tiles (down S = 3 over 112 chunks); one 256-row
+    # DSV3-shaped expert (gate/up S = 7, down S = 2: partial bytes equal to the
+    # weight bytes are still allowed); Qwen3-shaped, 5 rows (decode schedule);
+    # Maverick-shaped experts of 400, 100 and 32 rows (down S = 3)
+    (4096, 14336, [40, 7, 0, 19, 30, 25], 3),
     (7168, 2048, [256], 2),
     (2048, 768, [5], 1),
     (5120, 8192, [400, 100, 32], 3),

@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 CASES = [
     # (workload, rows per local expert for call 1, for call 2 (smaller))
     ("mixtral", [9, 14, 3, 0, 11, 8, 12, 7], [5, 0, 2, 1, 0, 3, 0, 1]),     # decode schedule in both
-    ("qwen3", [40] * 8 + [0] * 8, [3] * 4 + [0] * 12),                       # split-K, then decode schedule
+    ("qwen3", [40] * 24 + [0] * 8, [3] * 4 + [0] * 28),                      # rounds (split), then decode schedule
     ("tiny", [17, 0, 30, 5, 9, 2, 1, 64], [4, 0, 1, 0, 0, 2, 0, 3]),          # fp32
 ]
 
