@@ -181,18 +181,19 @@ moe_status moe_permute(const void* x, const int32_t* topk_ids, const int32_t* ex
  *              zero before the first call that uses the workspace (allocate
  *              it zero-filled); every call leaves them zero again. Calls on
  *              one workspace must not overlap.
- *              Schedule (bf16): when no expert has more than 64 rows (16
- *              when a reduction launch follows anyway, see below; 128 in a
+ *              Schedule (bf16): when no expert has more than 16 rows, or
+ *              64 when no reduction launch follows (see below), or 128 in a
  *              GEMM launch with no more 128-column tiles than half its
- *              blocks) each GEMM's (tile, K chunk) units are dealt to the CUs in equal
- *              shares and tiles split between CUs are finished inside the
- *              GEMM launch; otherwise whole tiles run in rounds, with
- *              split-K for tile-starved launches and a split of a partly
- *              filled last round, whose partials a launch after each GEMM
- *              sums. When no expert can have more than 64 rows (M_cap <= 64;
- *              for the _gather variant min(T, M_cap) <= 64, since a token
- *              adds at most one row to an expert) those launches are left
- *              out: two kernel launches in all. The first call on a device
+ *              blocks, each GEMM's (tile, K chunk) units are dealt to the
+ *              CUs in equal shares and tiles split between CUs are finished
+ *              inside the GEMM launch; otherwise whole tiles run in rounds,
+ *              with split-K for tile-starved launches and a split of a
+ *              partly filled last round, whose partials a launch after each
+ *              GEMM sums. When no expert can have more than 128 rows
+ *              (M_cap <= 128; for the _gather variant min(T, M_cap) <= 128,
+ *              since a token adds at most one row to an expert) those
+ *              launches are left out (two kernel launches in all) and
+ *              nothing is split outside the decode schedule. The first call on a device
  *              that is not under graph capture also launches a small
  *              one-time check of the GPU's workgroup-to-XCD assignment.
  * Limits: 0 <= E_local <= 256 (0 is a no-op); bf16: H % 128 == 0 and
@@ -209,7 +210,7 @@ moe_status moe_grouped_swiglu_ffn(const void* x_perm, const void* w_gate, const 
  *
  * Computes what moe_permute followed by moe_grouped_swiglu_ffn computes
  * (bitwise the same y_perm and h whenever both take the same schedule; with
- * T <= 64 this one may finish split tiles in its GEMM launches where the
+ * T <= 128 this one may finish split tiles in its GEMM launches where the
  * permuted call, bounded only by M_cap, splits differently, and results then
  * agree within the FFN's tolerance), but row r of the expert input is
  * read as x[perm_src[r] / k] (the token of flat assignment perm_src[r],

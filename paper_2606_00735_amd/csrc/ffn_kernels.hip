@@ -984,12 +984,14 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // break that bound get here) nothing is split.
   const bool can_split = a.part != nullptr && !a.no_reduce;
   // The decode schedule's fix-ups move more partial sums the more rows a
-  // split tile holds: above kSkPrefRows rows the round schedule with split-K
-  // and a reduction launch is faster, if that launch follows, unless the
-  // launch is tile-starved (no more tiles than half the blocks, which the
-  // round schedule could only fill by splitting every tile).
+  // split tile holds: above kSkPrefRows rows the round schedule is faster
+  // (with split-K and a reduction launch, if one follows), unless the launch
+  // is tile-starved (no more tiles than half the blocks, which rounds could
+  // only fill by splitting every tile) or, with no reduction launch to
+  // follow, no expert exceeds 64 rows. Otherwise a launch with no reduction
+  // to follow runs whole tiles in rounds.
   const bool sk_fits = a.sk && tot[4] == 0;
-  if (sk_fits && (a.no_reduce || tot[5] == 0 || 2 * T0 <= G)) {
+  if (sk_fits && (tot[5] == 0 || 2 * T0 <= G || (a.no_reduce && n_big == 0))) {
     if (tid < E) s_start[tid] = ex[0];
     if (tid == 0) s_xcd = xcd;
     if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
@@ -1388,12 +1390,14 @@ constexpr int kMaxBlocks = 1024;  // grid limit of a GEMM launch (tcnt entries)
 // Rows of a decode-schedule slot: the largest expert the decode schedule
 // takes (it finishes split tiles through the XCD's L2). Same-process A/B on
 // one expert: 27-36 % faster than split-K with reduction launches at 48-64
-// rows, 20-30 % at 80-128 rows. The host leaves out the reduction launches
-// when no expert can exceed kSkHostRows rows; between that and kSkRows the
-// GEMMs take the decode schedule only when tile-starved (on skewed batches
-// of many experts with up to 128 rows it was 20-30 % slower than rounds).
+// rows, 20-30 % at 80-128 rows; on skewed batches of many experts with up
+// to 128 rows it was 20-30 % slower than rounds, so above 64 rows it is
+// taken only by tile-starved launches (see grouped_gemm_body). The host
+// leaves out the reduction launches when no expert can exceed kSkHostRows
+// rows: every launch then either takes the decode schedule or runs whole
+// tiles in rounds, which such launches fill without splitting.
 constexpr int kSkRows = 128;
-constexpr int kSkHostRows = 64;
+constexpr int kSkHostRows = 128;
 // int offsets within the counters
 constexpr int kQueueGU = 0, kDoneGU = 8, kQueueDN = 16, kDoneDN = 24, kTcntGU = 64, kTcntDN = 64 + kMaxBlocks;
 static_assert((kTcntDN + kMaxBlocks) * 4 <= (int)kCntBytes, "counters");

@@ -338,7 +338,7 @@ def test_ffn_mx(H, I, rows):
 MX_DECODE_CASES = [
     # the decode schedule (equal shares of (tile, K chunk) units per CU,
     # split tiles finished inside the GEMMs) when no expert exceeds 16 rows,
-    # or 64 rows when no reduction launch follows (M_cap at most 64), or 128
+    # or 64 rows when no reduction launch follows (M_cap at most 128), or 128
     # rows in launches with no more tiles than half the CUs
     (4096, 14336, [9, 3, 0, 11]),     # Mixtral-shaped experts, M_cap 26
     (7168, 2048, [1, 16, 16]),        # DSV3-shaped experts, M_cap 36
@@ -365,11 +365,11 @@ def test_ffn_mx_decode_schedule(H, I, rows):
 MX_SPLIT_CASES = [
     # (H, I, rows per expert, S of the down GEMM), worked out by hand from the
     # split rule on 256 CUs (K chunks of 128): Mixtral-shaped experts of up to
-    # 40 rows, 160 down tiles (down S = 3 over 112 chunks); one 256-row
+    # 40 rows, M_cap 134, 192 down tiles (down S = 4 over 112 chunks); one 256-row
     # DSV3-shaped expert (gate/up S = 7, down S = 2: partial bytes equal to the
     # weight bytes are still allowed); Qwen3-shaped, 5 rows (decode schedule);
     # Maverick-shaped experts of 400, 100 and 32 rows (down S = 3)
-    (4096, 14336, [40, 7, 0, 19, 30, 25], 3),
+    (4096, 14336, [40, 7, 0, 19, 30, 25, 10], 4),
     (7168, 2048, [256], 2),
     (2048, 768, [5], 1),
     (5120, 8192, [400, 100, 32], 3),

@@ -60,12 +60,12 @@ def test_layer_parity(name, T, alpha):
     print("  stats", stats, "M_loc", int(r["offsets"][-1]), flush=True)
 
 
-# The FFN's decode schedule (include/moe.h): taken when no expert exceeds
-# 16 rows, or 64 rows when the host's bound on an expert's rows is at most 64
-# (M_cap; min(T, M_cap) for the gathering FFN, so the two calls can differ
-# there), or 128 rows in tile-starved launches (the same for both). Two
-# calls give the same bits when they take the same schedule.
-HOST_ROWS, PREF_ROWS = 64, 16
+# The FFN's schedule (include/moe.h) depends on the host's bound on an
+# expert's rows (M_cap; min(T, M_cap) for the gathering FFN) only through
+# whether it is at most 128 (then no reduction launch follows), and otherwise
+# on the rows and tiles, the same for both calls. Two calls give the same
+# bits when they take the same schedule.
+HOST_ROWS, PREF_ROWS = 128, 16
 
 
 def _same_schedule(max_rows, bound_a, bound_b):
@@ -361,22 +361,23 @@ SPLIT_CASES = [
     # Each GEMM launch takes the decode schedule (equal shares of (tile, K
     # chunk) units per CU, split tiles finished in the GEMM; the plan then
     # says 1) when no expert exceeds 16 rows, or 64 rows when no reduction
-    # launch follows (M_cap <= 64), or 128 rows when it has no more 128-column
+    # launch follows (M_cap <= 128), or 128 rows when it has no more 128-column
     # tiles than half its blocks (256 CUs here); other launches run tiles in
     # rounds, split along K (S from the split rule) when they have fewer
-    # tiles than CUs.
+    # tiles than CUs and a reduction launch follows.
     (1024, 2048, [40] * 20, 3),            # 160 down tiles: split-K, S = 3 (32 chunks)
     (4096, 14336, [64], 1),                # one Mixtral-shaped expert of 64 rows, M_cap 67: 32 down tiles, decode
     (4096, 14336, [1], 1),                 # decode schedule
     (4096, 14336, [16, 7, 0, 11], 1),      # decode schedule at its preferred 16-row bound
     (4096, 14336, [32, 7, 0, 19], 1),      # 32 rows, M_cap 61: no reduction launch, decode schedule
-    (4096, 14336, [40, 7, 0, 19, 30, 25], 3),  # M_cap 124, 160 down tiles: split-K, S = 3 (224 chunks)
+    (4096, 14336, [40, 7, 0, 19, 30, 25], 1),  # M_cap 124: no reduction launch, decode schedule
+    (4096, 14336, [40, 7, 0, 19, 30, 25, 10], 4),  # M_cap 134, 192 down tiles: split-K, S = 4 (224 chunks)
     (1024, 2048, [65, 3, 0, 1], 1),        # a 65-row expert, M_cap 72, 24 down tiles: decode schedule
     (4096, 14336, [128], 1),               # a 128-row expert, M_cap 131, 32 down tiles: decode schedule
     (7168, 2048, [256], 4),                # a 256-row DSV3-shaped expert: gate/up S = 8, down S = 4
     (5120, 8192, [400, 100, 32], 3),       # Maverick-shaped experts of mixed size: down S = 3
     (7168, 2048, [1, 33], 1),              # DSV3-shaped experts, M_cap 37: decode schedule
-    (7168, 2048, [1, 33, 40], 3),          # M_cap 77, 168 down tiles: split-K, S = 3 (32 chunks)
+    (7168, 2048, [1, 33, 40, 60, 5], 1),   # M_cap 142, 280 down tiles: rounds, last one split along K (plan S = 1)
     (7168, 2048, [1], 1),                  # one DSV3-shaped expert: decode schedule
     (5120, 8192, [1], 1),                  # one Maverick-shaped expert: decode schedule
     (2048, 768, [5], 1),                   # one Qwen3-shaped expert: decode schedule
