@@ -1359,10 +1359,11 @@ __global__ __launch_bounds__(256) void down_f32_kernel(const float* __restrict__
   y[(size_t)row * H + c] = s;
 }
 
-// Clears the per-XCD work counters of an FFN call (a kernel, not a memset,
-// so that the call can be captured in a graph).
+// Zeroes the work counters at the start of the scratch of the entry point
+// that allocates nothing, at its first use on a device (a kernel, not a
+// memset, so that a first call under graph capture records no memset).
 __global__ void clear_counters_kernel(int32_t* q, int n) {
-  if ((int)threadIdx.x < n) q[threadIdx.x] = 0;
+  for (int i = (int)threadIdx.x; i < n; i += (int)blockDim.x) q[i] = 0;
 }
 
 __global__ void set_offsets_kernel(int32_t* offsets, int m) {
