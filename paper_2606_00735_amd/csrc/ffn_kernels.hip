@@ -99,7 +99,7 @@ struct GemmArgs {
   float* skpart;
   int32_t* tcnt;
   int no_reduce;
-  // Verdict of the XCD check (see xcd_probe_kernel; 1: block b of a launch
+  // Result of the XCD check (see xcd_probe_kernel; 1: block b of a launch
   // runs on XCD b % 8), or nullptr. The decode schedule reads it to choose
   // L2-local partial sums; results do not depend on it.
   const int32_t* xcd_state;
@@ -813,24 +813,27 @@ __device__ __forceinline__ long long sk_blocks(long long U, long long G) {
 }
 
 // Sum of the nc contributors' slots of a split tile (rows [m0, m_end) of C,
-// columns [n0, n0 + 128)) in contributor order, the epilogue, and bf16 (or
-// MXFP8 h) stores; every thread of the block takes 4 columns of a row at a
-// time and loads the slots of up to kFixBatch contributors before waiting
-// for them. coh: the slots were written with st_coh4, else with ordinary
-// stores on this block's XCD.
+// columns [n0, n0 + cols): cols = 128 per matrix, or 256 for a single GEMM's
+// wide tile) in contributor order, the epilogue, and bf16 (or MXFP8 h)
+// stores; every thread of the block takes 4 columns of a row at a time and
+// loads the slots of up to kFixBatch contributors before waiting for them.
+// coh: the slots were written with st_coh4, else with ordinary stores on
+// this block's XCD. A slot holds NB planes of sk_rows x cols floats
+// (2 x 128 or 1 x 256 columns: the same size).
 constexpr int kFixBatch = 8;
 template <bool DUAL, bool MX>
-__device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int bf, int nc, int j0,
-                                         bool coh) {
+__device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, int n0, int cols, int bf, int nc,
+                                         int j0, bool coh) {
   constexpr int NB = DUAL ? 2 : 1;
-  const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
-  const int items = (m_end - m0) * 32;
+  const size_t plane = (size_t)a.sk_rows * cols, slot_f = NB * plane;
+  const int c4 = cols / 4;  // items per row
+  const int items = (m_end - m0) * c4;
   // the CU's L1 holds no line of these slots from before their stores (each
   // slot is written and read once a launch); invalidate it all the same
   if (!coh) asm volatile("buffer_inv sc0" ::: "memory");
   for (int it = (int)threadIdx.x; it < items; it += kThreads) {
-    const int r = it >> 5, c = (it & 31) * 4;
-    const float* p0 = a.skpart + (size_t)r * 128 + c;
+    const int r = it / c4, c = (it - r * c4) * 4;
+    const float* p0 = a.skpart + (size_t)r * cols + c;
     f32x4_t g = f32x4_t{}, u = f32x4_t{};
     for (int q0 = 0; q0 < nc; q0 += kFixBatch) {
       f32x4_t vg[kFixBatch], vu[kFixBatch];
@@ -869,11 +872,14 @@ __device__ __forceinline__ void sk_fixup(const GemmArgs& a, int m0, int m_end, i
   }
 }
 
-// xcd_ok: the XCD check's verdict (1: block b runs on XCD b % 8).
+// xcd_ok: the XCD check's result (1: block b runs on XCD b % 8). wide: a
+// single GEMM in 256-column tiles (T0 and s_start count those tiles), which
+// halves the tiles, and so the pipeline fills, of short-K launches.
 template <bool DUAL, bool MX>
 __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem, int T0, const int* s_start,
-                                                const int* s_row0, const int* s_rows, bool xcd_ok) {
+                                                const int* s_row0, const int* s_rows, bool xcd_ok, bool wide) {
   constexpr int NB = DUAL ? 2 : 1;
+  const int cols = wide ? 256 : 128;
   __shared__ int s_last;
   const int G = gridDim.x, b = blockIdx.x;
   const bool g8 = (G & 7) == 0;
@@ -910,28 +916,44 @@ __device__ __forceinline__ void decode_schedule(const GemmArgs& a, bf16_t* smem,
   const bool coh = !(per_xcd && xcd_ok);
   if (P.U == 0 || bo - P.b0 >= P.Ga) return;
   const long long u_beg = P.start(bo), u_end = P.start(bo + 1);
-  const size_t plane = (size_t)a.sk_rows * 128, slot_f = NB * plane;
+  const size_t plane = (size_t)a.sk_rows * cols, slot_f = NB * plane;
   for (long long u = u_beg; u < u_end;) {
     const int t = (int)sk_div(u, nK);
     const int kc0 = (int)(u - (long long)t * nK);
     const int kc1 = (int)min((long long)nK, kc0 + (u_end - u));
-    const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, 128, a.N);
+    const TileRef tr = decode_tile(t, a.E_local, s_start, s_row0, s_rows, cols, a.N);
     const int cls = tile_class(tr.left);
     if (kc0 == 0 && kc1 == nK) {
-      run_tile<DUAL, MX, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+      if constexpr (!DUAL) {
+        if (wide)
+          run_tile<DUAL, MX, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+        else
+          run_tile<DUAL, MX, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+      } else {
+        run_tile<DUAL, MX, false>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0);
+      }
     } else {
       const long long t0 = (long long)t * nK;
       const int bf = P.block_of(t0);
       const int nc = P.block_of(t0 + nK - 1) - bf + 1;
       const int j0 = P.start(bf) == t0 ? 0 : 1;
       float* mine = a.skpart + ((size_t)bo * 2 + (u == u_beg ? 0 : 1)) * slot_f;
-      run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128, 0,
-                                          coh);
+      if constexpr (!DUAL) {
+        if (wide)
+          run_split_tile<DUAL, MX, 256, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane,
+                                              256, 0, coh);
+        else
+          run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane,
+                                              128, 0, coh);
+      } else {
+        run_split_tile<DUAL, MX, 128, true>(a, smem, cls, tr.e, tr.m0, tr.m_end, tr.n0, kc0, kc1, mine, plane, 128,
+                                            0, coh);
+      }
       __syncthreads();  // every wave's stores have completed
       if (threadIdx.x == 0) s_last = atomicAdd(a.tcnt + bf, 1) == nc - 1;
       __syncthreads();
       if (s_last) {
-        sk_fixup<DUAL, MX>(a, tr.m0, tr.m_end, tr.n0, bf, nc, j0, coh);
+        sk_fixup<DUAL, MX>(a, tr.m0, tr.m_end, tr.n0, cols, bf, nc, j0, coh);
         if (threadIdx.x == 0) __hip_atomic_store(a.tcnt + bf, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -955,8 +977,8 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   const int tid = threadIdx.x;
   const int E = a.E_local, G = gridDim.x;
   __shared__ int s_xcd;
-  // the XCD check's verdict, loaded early (its latency overlaps the scan);
-  // an ordinary load: the verdict only ever changes from 0 (none yet, read
+  // the XCD check's result, loaded early (its latency overlaps the scan);
+  // an ordinary load: the result only ever changes from 0 (none yet, read
   // as "not confirmed") to its final value, so a stale copy is safe
   int xcd = 0;
   if (a.sk && a.xcd_state != nullptr && tid == 0) xcd = *a.xcd_state;
@@ -992,14 +1014,21 @@ __device__ __forceinline__ void grouped_gemm_body(const GemmArgs& a) {
   // to follow runs whole tiles in rounds.
   const bool sk_fits = a.sk && tot[4] == 0;
   if (sk_fits && (tot[5] == 0 || 2 * T0 <= G || (a.no_reduce && n_big == 0))) {
-    if (tid < E) s_start[tid] = ex[0];
+    // a single GEMM with at least as many 256-column tiles as blocks takes
+    // them (the tile counts at 128 columns are even then): each block then
+    // runs whole tiles, half as many pipeline fills (same-process A/B,
+    // Qwen3-shaped T = 128, 128 experts of up to 13 rows: FFN 233 -> 220 us).
+    // With fewer tiles, wider ones only split more (one expert: up to 70 %
+    // slower)
+    const bool dwide = !DUAL && (a.N % 256) == 0 && T0 / 2 >= G;
+    if (tid < E) s_start[tid] = dwide ? ex[0] / 2 : ex[0];
     if (tid == 0) s_xcd = xcd;
     if (blockIdx.x == 0 && tid == 0 && a.plan != nullptr) {
       a.plan[0] = 1;  // nothing for a reduction launch to do
       a.plan[2] = 1;
     }
     __syncthreads();
-    decode_schedule<DUAL, MX>(a, smem, T0, s_start, s_row0, s_rows, s_xcd == 1);
+    decode_schedule<DUAL, MX>(a, smem, dwide ? T0 / 2 : T0, s_start, s_row0, s_rows, s_xcd == 1, dwide);
     return;
   }
 
@@ -1477,7 +1506,7 @@ static int device_cu_count() {
 // runs on XCD b % 8 (the hardware deals workgroups to the XCDs round robin).
 // This kernel checks that once per device: block b compares the XCC_ID
 // hardware register with b % 8; the last block to finish publishes the
-// verdict in st[0] (1: every block matched, 2: some did not; 0 until then).
+// result in st[0] (1: every block matched, 2: some did not; 0 until then).
 // st[1] counts mismatches, st[2] finished blocks. It has the GEMMs' block
 // size and holds a comparable share of LDS, so blocks are placed as theirs.
 static __device__ int32_t xcd_check[4];
@@ -1498,12 +1527,12 @@ __global__ __launch_bounds__(kThreads) void xcd_probe_kernel(int32_t* st) {
   }
 }
 
-// The XCD check's verdict on the current device for a launch on stream s,
+// The XCD check's result on the current device for a launch on stream s,
 // or nullptr (kernels then keep partial sums at the point of coherence; the
 // results are the same). The check is launched on stream s by the first call
-// on the device that is not under graph capture. Its verdict goes to launches
+// on the device that is not under graph capture. Its result goes to launches
 // on that stream (ordered after it) and, once the check has completed, to
-// launches on any stream, so that no launch runs while the verdict changes.
+// launches on any stream, so that no launch runs while the result changes.
 static const int32_t* xcd_state(hipStream_t s) {
   struct Dev {
     int32_t* ptr;
@@ -1702,7 +1731,7 @@ struct MxSplit {
   int32_t* done;   // finished-block counter (the queue's reset) or nullptr
   int32_t* tcnt;   // decode schedule: tile arrival counters, or nullptr (off)
   bool no_reduce;  // no reduction launch follows (nothing may split)
-  const int32_t* xcd;  // the XCD check's verdict (see xcd_state), or nullptr
+  const int32_t* xcd;  // the XCD check's result (see xcd_state), or nullptr
 };
 
 static void mx_split_args(GemmArgs& g, const MxSplit& sp) {
