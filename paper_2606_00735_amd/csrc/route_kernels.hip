@@ -47,6 +47,50 @@ __device__ __forceinline__ int block_exclusive_scan_256(int v, int* s_wave_tot, 
 // (value descending, column ascending). Every lane of the group ends with the
 // same selection.
 // ---------------------------------------------------------------------------
+// Best (value, column) of each group of GROUP = 32 or 64 consecutive lanes,
+// returned in every lane of the group, by DPP (a few cycles a step, where a
+// lane shuffle through LDS takes tens): a running best along each row of 16
+// lanes (row_shr 1, 2, 4, 8; lanes shifted in from outside the row offer
+// (-inf, INT_MAX), which never wins), leaving each row's best in its lane
+// 15; row_bcast:15 then gives lanes 31 and 63 the best of rows 0-1 and 2-3,
+// and row_bcast:31 lane 63 the best of all four. The order (value
+// descending, column ascending) is strict, so the winner does not depend on
+// the reduction's shape.
+// One DPP step of group_best: (v, i) becomes the better of itself and the
+// pair DPP control CTRL brings from another lane of rows ROW_MASK.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void best_dpp(float& v, int& i) {
+  const float ov = __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(-__builtin_huge_valf()), __float_as_int(v), CTRL, ROW_MASK, 0xf, false));
+  const int oi = __builtin_amdgcn_update_dpp(0x7fffffff, i, CTRL, ROW_MASK, 0xf, false);
+  if (better(ov, oi, v, i)) {
+    v = ov;
+    i = oi;
+  }
+}
+
+template <int GROUP>
+__device__ __forceinline__ void group_best(float& v, int& i) {
+  static_assert(GROUP == 32 || GROUP == 64, "group of 32 or 64 lanes");
+  best_dpp<0x111, 0xf>(v, i);  // row_shr:1
+  best_dpp<0x112, 0xf>(v, i);  // row_shr:2
+  best_dpp<0x114, 0xf>(v, i);  // row_shr:4
+  best_dpp<0x118, 0xf>(v, i);  // row_shr:8
+  best_dpp<0x142, 0xa>(v, i);  // row_bcast:15 into rows 1, 3
+  if (GROUP == 64) {
+    best_dpp<0x143, 0xc>(v, i);  // row_bcast:31 into rows 2, 3
+    v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+    i = __builtin_amdgcn_readlane(i, 63);
+  } else {
+    const float v0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 31));
+    const float v1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+    const int i0 = __builtin_amdgcn_readlane(i, 31), i1 = __builtin_amdgcn_readlane(i, 63);
+    const bool hi = (threadIdx.x & 32) != 0;
+    v = hi ? v1 : v0;
+    i = hi ? i1 : i0;
+  }
+}
+
 template <int GROUP, int NV>
 __device__ __forceinline__ void topk_group(const float (&val)[NV], int g, int E, int k,
                                            float (&sel_v)[kMaxTopk], int (&sel_i)[kMaxTopk]) {
@@ -64,15 +108,7 @@ __device__ __forceinline__ void topk_group(const float (&val)[NV], int g, int E,
           li = col;
         }
       }
-#pragma unroll
-      for (int off = GROUP / 2; off >= 1; off >>= 1) {
-        float ov = __shfl_xor(lv, off, GROUP);
-        int oi = __shfl_xor(li, off, GROUP);
-        if (better(ov, oi, lv, li)) {
-          lv = ov;
-          li = oi;
-        }
-      }
+      group_best<GROUP>(lv, li);
       sel_v[j] = lv;
       sel_i[j] = li;
       if ((li % GROUP) == g) taken |= 1u << (li / GROUP);
