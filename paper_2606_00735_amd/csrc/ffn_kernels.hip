@@ -1554,12 +1554,13 @@ static const int32_t* xcd_state(hipStream_t s) {
     }
     d.ptr = static_cast<int32_t*>(p);
   }
+  // no launch, event record or event query under graph capture (they could
+  // end it); the result is then passed on only if it is known
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
+  const bool capturing = hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+  if (capturing) (void)hipGetLastError();
   if (!d.launched) {
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusActive;
-    if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
-      (void)hipGetLastError();
-      return nullptr;
-    }
+    if (capturing) return nullptr;
     if (d.done == nullptr && hipEventCreateWithFlags(&d.done, hipEventDisableTiming) != hipSuccess) {
       (void)hipGetLastError();
       d.done = nullptr;
@@ -1573,7 +1574,7 @@ static const int32_t* xcd_state(hipStream_t s) {
     d.launched = true;
     d.stream = s;
   }
-  if (!d.ready) {
+  if (!d.ready && !capturing) {
     const hipError_t q = hipEventQuery(d.done);
     if (q == hipSuccess)
       d.ready = true;
