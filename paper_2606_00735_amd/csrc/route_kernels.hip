@@ -922,16 +922,16 @@ static int device_cus() {
   return n;
 }
 
-// Largest batch the split router takes for E = 128 (kRouterSplitMaxT128, or
-// kRouterSplitMaxT128Wide for rows of at least 4096 elements): beyond it
-// the one-pass kernels fill the CUs with 128-token blocks and were measured
-// as fast or faster with the last-level cache flushed before each call
-// (H = 5120: 8192 tokens 56 us split vs 83 one pass, 32768 tokens 152 vs
-// 144; H = 2048: 8192 tokens 46 vs 46, 16384 tokens 69 vs 64). At E = 256
-// the one-pass kernel re-reads all 256 router rows per 64 tokens, so the
-// split router takes every batch.
+// Batches the split router takes for E = 128: up to kRouterSplitMaxT128
+// tokens for rows shorter than 4096 elements; for longer rows every batch
+// whose 128-token blocks would fill at most half the CUs, where the one-pass
+// kernel leaves CUs idle. Measured with the last-level cache flushed before
+// each call, H = 5120: 8192 tokens 56 us split vs 83 one pass, 12000 tokens
+// 69 vs 92, 16384 tokens 90 vs 95, but 32768 tokens (256 blocks) 151 vs
+// 141; H = 2048: 8192 tokens 46 vs 46, 16384 tokens 69 vs 64. At E = 256 the
+// one-pass kernel re-reads all 256 router rows per 64 tokens, so the split
+// router takes every batch.
 constexpr int kRouterSplitMaxT128 = 4096;
-constexpr int kRouterSplitMaxT128Wide = 8192;
 constexpr size_t kRouterSplitMaxBytes = 256ull << 20;  // partial logits at most
 
 // K ranges of the split router for T tokens (0: not used). E = 128 or 256
@@ -939,7 +939,7 @@ constexpr size_t kRouterSplitMaxBytes = 256ull << 20;  // partial logits at most
 // the partials within kRouterSplitMaxBytes.
 static int router_split_factor(int T, int H, int E) {
   if ((E != 128 && E != 256) || T < 1 || H % kGateBK != 0) return 0;
-  if (E == 128 && T > (H >= 4096 ? kRouterSplitMaxT128Wide : kRouterSplitMaxT128)) return 0;
+  if (E == 128 && (H >= 4096 ? 2LL * ((T + 127) / 128) > device_cus() : T > kRouterSplitMaxT128)) return 0;
   const long long tiles = (T + 255) / 256;
   const int nK = H / kGateBK;
   long long S = device_cus() / tiles;

@@ -79,13 +79,17 @@ def test_gate_topk_workspace(L):
                            None) == 0
     big = n.value
     assert big >= 16384 * 256 * 4 and big % 256 == 0
-    for T, H, E in ((1, 2048, 128), (128, 2048, 128), (4096, 5120, 128), (8192, 5120, 128), (512, 7168, 256),
+    for T, H, E in ((1, 2048, 128), (128, 2048, 128), (4096, 5120, 128), (8192, 5120, 128), (8193, 5120, 128),
+                    (16384, 5120, 128), (512, 7168, 256),
                     (32, 4096, 8),
                     (16, 4096, 8), (256, 2048, 96)):
         assert L.moe_gate_topk(None, None, None, T, H, E, 1, 1, None, None, None, None, ctypes.byref(n),
                                None) == 0
         assert n.value >= T * E * 4, (T, H, E)
-    for T, H, E, dt in ((16384, 7168, 256, 0), (8192, 2048, 128, 1), (8193, 5120, 128, 1), (16384, 4096, 8, 1),
+    # (no GPU here: the launcher assumes 256 CUs, so rows of 5120 split up to
+    # 16384 tokens, 128 blocks of 128 tokens)
+    for T, H, E, dt in ((16384, 7168, 256, 0), (8192, 2048, 128, 1), (16385, 5120, 128, 1), (32768, 5120, 128, 1),
+                        (16384, 4096, 8, 1),
                         (4096, 2048, 96, 1),
                         (257, 4096, 8, 1), (32, 1088, 8, 1), (1, 4096, 8, 1), (15, 4096, 8, 1)):
         n = ctypes.c_size_t(123)

@@ -280,7 +280,8 @@ ROUTER_SPLIT = [
     (5120, 128, 1, 3000),     # Maverick-shaped: 12 tiles x 8 ranges, ragged last tile
     (256, 256, 8, 66000),     # 258 tiles: one K range
     (2048, 128, 8, 4096),     # Qwen3-shaped, the largest E = 128 batch it takes at H < 4096
-    (5120, 128, 1, 6000),     # Maverick-shaped: rows of 5120 take up to 8192 tokens (ragged tile)
+    (5120, 128, 1, 6000),     # Maverick-shaped, ragged tile
+    (5120, 128, 1, 12000),    # rows of 5120: batches whose 128-token blocks half-fill the CUs (ragged tile)
     (7168, 256, 8, 77),       # decode-sized DSV3-shaped batch
     # decode-sized batches over <= 128 experts: 32-token blocks x K ranges
     (4096, 8, 2, 32),         # Mixtral-shaped decode: 8 ranges of 32 k-steps
