@@ -90,12 +90,15 @@ int moe_abi_version(void);
  *            fixed order before the top-k:
  *              - batches of at most 256 tokens over at most 128 experts
  *                (when a 32-token block's distinct x and router rows reach
- *                192 KB): 32-token blocks times up to 8 K ranges;
- *              - 256 experts (any batch) or 128 experts (up to 4096 tokens,
- *                8192 when H >= 4096):
- *                256-token tiles times K ranges, so a CU loads 256 tokens'
- *                rows and a K range of the router rows instead of every
- *                router row for each 64 tokens.
+ *                192 KB), and batches over at most 64 experts whose
+ *                32-token blocks would fill at most half the CUs: 32-token
+ *                blocks times up to 8 K ranges;
+ *              - 256 experts (any batch) or 128 experts (up to 4096 tokens;
+ *                when H >= 4096, every batch whose 128-token blocks would
+ *                fill at most half the CUs): 256-token tiles times K
+ *                ranges, so a CU loads 256 tokens' rows and a K range of
+ *                the router rows instead of every router row for each 64
+ *                or 128 tokens.
  *            The count is 0 where no workspace is used (fp32 and every other
  *            case). It depends on the device's compute-unit count: query it
  *            with the device the call will run on current.
