@@ -892,9 +892,114 @@ __global__ __launch_bounds__(256) void gate_topk_reduce_kernel(const float* __re
   write_topk(sel_v, sel_i, lane, k, row, ids, wts);
 }
 
+// The same pass for 256-column partial rows (E = 256): 16 lanes per token,
+// four tokens per wave, lane g of a token holding columns [16 g, 16 g + 16)
+// (four 16-byte loads per slice). A selection round then takes a 16-value
+// scan in the lane and four DPP steps in its row instead of six steps over
+// the whole wave for every token. Same sums in the same order, same
+// selection order (value descending, then column ascending), same weights
+// (same-process A/B, DSV3-shaped router at T = 16384: 138 -> 132 us).
+template <int S>
+__global__ __launch_bounds__(256) void gate_topk_reduce16_kernel(const float* __restrict__ part, int T, int E,
+                                                                 int k, const float* __restrict__ bias,
+                                                                 float* __restrict__ logits,
+                                                                 int32_t* __restrict__ ids, float* __restrict__ wts) {
+  static_assert(S >= 1 && S <= kMaxRouterSplit, "slices");
+  constexpr int EP = 256;
+  const int lane = threadIdx.x & 63, g = lane & 15;
+  const int row = ((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6)) * 4 + (lane >> 4);
+  const bool live = row < T;
+  const int rr = live ? row : T - 1;  // every lane takes part in the DPP steps
+  float p[S][16];
+#pragma unroll
+  for (int sp = 0; sp < S; ++sp) {
+    const float4* src = reinterpret_cast<const float4*>(part + ((size_t)sp * T + rr) * EP + 16 * g);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 f = src[q];
+      p[sp][4 * q] = f.x;
+      p[sp][4 * q + 1] = f.y;
+      p[sp][4 * q + 2] = f.z;
+      p[sp][4 * q + 3] = f.w;
+    }
+  }
+  float v[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const int col = 16 * g + c;
+    float x = p[0][c];
+#pragma unroll
+    for (int sp = 1; sp < S; ++sp) x = x + p[sp][c];
+    x = x + (bias != nullptr && col < E ? bias[col] : 0.0f);
+    v[c] = col < E ? x : -__builtin_huge_valf();
+  }
+  if (logits != nullptr && live) {
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+      if (16 * g + c < E) logits[(size_t)row * E + 16 * g + c] = v[c];
+  }
+  float sel_v[kMaxTopk];
+  int sel_i[kMaxTopk];
+  uint32_t taken = 0;
+#pragma unroll
+  for (int j = 0; j < kMaxTopk; ++j) {
+    if (j < k) {
+      float lv = -__builtin_huge_valf();
+      int li = 0x7fffffff;
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const int col = 16 * g + c;
+        if (!((taken >> c) & 1u) && better(v[c], col, lv, li)) {
+          lv = v[c];
+          li = col;
+        }
+      }
+      best_dpp<0x111, 0xf>(lv, li);  // row_shr:1
+      best_dpp<0x112, 0xf>(lv, li);  // row_shr:2
+      best_dpp<0x114, 0xf>(lv, li);  // row_shr:4
+      best_dpp<0x118, 0xf>(lv, li);  // row_shr:8: lane 15 of each row holds the row's best
+      float rv[4];
+      int ri[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        rv[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lv), 16 * q + 15));
+        ri[q] = __builtin_amdgcn_readlane(li, 16 * q + 15);
+      }
+      const int r4 = lane >> 4;
+      lv = r4 == 0 ? rv[0] : (r4 == 1 ? rv[1] : (r4 == 2 ? rv[2] : rv[3]));
+      li = r4 == 0 ? ri[0] : (r4 == 1 ? ri[1] : (r4 == 2 ? ri[2] : ri[3]));
+      sel_v[j] = lv;
+      sel_i[j] = li;
+      if ((li >> 4) == g) taken |= 1u << (li & 15);
+    }
+  }
+  if (live) write_topk(sel_v, sel_i, g, k, row, ids, wts);
+}
+
 template <int NV>
 static void launch_topk_reduce(const float* part, int S, int T, int E, int EP, int k, const float* bias,
                                float* logits, int32_t* ids, float* wts, dim3 grid, hipStream_t s) {
+  if (NV == 4 && EP == 256) {
+    // 16 lanes per token: 16 tokens per 256-thread block
+    const dim3 g16((unsigned)((T + 15) / 16));
+#define MOE_TOPK_REDUCE16(N)                                                                           \
+  case N:                                                                                              \
+    gate_topk_reduce16_kernel<N><<<g16, 256, 0, s>>>(part, T, E, k, bias, logits, ids, wts); \
+    return;
+    switch (S) {
+      MOE_TOPK_REDUCE16(1)
+      MOE_TOPK_REDUCE16(2)
+      MOE_TOPK_REDUCE16(3)
+      MOE_TOPK_REDUCE16(4)
+      MOE_TOPK_REDUCE16(5)
+      MOE_TOPK_REDUCE16(6)
+      MOE_TOPK_REDUCE16(7)
+      MOE_TOPK_REDUCE16(8)
+      default:
+        return;
+    }
+#undef MOE_TOPK_REDUCE16
+  }
 #define MOE_TOPK_REDUCE(N)                                                                               \
   case N:                                                                                                \
     gate_topk_reduce_kernel<NV, N><<<grid, 256, 0, s>>>(part, T, E, EP, k, bias, logits, ids, wts); \
