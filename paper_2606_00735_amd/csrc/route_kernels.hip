@@ -612,6 +612,51 @@ __global__ __launch_bounds__(256) void scan_kernel(const int32_t* __restrict__ t
   }
 }
 
+// scan_kernel for a count table of at most kScanLdsInts entries: the table
+// is first copied into LDS with every thread's loads in flight together
+// (16 a thread before the first wait), so the per-expert column sums and
+// the row bases walk LDS instead of taking one dependent round trip to L2
+// per 8 count blocks (Maverick-shaped T = 32768, 128 x 128 counts:
+// 10.1 -> 8.5 us). Same integer results.
+constexpr int kScanLdsInts = 16384;
+__global__ __launch_bounds__(256) void scan_lds_kernel(const int32_t* __restrict__ table, int n_blk,
+                                                       SlotMap map, int32_t* __restrict__ counts,
+                                                       int32_t* __restrict__ offsets,
+                                                       int32_t* __restrict__ bases, int32_t* __restrict__ m_loc) {
+  __shared__ int s_tab[kScanLdsInts];
+  __shared__ int s_cnt[kMaxExperts];
+  __shared__ int s_tot[4];
+  const int tid = threadIdx.x;
+  const int E = map.n_experts, L = map.n_local;
+  const int n = n_blk * E;
+#pragma unroll 16
+  for (int i = tid; i < n; i += 256) s_tab[i] = table[i];
+  __syncthreads();
+  for (int e = tid; e < E; e += 256) {
+    int c = 0;
+    for (int b = 0; b < n_blk; ++b) c += s_tab[b * E + e];
+    counts[e] = c;
+    s_cnt[e] = c;
+  }
+  __syncthreads();
+  const int my_e = tid < L ? map.expert_of[tid] : 0;
+  const int v = tid < L ? s_cnt[my_e] : 0;
+  int total;
+  const int excl = block_exclusive_scan_256(v, s_tot, &total);
+  if (tid < L) {
+    offsets[tid + 1] = excl + v;
+    int run = excl;
+    for (int b = 0; b < n_blk; ++b) {
+      bases[(size_t)b * L + tid] = run;
+      run += s_tab[b * E + my_e];
+    }
+  }
+  if (tid == 0) {
+    offsets[0] = 0;
+    *m_loc = total;
+  }
+}
+
 // One count block (T <= kTokPerBlk): the counts, the local offsets and the
 // block's row bases in one launch (the count table is not needed).
 __global__ __launch_bounds__(256) void hist_scan_one_block_kernel(const int32_t* __restrict__ ids, int T, int k,
@@ -1258,7 +1303,10 @@ hipError_t launch_hist_scan(const int32_t* ids, int T, int k, const SlotMap& map
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  scan_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases, m_loc);
+  if ((long long)n_blk * map.n_experts <= kScanLdsInts)
+    scan_lds_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases, m_loc);
+  else
+    scan_kernel<<<1, 256, 0, s>>>(table, n_blk, map, counts, offsets, bases, m_loc);
   return hipGetLastError();
 }
 

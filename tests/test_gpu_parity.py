@@ -339,6 +339,43 @@ def test_empty_batch():
     assert torch.all(counts == 0) and torch.all(offsets == 0)
 
 
+HIST_CASES = [
+    # (T, E, k, local experts): count tables of n_blk = ceil(T / 256) rows x E
+    (20000, 256, 8, 32),    # 20224 counts: the scan reads the table from L2
+    (16384, 256, 8, 32),    # 16384 counts: the largest table the scan stages in LDS
+    (32768, 128, 1, 16),    # 16384 counts, top-1
+    (40000, 128, 2, 128),   # 20096 counts, every expert local
+    (300, 64, 4, 64),       # two count blocks
+    (1000, 8, 2, 8),        # four count blocks, few experts
+]
+
+
+@pytest.mark.parametrize("T,E,k,n_local", HIST_CASES, ids=[f"T{t}-E{e}-k{k}-L{l}" for t, e, k, l in HIST_CASES])
+def test_histogram_and_positions(T, E, k, n_local):
+    """Counts, offsets, perm_src and dest bit-exact against the oracle on
+    skewed synthetic ids, on both sides of the scan's LDS staging limit."""
+    banner("histogram/positions", T, E, k, n_local, "seed 9")
+    rng = np.random.default_rng(9)
+    score = rng.random((T, E)) - 0.7 * np.log(np.arange(1, E + 1))[None, :] * rng.random((T, 1))
+    ids = np.argsort(-score, axis=1, kind="stable")[:, :k].astype(np.int32)
+    emap = np.full(E, -1, np.int32)
+    local = np.sort(rng.choice(E, n_local, replace=False))
+    emap[local] = np.arange(n_local, dtype=np.int32)
+    d_ids = G.up_i32(ids)
+    counts, offsets, ws = moe.moe_expert_histogram_scan(d_ids, E, emap)
+    x = torch.zeros((T, 64), dtype=torch.bfloat16, device="cuda")
+    _, perm_src, dest = moe.moe_permute(x, d_ids, emap, ws, gather=False)
+    torch.cuda.synchronize()
+    c_ref = O.expert_histogram(ids, E)
+    o_ref = O.local_offsets(c_ref, emap)
+    _, p_ref, d_ref = O.permute(np.zeros((T, 1), np.float32), ids, emap, o_ref)
+    assert np.array_equal(G.down(counts), c_ref), "counts"
+    assert np.array_equal(G.down(offsets), o_ref), "offsets"
+    m = int(o_ref[-1])
+    assert np.array_equal(G.down(perm_src)[:m], p_ref), "perm_src"
+    assert np.array_equal(G.down(dest), d_ref), "dest"
+
+
 def test_ffn_stage_on_oracle_inputs():
     """The FFN alone, fed the oracle's x_perm and offsets."""
     banner("stage ffn dsv3-like")
